@@ -1,0 +1,217 @@
+"""Seeded synthetic prefill workloads.
+
+Every array is drawn from ``numpy.random.Generator(PCG64(SeedSequence([SEED_ROOT, cfg_id, layer,
+stream, extra])))`` so that any (workload, layer, stream) can be regenerated on its own.  Streams:
+
+* ``STREAM_ROUTER``  router weight of the layer, N(0, 0.02^2), shape E x H;
+* ``STREAM_BIAS``    per-expert selection bias, N(0, 0.01^2) (sigmoid-scored workloads only);
+* ``STREAM_CLUSTER`` token -> cluster draw, shared by every layer of a workload (layer slot 0);
+* ``STREAM_NOISE``   per-layer hidden-state noise N(0, 1);
+* ``STREAM_RESID``   per-layer residual update N(0, sigma^2) that turns h_{l-1} into the target
+  router input H_l.
+
+The hidden state entering layer l is ``h = 3 * w_l[z_t] + N(0, 1)`` for token cluster ``z_t``, so a
+token's own cluster expert gets a large logit and the cluster frequencies (truncated Zipf) become the
+routing skew the planner has to fight.  Floating-point draws are made in float32 and, for bfloat16
+workloads, stored as bfloat16 bit patterns by round-to-nearest-even.
+
+The module contains no part of the predictor (no logits, scores, selections or counts) and no part of
+the planner.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+SEED_ROOT = 260814205
+STREAM_ROUTER, STREAM_BIAS, STREAM_CLUSTER, STREAM_NOISE, STREAM_RESID = range(5)
+
+# Token rows are generated in fixed chunks so that a workload's bytes do not depend on how the caller
+# slices it, and so that the 65536 x 7168 sweep layers never need a full float32 copy in memory.
+_CHUNK = 2048
+
+
+def rng(cfg_id: int, layer: int, stream: int, extra: int = 0) -> np.random.Generator:
+    """Independent generator for one (workload, layer, stream[, extra]) slot."""
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+        [SEED_ROOT, int(cfg_id), int(layer), int(stream), int(extra)])))
+
+
+def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
+    """Round finite float32 values to bfloat16 (round-to-nearest, ties to even); return uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("bf16_bits_from_f32: inputs must be finite")
+    u = x.view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    return ((u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)).astype(np.uint16)
+
+
+def truncated_zipf_probs(s: float, K: int) -> np.ndarray:
+    """p_i proportional to i^-s for i = 1..K (cluster i-1); defined for any s >= 0."""
+    i = np.arange(1, K + 1, dtype=np.float64)
+    p = i ** (-float(s))
+    return p / p.sum()
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """Shape, routing rule, placement and input recipe of one synthetic prefill workload."""
+
+    name: str
+    cfg_id: int
+    T: int
+    H: int
+    E: int
+    k: int
+    dtype: str                 # "bf16" | "f32": storage and MFMA input type of hidden and router
+    kind: str                  # "softmax" | "sigmoid"
+    n_group: int = 1           # expert groups for group-limited selection (1 = plain top-k)
+    topk_group: int = 1        # groups kept per token
+    group_topn: int = 1        # group score = sum of the group's top-n scores
+    select_bias: bool = False  # per-expert bias added to the sigmoid score (selection only)
+    R: int = 8                 # placement ranks
+    S: int = 2                 # expert slots per rank
+    budget: int = 1            # swap cap per layer
+    sigma: float = 0.3         # residual-update std between h_{l-1} and H_l
+    zipf_s: Tuple[float, ...] = (1.2,)   # one exponent, or one per task for a task mixture
+    n_clusters: int = 16
+    layers: int = 1
+    budgets: Tuple[int, ...] = ()        # swap caps reported by the multi-task sweep
+
+    @property
+    def experts_per_rank(self) -> int:
+        return self.E // self.R
+
+    @property
+    def tasks(self) -> int:
+        return len(self.zipf_s)
+
+    def with_T(self, T: int) -> "Workload":
+        return dataclasses.replace(self, T=int(T))
+
+    def input_bytes(self) -> int:
+        b = 2 if self.dtype == "bf16" else 4
+        return (self.T * self.H + self.E * self.H) * b
+
+
+CONFIGS = {
+    "tiny": Workload("tiny", 0, T=512, H=1024, E=16, k=2, dtype="f32", kind="softmax",
+                     R=8, S=2, budget=2, sigma=0.3, zipf_s=(1.2,), n_clusters=16),
+    "mixtral": Workload("mixtral", 1, T=8192, H=4096, E=8, k=2, dtype="bf16", kind="softmax",
+                        R=8, S=2, budget=1, sigma=0.3, zipf_s=(1.2,), n_clusters=8),
+    "qwen3": Workload("qwen3", 2, T=16384, H=2048, E=128, k=8, dtype="bf16", kind="softmax",
+                      R=32, S=4, budget=6, sigma=0.2, zipf_s=(1.0,), n_clusters=128, layers=48),
+    "dsv3": Workload("dsv3", 3, T=32768, H=7168, E=256, k=8, dtype="bf16", kind="sigmoid",
+                     n_group=8, topk_group=4, group_topn=2, select_bias=True,
+                     R=32, S=8, budget=8, sigma=0.25, zipf_s=(1.1,), n_clusters=256),
+}
+
+
+def sweep_workload(T: int) -> Workload:
+    """Multi-task skew sweep: DeepSeek-V3 shapes, 4 tasks with Zipf exponents 0.8..1.6 over
+    independently permuted clusters, Dirichlet(1) mixing, 58 layers, caps {0, 4, 8, 16}."""
+    base = CONFIGS["dsv3"]
+    return dataclasses.replace(base, name=f"sweep-T{T}", cfg_id=4, T=int(T), layers=58,
+                               zipf_s=tuple(float(s) for s in np.linspace(0.8, 1.6, 4)),
+                               budgets=(0, 4, 8, 16), budget=8)
+
+
+SWEEP_T = (4096, 16384, 65536)
+
+
+def contiguous_placement(E: int, R: int, S: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Rank r holds experts r*epr .. r*epr+epr-1 (epr = E // R) in its first slots; the remaining
+    S - epr slots of each rank are empty (-1).  Returns (slot table R x S, expert -> rank)."""
+    if E % R != 0:
+        raise ValueError("contiguous_placement: E must be a multiple of R")
+    epr = E // R
+    if epr > S:
+        raise ValueError("contiguous_placement: more experts per rank than slots")
+    slots = np.full((R, S), -1, dtype=np.int32)
+    for r in range(R):
+        slots[r, :epr] = np.arange(r * epr, (r + 1) * epr, dtype=np.int32)
+    e2r = (np.arange(E, dtype=np.int32) // epr).astype(np.int32)
+    return slots, e2r
+
+
+@dataclasses.dataclass
+class LayerInputs:
+    """One layer's inputs.  ``x`` / ``h_target`` / ``w`` hold bf16 bit patterns (uint16) for bf16
+    workloads and float32 values for f32 workloads."""
+
+    x: np.ndarray                    # T x H: residual hidden state h_{l-1}
+    w: np.ndarray                    # E x H: router weight of layer l (row e = expert e)
+    select_bias: Optional[np.ndarray]  # E float32 or None
+    logit_bias: Optional[np.ndarray]   # E float32 or None (the b of the linear router)
+    h_target: Optional[np.ndarray]   # T x H: the target router input H_l, or None
+    clusters: np.ndarray             # T int32: token cluster ids
+
+
+def _token_clusters(wl: Workload, T: int) -> np.ndarray:
+    g = rng(wl.cfg_id, 0, STREAM_CLUSTER, extra=T)
+    K = wl.n_clusters
+    if wl.tasks == 1:
+        return g.choice(K, size=T, p=truncated_zipf_probs(wl.zipf_s[0], K)).astype(np.int32)
+    perms = [g.permutation(K) for _ in range(wl.tasks)]
+    mix = g.dirichlet(np.ones(wl.tasks))
+    task = g.choice(wl.tasks, size=T, p=mix)
+    out = np.empty(T, dtype=np.int32)
+    for j in range(wl.tasks):
+        sel = np.nonzero(task == j)[0]
+        ranks = g.choice(K, size=sel.size, p=truncated_zipf_probs(wl.zipf_s[j], K))
+        out[sel] = perms[j][ranks]
+    return out
+
+
+def _store(wl: Workload, a: np.ndarray) -> np.ndarray:
+    return bf16_bits_from_f32(a) if wl.dtype == "bf16" else np.ascontiguousarray(a, np.float32)
+
+
+def make_layer(wl: Workload, layer: int = 0, with_target: bool = False,
+               rows: Optional[Sequence[int]] = None) -> LayerInputs:
+    """Generate layer ``layer`` of workload ``wl``.
+
+    ``rows`` restricts the returned hidden states to those token rows (the bytes of each row are
+    identical to the full generation); the chunked draw still visits every chunk up to the last row
+    requested, which keeps sampled rows bit-identical to a full run.
+    """
+    T, H, E = wl.T, wl.H, wl.E
+    w32 = rng(wl.cfg_id, layer, STREAM_ROUTER).normal(0.0, 0.02, size=(E, H)).astype(np.float32)
+    sb = None
+    if wl.select_bias:
+        sb = rng(wl.cfg_id, layer, STREAM_BIAS).normal(0.0, 0.01, size=E).astype(np.float32)
+    clusters = _token_clusters(wl, T)
+    centers = np.float32(3.0) * w32
+
+    want = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    last = int(want.max()) + 1 if want.size else 0
+    pos = {int(t): i for i, t in enumerate(want)} if rows is not None else None
+    store_dtype = np.uint16 if wl.dtype == "bf16" else np.float32
+    x_out = np.empty((want.size, H), dtype=store_dtype)
+    h_out = np.empty((want.size, H), dtype=store_dtype) if with_target else None
+    g_noise = rng(wl.cfg_id, layer, STREAM_NOISE)
+    g_res = rng(wl.cfg_id, layer, STREAM_RESID)
+    for c0 in range(0, last, _CHUNK):
+        c1 = min(T, c0 + _CHUNK)
+        h = centers[clusters[c0:c1]] + g_noise.standard_normal((c1 - c0, H), dtype=np.float32)
+        if with_target:
+            upd = g_res.standard_normal((c1 - c0, H), dtype=np.float32)
+            # sigma = 0 must give H_l identical to h_{l-1} bit for bit (no -0.0 -> +0.0 flips)
+            ht = h.copy() if wl.sigma == 0 else h + np.float32(wl.sigma) * upd
+        if pos is None:
+            x_out[c0:c1] = _store(wl, h)
+            if with_target:
+                h_out[c0:c1] = _store(wl, ht)
+        else:
+            idx = [t for t in range(c0, c1) if t in pos]
+            if idx:
+                loc = np.array(idx) - c0
+                dst = [pos[t] for t in idx]
+                x_out[dst] = _store(wl, h[loc])
+                if with_target:
+                    h_out[dst] = _store(wl, ht[loc])
+    return LayerInputs(x=x_out, w=_store(wl, w32), select_bias=sb, logit_bias=None,
+                       h_target=h_out, clusters=clusters[want] if rows is not None else clusters)
