@@ -1,0 +1,194 @@
+"""Benchmark of the residual workload predictor + swap planner on one MI355X.
+
+A step is one pass of the whole hot path over one batch: the fused predictor kernel (router GEMM,
+scoring, top-k, histogram, rank fold, max/mean) followed by the device swap planner, back to back on
+one stream.  The workload is the DeepSeek-V3-shaped prefill batch: T=32768 tokens, H=7168, E=256
+routed experts, sigmoid scoring with a per-expert selection bias, group-limited top-8 (8 groups,
+4 kept, group score = sum of the top-2), 32 ranks x 8 slots, swap cap 8.  Inputs are seeded
+synthetic data resident in HBM before timing starts; hidden-state buffers rotate so every step reads
+its 470 MB from HBM rather than the 256 MB last-level cache.
+
+Prints one JSON line (see the fields below).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "predict_dsv3_counters.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_14205_amd", "csrc", "fb_predict.hip")
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(wl) -> int:
+    """Bytes the predictor must move once per launch: hidden states and router weight read, the
+    per-expert bias and placement read, counts / rank loads / max-mean written."""
+    elem = 2 if wl.dtype == "bf16" else 4
+    return (wl.T * wl.H + wl.E * wl.H) * elem + wl.E * 4 * 3 + wl.R * 4 + 8
+
+
+def traffic_from_profile():
+    """HBM bytes per launch measured with rocprofv3 counters, if taken on the current kernel."""
+    try:
+        with open(PROFILE_COUNTERS) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, li, e2r, slots, target_s: float):
+    """The CPU oracle, as it stands, on a bounded prefix of the same workload."""
+    import oracle.planner as OPL
+    import oracle.predictor as OPR
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(int(i.get("num_threads", 1)) for i in threadpool_info()) if threadpool_info() else 1
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        cores = os.cpu_count() or 1
+
+    def run(n):
+        t0 = time.perf_counter()
+        out = OPR.predict_load(li.x[:n], li.w, wl.dtype, wl.k, wl.kind, e2r, wl.R,
+                               select_bias=li.select_bias, n_group=wl.n_group,
+                               topk_group=wl.topk_group, group_topn=wl.group_topn)
+        OPL.plan_swaps(out["counts"], slots, wl.budget)
+        return time.perf_counter() - t0
+
+    n = min(wl.T, 1024)
+    dt = run(n)
+    if dt < target_s and n < wl.T:
+        n = int(min(wl.T, max(n, math.floor(n * target_s / max(dt, 1e-6)) // 1024 * 1024)))
+        dt = run(n)
+    return {"value": n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {n} of {wl.T} tokens of the DeepSeek-V3-shaped batch, layer 0: "
+                      f"float64 router GEMM, scoring, group-limited top-8, histogram, rank fold and "
+                      f"the frontier planner (B={wl.budget}); {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the predictor shards over tokens with one 1 KB count "
+              "all-reduce, which this single-GPU build does not run; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_14205_amd as fb
+    from workloads import CONFIGS, contiguous_placement, make_layer
+
+    wl = CONFIGS["dsv3"]
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    li = make_layer(wl, 0)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    x0 = torch.from_numpy(li.x.view(np.int16)).to(dev).view(torch.bfloat16)
+    w = torch.from_numpy(li.w.view(np.int16)).to(dev).view(torch.bfloat16)
+    sb = torch.from_numpy(li.select_bias).to(dev)
+    e2r_t = torch.from_numpy(e2r).to(dev)
+    slots_t = torch.from_numpy(slots).to(dev)
+    nbuf = max(2, math.ceil(768e6 / x0.numel() / 2))
+    xs = [x0] + [x0.clone() for _ in range(nbuf - 1)]
+    scoring = fb.Scoring(wl.kind, wl.k, wl.n_group, wl.topk_group, wl.group_topn)
+    budget = fb.Budget(wl.budget)
+    pred = fb.Predictor(dev)
+    out = fb.Prediction(torch.empty(wl.E, dtype=torch.int32, device=dev),
+                        torch.empty(wl.R, dtype=torch.int32, device=dev),
+                        torch.empty(1, dtype=torch.float64, device=dev))
+    plan = fb.plan_swaps_device(out.counts, slots_t, budget)   # allocates the plan buffers once
+
+    def step(i):
+        pred.predict_load(xs[i % nbuf], w, scoring, e2r_t, wl.R, select_bias=sb, out=out)
+        fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(K):
+        ev[i][0].record(stream)
+        pred.predict_load(xs[i % nbuf], w, scoring, e2r_t, wl.R, select_bias=sb, out=out)
+        ev[i][1].record(stream)
+        fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    kern_ms = [a.elapsed_time(b) for a, b in ev]
+    avg_kernel_s = sum(kern_ms) / len(kern_ms) / 1e3
+
+    counts = out.counts.cpu().numpy()
+    host_plan = plan.to_host()
+    assert int(counts.sum()) == wl.T * wl.k, "predictor output failed its invariant"
+    assert len(host_plan.swaps) <= wl.budget
+
+    nbytes = algorithmic_bytes(wl)
+    flops = 2.0 * wl.T * wl.H * wl.E
+    achieved = nbytes / avg_kernel_s / 1e9
+    tflops = flops / avg_kernel_s / 1e12
+    result = {
+        "metric": "predicted tokens/sec (GEMM+top-k+histogram), % of HBM/MFMA roofline",
+        "value": wl.T * K / (total_ms / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "deepseek-v3-shaped prefill", "T": wl.T, "H": wl.H, "E": wl.E,
+                   "k": wl.k, "scoring": "sigmoid+bias, 8 groups keep 4 (top-2 sum)",
+                   "ranks": wl.R, "slots_per_rank": wl.S, "swap_budget": wl.budget,
+                   "step": "fb_predict_load + fb_plan_swaps_device, one stream"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic_from_profile(),
+                     "bytes_per_launch": nbytes, "kernel_ms": avg_kernel_s * 1e3,
+                     "mfma": {"achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                              "frac": tflops / PEAK_BF16_TFLOPS}},
+        "plan": {"swaps": len(host_plan.swaps),
+                 "max_mean_before": float(out.max_mean.item()),
+                 "max_mean_after": float(host_plan.rank_loads.max() * wl.R / host_plan.rank_loads.sum())},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, li, e2r, slots, args.cpu_seconds)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,213 @@
+/*
+ * freebalance.h -- C ABI of the residual workload predictor and the budgeted expert-swap planner
+ * (FreeBalance, arXiv 2608.14205) for AMD Instinct MI355X (gfx950).
+ *
+ * The predictor is the paper's early router invocation: it applies layer l's router to the residual
+ * hidden state h_{l-1} that leaves layer l-1 (Sec. "Residual Workload Prediction", Eq. 2 and the
+ * linear router of Eq. 4), applies the routed model's own top-k rule, counts how many tokens chose
+ * each expert (the predicted workload, Eq. 5) and folds the counts into per-rank loads under the
+ * expert-to-rank placement (Alg. 1, "aggregate expert workloads into rank loads"), reporting the
+ * max-to-mean rank-load ratio of Sec. "Metrics".  The planner turns counts and a slot table into a
+ * budget-feasible list of pairwise expert swaps (Sec. "Budgeted Expert-Swap Planning", Eq. 6-8 and
+ * Alg. 1); fb_swap_budget_from_cost converts the cost model of Eq. 9-10 into a swap count.
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer is owned by the caller; the library keeps no reference after a call returns
+ *     (host entry points) or after the stream reaches the call (device entry points).
+ *   - "device" pointers must be device-accessible on the current HIP device; "host" pointers are
+ *     ordinary host memory.
+ *   - Device entry points are stream-ordered and asynchronous: they validate their host-visible
+ *     arguments, enqueue kernels on `stream` (a hipStream_t passed as void*, NULL = the default
+ *     stream) and return.  They allocate no memory, never synchronise, and may run on a side stream
+ *     concurrently with other work (the paper overlaps the early pass with attention).
+ *   - Return value: FB_OK (0) or a negative FB_E* code.  No exception crosses the ABI.  Arguments are
+ *     checked before anything is enqueued, so an error return leaves every output untouched.
+ *   - Thread safety: host entry points are reentrant.  Device calls that share a workspace must be
+ *     ordered on one stream.
+ */
+#ifndef FREEBALANCE_H
+#define FREEBALANCE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FB_ABI_VERSION 1
+
+/* Status codes. */
+#define FB_OK 0
+#define FB_EINVAL (-1)        /* an argument is invalid (null pointer, bad size, bad placement...) */
+#define FB_EUNSUPPORTED (-2)  /* valid, but outside what this build implements (shape, device) */
+#define FB_EDEVICE (-3)       /* the HIP runtime reported an error (no device, launch failure) */
+#define FB_ENOSPC (-4)        /* a caller-provided buffer or workspace is too small */
+
+/* Element types of hidden states and router weights. */
+#define FB_BF16 0
+#define FB_F32 1
+
+/* Scoring rules (the routed model's "original top-k rule"). */
+#define FB_SOFTMAX 0 /* softmax over logits; selection = top-k of the logits (softmax is monotone) */
+#define FB_SIGMOID 1 /* score = sigmoid(logit) [+ select_bias]; DeepSeek-V3 style */
+
+/* Planner candidate enumeration. */
+#define FB_FRONTIER 0 /* only the most and the least loaded rank (Sec. Budgeted Expert-Swap Planning) */
+#define FB_FULL 1     /* every ordered rank pair (a, b) with L_a > L_b */
+
+/* Limits of this build. */
+#define FB_MAX_EXPERTS 256     /* E of fb_predict_load */
+#define FB_MAX_TOPK 32         /* k of fb_predict_load */
+#define FB_MAX_RANKS 1024      /* R of fb_predict_load and fb_plan_swaps_device */
+#define FB_MAX_SLOTS_TOTAL 4096 /* R * S of fb_plan_swaps_device */
+
+/* Routing rule applied to the early logits.
+ *   kind        FB_SOFTMAX or FB_SIGMOID.
+ *   k           experts per token, 1 <= k <= min(E, FB_MAX_TOPK).
+ *   n_group     1 = plain top-k.  > 1: the E experts form n_group contiguous groups of E / n_group;
+ *               each group is scored by the sum of its group_topn best scores, the topk_group best
+ *               groups are kept (ties: lower group index) and the k experts are chosen inside them.
+ *               Requires E % n_group == 0 and either (E / n_group) % 16 == 0 with (E / n_group) / 16
+ *               a power of two, or 16 % (E / n_group) == 0 (FB_EUNSUPPORTED otherwise).
+ *   topk_group  1 <= topk_group <= n_group, and k <= topk_group * E / n_group.
+ *   group_topn  1 (group max) or 2 (sum of the two best scores); ignored when n_group == 1. */
+typedef struct fb_scoring {
+  int32_t kind;
+  int32_t k;
+  int32_t n_group;
+  int32_t topk_group;
+  int32_t group_topn;
+} fb_scoring;
+
+/* Planner budget and options.
+ *   max_swaps     global swap cap B >= 0 (from the configuration or fb_swap_budget_from_cost).
+ *   per_rank_cap  0 = none; otherwise the most swaps any one rank may take part in (the paper
+ *                 enforces budgets per participant, not only as a global sum).
+ *   tau           stop when L_max - L_min <= tau (tokens, >= 0): Alg. 1's imbalance threshold.
+ *   gamma_num, gamma_den  gamma of Eq. 8 as a ratio >= 0; gamma_den == 0 selects gamma = 1 / N,
+ *                 N = sum of counts.  Benefits are reported as gamma_den * Delta (exact integers).
+ *   mode          FB_FRONTIER or FB_FULL.
+ *   layer_id      first key of the deterministic tie-break (layer, src rank, dst rank, expert ids). */
+typedef struct fb_budget {
+  int32_t max_swaps;
+  int32_t per_rank_cap;
+  int64_t tau;
+  int64_t gamma_num;
+  int64_t gamma_den;
+  int32_t mode;
+  int32_t layer_id;
+} fb_budget;
+
+/* One accepted swap, in acceptance order.  The expert in src_slot of src_rank (the more loaded
+ * rank) trades places with the expert in dst_slot of dst_rank.  expert_* is -1 for an empty slot
+ * (then the swap moves a single expert).  gain = gamma_den * (Phi(L) - Phi(L')) > 0. */
+typedef struct fb_swap {
+  int32_t src_rank;
+  int32_t dst_rank;
+  int32_t src_slot;
+  int32_t dst_slot;
+  int32_t expert_src;
+  int32_t expert_dst;
+  int64_t gain;
+} fb_swap;
+
+/* ABI version of the loaded library (FB_ABI_VERSION it was built with). */
+int fb_abi_version(void);
+
+/* Static text for a status code; never NULL. */
+const char* fb_status_string(int status);
+
+/* Bytes of device workspace fb_predict_load needs (independent of T, E and R). */
+size_t fb_predict_workspace_bytes(void);
+
+/* Prepare a predictor workspace: zero-fills it with a kernel on `stream` (no memset node, so the
+ * call may be captured into a HIP graph).  Required once before the workspace's first use; every
+ * completed fb_predict_load call leaves the workspace zeroed again.
+ *   workspace  device, >= fb_predict_workspace_bytes() bytes, 16-byte aligned. */
+int fb_predict_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
+
+/* Early router pass + top-k + predicted workload + rank fold (Eq. 2, 4, 5; Alg. 1 steps 1-2).
+ *   hidden          device, T rows of H elements, row stride ld_hidden elements (>= H), element type
+ *                   `dtype`; rows 16-byte aligned (ld_hidden * element size % 16 == 0).
+ *   T               tokens, >= 0.  T == 0 yields zero counts and *max_mean = 1.0.
+ *   H               hidden size; H % 32 == 0 for FB_BF16, H % 16 == 0 for FB_F32.
+ *   router_w        device, E x H row-major (row e is expert e's weight column of the paper's
+ *                   W in R^{H x E}), same element type, 16-byte aligned.
+ *   E               experts, 1 <= E <= FB_MAX_EXPERTS.
+ *   logit_bias      device float[E] or NULL: the b of the linear router g(X) = XW + 1b^T, added to
+ *                   the logits.
+ *   select_bias     device float[E] or NULL: FB_SIGMOID only (FB_EINVAL with FB_SOFTMAX); added to
+ *                   the sigmoid score for selection only.
+ *   scoring         host, routing rule (see fb_scoring).
+ *   expert_to_rank  device int32[E], rank id of each expert in [0, R).  An entry outside [0, R) is
+ *                   a precondition violation: the kernel skips that expert in the fold and writes
+ *                   *max_mean = -1.0 instead of the ratio.
+ *   R               ranks, 1 <= R <= FB_MAX_RANKS.
+ *   counts          device int32[E] out: n^_e, tokens whose predicted top-k contains e.
+ *   rank_loads      device int32[R] out: L_r = sum of counts of experts placed on r.
+ *   max_mean        device double out: max_r L_r / (sum_r L_r / R), 1.0 if every load is 0.
+ *   workspace       device, fb_predict_workspace_bytes() bytes, prepared by
+ *                   fb_predict_workspace_init; must not be used by an overlapping call.
+ *   topk_idx        device int32[T * k] out or NULL: the selected experts of each token in
+ *                   descending score order (lower index first on equal scores).
+ *   logits          device float[T * E] out or NULL: the early logits (incl. logit_bias).
+ *   stream          hipStream_t as void*, or NULL.
+ * Scores are compared in float32; ties in score go to the lower expert index.  Selection does not
+ * depend on whether topk_idx / logits are requested. */
+int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
+                    const void* router_w, int32_t E, const float* logit_bias,
+                    const float* select_bias, const fb_scoring* scoring,
+                    const int32_t* expert_to_rank, int32_t R, int32_t* counts,
+                    int32_t* rank_loads, double* max_mean, void* workspace,
+                    size_t workspace_bytes, int32_t* topk_idx, float* logits, void* stream);
+
+/* Budgeted greedy expert-swap planner on the host (Sec. Budgeted Expert-Swap Planning, Eq. 6-8,
+ * Alg. 1).  Pure and deterministic: identical inputs give a byte-identical plan.
+ *   counts            host int32[E] (>= 0): the predicted per-expert workload, not rank loads.
+ *   E                 experts, >= 1.
+ *   slot_expert       host int32[R * S] row-major: expert in slot s of rank r, -1 = empty slot.
+ *                     Every expert 0..E-1 must appear exactly once (FB_EINVAL otherwise).
+ *   R, S              ranks (>= 1) and slots per rank (>= 1).
+ *   budget            host, see fb_budget.
+ *   swaps             host fb_swap[swaps_cap] out; swaps_cap >= budget->max_swaps (FB_ENOSPC).
+ *   n_swaps           host out: number of swaps written.
+ *   new_slot_expert   host int32[R * S] out, may be NULL: slot table after the plan.
+ *   new_expert_to_rank host int32[E] out, may be NULL.
+ *   new_rank_loads    host int64[R] out, may be NULL: predicted loads after the plan.
+ * An empty plan (B = 0, no positive-benefit swap, R = 1, all counts zero) retains the placement. */
+int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
+                  int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t swaps_cap,
+                  int32_t* n_swaps, int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                  int64_t* new_rank_loads);
+
+/* The same planner as one stream-ordered single-workgroup kernel, so that prediction and planning
+ * run back to back on the device with no host round trip.  Produces exactly the plan of
+ * fb_plan_swaps.  Limits: R <= FB_MAX_RANKS, R * S <= FB_MAX_SLOTS_TOTAL, E <= R * S.
+ *   counts, slot_expert   device inputs as in fb_plan_swaps.
+ *   budget                host struct, read during the call.
+ *   swaps                 device fb_swap[budget->max_swaps] out.
+ *   n_swaps               device int32 out.
+ *   new_slot_expert       device int32[R * S] out (required).
+ *   new_expert_to_rank    device int32[E] out (required).
+ *   new_rank_loads        device int64[R] out (required).
+ *   status                device int32 out: FB_OK, or FB_EINVAL if the slot table is invalid or a
+ *                         count is negative (then the plan is empty and the placement unchanged). */
+int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
+                         int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
+                         int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                         int64_t* new_rank_loads, int32_t* status, void* stream);
+
+/* Swap cap from the cost model: with a uniform expert size S_e and one link type every swap costs
+ * C = alpha + 2 * S_e / beta (Eq. 9) and the window is B_l = max(0, t_attn - delta) (Eq. 10); the
+ * result is the largest n with n * C <= B_l.  Times in microseconds, beta in bytes per microsecond.
+ * Returns the count (>= 0), or FB_EINVAL for beta <= 0, alpha < 0, expert_bytes < 0, a
+ * non-positive cost or non-finite inputs. */
+int64_t fb_swap_budget_from_cost(double t_attn_us, double delta_us, double alpha_us,
+                                 double beta_bytes_per_us, int64_t expert_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FREEBALANCE_H */

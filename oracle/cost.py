@@ -10,6 +10,7 @@ bandwidth in bytes per microsecond.
 from __future__ import annotations
 
 import math
+from fractions import Fraction
 
 
 def swap_cost_us(alpha_us: float, beta_bytes_per_us: float, bytes_a: int, bytes_b: int) -> float:
@@ -30,4 +31,8 @@ def swap_budget(t_attn_us: float, delta_us: float, alpha_us: float, beta_bytes_p
     c = swap_cost_us(alpha_us, beta_bytes_per_us, expert_bytes, expert_bytes)
     if c <= 0:
         raise ValueError("swap cost must be positive")
-    return int(math.floor(window_us(t_attn_us, delta_us) / c))
+    for v in (t_attn_us, delta_us, alpha_us, beta_bytes_per_us):
+        if not math.isfinite(v):
+            raise ValueError("non-finite cost-model input")
+    # largest n with n * C <= B_l, decided exactly on the two (double) quantities
+    return int(math.floor(Fraction(window_us(t_attn_us, delta_us)) / Fraction(c)))

@@ -1,0 +1,19 @@
+"""MI355X-native residual workload predictor and budgeted expert-swap planner (FreeBalance).
+
+The computation lives in libfreebalance.so (HIP kernels for gfx950 behind the C ABI declared in
+include/freebalance.h); this package only binds it.  The library is loaded on first use and its
+absence raises an error: nothing here computes on the CPU in its place.
+"""
+from .api import (  # noqa: F401
+    Budget,
+    DevicePlan,
+    Plan,
+    Prediction,
+    Predictor,
+    Scoring,
+    plan_swaps,
+    plan_swaps_device,
+    predict_load,
+    swap_budget_from_cost,
+)
+from ._lib import FreeBalanceError, LIB_PATH, lib  # noqa: F401

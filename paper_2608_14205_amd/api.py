@@ -1,0 +1,244 @@
+"""Python binding of libfreebalance.so over torch tensors.
+
+Argument marshalling only: every step of the predictor and the device planner runs in the library's
+HIP kernels; torch provides device memory and the current stream.  Names follow the C ABI
+(include/freebalance.h).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+from typing import List, NamedTuple, Optional, Tuple
+
+import numpy as np
+import torch
+
+from . import _lib as L
+
+SWAP_DTYPE = np.dtype([("src_rank", "<i4"), ("dst_rank", "<i4"), ("src_slot", "<i4"),
+                       ("dst_slot", "<i4"), ("expert_src", "<i4"), ("expert_dst", "<i4"),
+                       ("gain", "<i8")])
+SWAP_BYTES = SWAP_DTYPE.itemsize  # 32 == sizeof(fb_swap)
+
+
+@dataclasses.dataclass(frozen=True)
+class Scoring:
+    """The routed model's top-k rule (fb_scoring)."""
+
+    kind: str = "softmax"      # "softmax" | "sigmoid"
+    k: int = 2
+    n_group: int = 1
+    topk_group: int = 1
+    group_topn: int = 1
+
+    def to_c(self) -> L.fb_scoring:
+        kinds = {"softmax": L.FB_SOFTMAX, "sigmoid": L.FB_SIGMOID}
+        if self.kind not in kinds:
+            raise ValueError(f"unknown scoring kind {self.kind!r}")
+        return L.fb_scoring(kinds[self.kind], self.k, self.n_group, self.topk_group, self.group_topn)
+
+
+@dataclasses.dataclass(frozen=True)
+class Budget:
+    """Planner budget (fb_budget).  gamma=None selects 1/N."""
+
+    max_swaps: int
+    per_rank_cap: int = 0
+    tau: int = 0
+    gamma: Optional[Tuple[int, int]] = None
+    mode: str = "frontier"     # "frontier" | "full"
+    layer_id: int = 0
+
+    def to_c(self) -> L.fb_budget:
+        modes = {"frontier": L.FB_FRONTIER, "full": L.FB_FULL}
+        if self.mode not in modes:
+            raise ValueError(f"unknown planner mode {self.mode!r}")
+        num, den = self.gamma if self.gamma is not None else (0, 0)
+        return L.fb_budget(self.max_swaps, self.per_rank_cap, self.tau, num, den, modes[self.mode],
+                           self.layer_id)
+
+
+@dataclasses.dataclass
+class Prediction:
+    counts: torch.Tensor                 # int32 [E]
+    rank_loads: torch.Tensor             # int32 [R]
+    max_mean: torch.Tensor               # float64 [1]
+    topk: Optional[torch.Tensor] = None  # int32 [T, k]
+    logits: Optional[torch.Tensor] = None  # float32 [T, E]
+
+
+class Plan(NamedTuple):
+    swaps: List[tuple]         # (src_rank, dst_rank, src_slot, dst_slot, expert_src, expert_dst, gain)
+    slots: np.ndarray          # int32 R x S
+    expert_to_rank: np.ndarray  # int32 E
+    rank_loads: np.ndarray     # int64 R
+
+
+@dataclasses.dataclass
+class DevicePlan:
+    swaps: torch.Tensor        # uint8 [max_swaps * 32]: fb_swap records
+    n_swaps: torch.Tensor      # int32 [1]
+    slots: torch.Tensor        # int32 [R, S]
+    expert_to_rank: torch.Tensor  # int32 [E]
+    rank_loads: torch.Tensor   # int64 [R]
+    status: torch.Tensor       # int32 [1]
+
+    def to_host(self) -> Plan:
+        st = int(self.status.item())
+        L.check(st, "fb_plan_swaps_device (device status)")
+        n = int(self.n_swaps.item())
+        rec = np.frombuffer(self.swaps.cpu().numpy().tobytes(), dtype=SWAP_DTYPE)[:n]
+        return Plan([tuple(int(v) for v in r) for r in rec], self.slots.cpu().numpy(),
+                    self.expert_to_rank.cpu().numpy(), self.rank_loads.cpu().numpy())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(device: torch.device, stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return s.cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return L.FB_BF16
+    if t.dtype == torch.float32:
+        return L.FB_F32
+    raise TypeError("hidden states and router weights must be bfloat16 or float32")
+
+
+class Predictor:
+    """Holds the device workspace of fb_predict_load for one device.
+
+    Calls on one Predictor must be ordered on one stream (they share the workspace)."""
+
+    def __init__(self, device=None, stream: Optional[torch.cuda.Stream] = None):
+        dev = torch.device(device) if device is not None else torch.device("cuda")
+        if dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
+        lib = L.lib()
+        nbytes = int(lib.fb_predict_workspace_bytes())
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        with torch.cuda.device(self.device):
+            L.check(lib.fb_predict_workspace_init(self.workspace.data_ptr(), nbytes,
+                                                  _stream_handle(self.device, stream)),
+                    "fb_predict_workspace_init")
+
+    def predict_load(self, hidden: torch.Tensor, router_w: torch.Tensor, scoring: Scoring,
+                     expert_to_rank: torch.Tensor, R: int, *, logit_bias=None, select_bias=None,
+                     out: Optional[Prediction] = None, return_topk: bool = False,
+                     return_logits: bool = False,
+                     stream: Optional[torch.cuda.Stream] = None) -> Prediction:
+        if hidden.dim() != 2 or router_w.dim() != 2:
+            raise ValueError("hidden must be T x H and router_w E x H")
+        if hidden.stride(1) != 1 or not router_w.is_contiguous():
+            raise ValueError("hidden rows and router_w must be contiguous in H")
+        T, H = hidden.shape
+        E = router_w.shape[0]
+        if router_w.shape[1] != H or router_w.dtype != hidden.dtype:
+            raise ValueError("router_w must be E x H with the hidden states' dtype")
+        for t in (hidden, router_w, expert_to_rank, logit_bias, select_bias):
+            if t is not None and t.device != self.device:
+                raise ValueError("all tensors must live on the predictor's device")
+        if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
+            raise ValueError("expert_to_rank must be int32[E]")
+        for b in (logit_bias, select_bias):
+            if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
+                raise ValueError("biases must be contiguous float32[E]")
+        if out is None:
+            out = Prediction(torch.empty(E, dtype=torch.int32, device=self.device),
+                             torch.empty(R, dtype=torch.int32, device=self.device),
+                             torch.empty(1, dtype=torch.float64, device=self.device))
+        if return_topk and out.topk is None:
+            out.topk = torch.empty((T, scoring.k), dtype=torch.int32, device=self.device)
+        if return_logits and out.logits is None:
+            out.logits = torch.empty((T, E), dtype=torch.float32, device=self.device)
+        sc = scoring.to_c()
+        ld = hidden.stride(0) if T > 0 else H
+        with torch.cuda.device(self.device):
+            st = L.lib().fb_predict_load(
+                _ptr(hidden), T, H, ld, _dtype_code(hidden), _ptr(router_w), E, _ptr(logit_bias),
+                _ptr(select_bias), ctypes.byref(sc), _ptr(expert_to_rank), R, _ptr(out.counts),
+                _ptr(out.rank_loads), _ptr(out.max_mean), _ptr(self.workspace),
+                self.workspace.numel(), _ptr(out.topk) if return_topk else None,
+                _ptr(out.logits) if return_logits else None, _stream_handle(self.device, stream))
+        L.check(st, "fb_predict_load")
+        return out
+
+
+_default_predictors = {}
+
+
+def predict_load(hidden: torch.Tensor, router_w: torch.Tensor, scoring: Scoring,
+                 expert_to_rank: torch.Tensor, R: int, **kw) -> Prediction:
+    """fb_predict_load on the current stream with a per-device default workspace."""
+    dev = hidden.device
+    key = (dev.index if dev.index is not None else torch.cuda.current_device())
+    pred = _default_predictors.get(key)
+    if pred is None:
+        pred = _default_predictors[key] = Predictor(torch.device("cuda", key))
+    return pred.predict_load(hidden, router_w, scoring, expert_to_rank, R, **kw)
+
+
+def plan_swaps(counts, slots, budget: Budget) -> Plan:
+    """fb_plan_swaps (host planner) on host arrays."""
+    c = np.ascontiguousarray(np.asarray(counts), dtype=np.int32)
+    sl = np.ascontiguousarray(np.asarray(slots), dtype=np.int32)
+    if sl.ndim != 2:
+        raise ValueError("slots must be R x S")
+    R, S = sl.shape
+    E = c.size
+    bg = budget.to_c()
+    cap = max(budget.max_swaps, 1)
+    swaps = (L.fb_swap * cap)()
+    n = ctypes.c_int32(0)
+    new_slots = np.empty((R, S), np.int32)
+    new_e2r = np.empty(E, np.int32)
+    new_L = np.empty(R, np.int64)
+    st = L.lib().fb_plan_swaps(c.ctypes.data, E, sl.ctypes.data, R, S, ctypes.byref(bg),
+                               ctypes.addressof(swaps), cap, ctypes.addressof(n),
+                               new_slots.ctypes.data, new_e2r.ctypes.data, new_L.ctypes.data)
+    L.check(st, "fb_plan_swaps")
+    out = [(s.src_rank, s.dst_rank, s.src_slot, s.dst_slot, s.expert_src, s.expert_dst, s.gain)
+           for s in swaps[:n.value]]
+    return Plan(out, new_slots, new_e2r, new_L)
+
+
+def plan_swaps_device(counts: torch.Tensor, slots: torch.Tensor, budget: Budget,
+                      out: Optional[DevicePlan] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> DevicePlan:
+    """fb_plan_swaps_device: the planner as a stream-ordered kernel on device tensors."""
+    if counts.dtype != torch.int32 or slots.dtype != torch.int32 or slots.dim() != 2:
+        raise ValueError("counts must be int32[E] and slots int32[R, S]")
+    if not (counts.is_contiguous() and slots.is_contiguous()):
+        raise ValueError("counts and slots must be contiguous")
+    dev = counts.device
+    R, S = slots.shape
+    E = counts.numel()
+    if out is None:
+        out = DevicePlan(torch.empty(max(budget.max_swaps, 1) * SWAP_BYTES, dtype=torch.uint8, device=dev),
+                         torch.empty(1, dtype=torch.int32, device=dev),
+                         torch.empty((R, S), dtype=torch.int32, device=dev),
+                         torch.empty(E, dtype=torch.int32, device=dev),
+                         torch.empty(R, dtype=torch.int64, device=dev),
+                         torch.empty(1, dtype=torch.int32, device=dev))
+    bg = budget.to_c()
+    with torch.cuda.device(dev):
+        st = L.lib().fb_plan_swaps_device(
+            counts.data_ptr(), E, slots.data_ptr(), R, S, ctypes.byref(bg), out.swaps.data_ptr(),
+            out.n_swaps.data_ptr(), out.slots.data_ptr(), out.expert_to_rank.data_ptr(),
+            out.rank_loads.data_ptr(), out.status.data_ptr(), _stream_handle(dev, stream))
+    L.check(st, "fb_plan_swaps_device")
+    return out
+
+
+def swap_budget_from_cost(t_attn_us: float, delta_us: float, alpha_us: float,
+                          beta_bytes_per_us: float, expert_bytes: int) -> int:
+    """fb_swap_budget_from_cost (Eq. 9-10 as a swap count)."""
+    n = int(L.lib().fb_swap_budget_from_cost(t_attn_us, delta_us, alpha_us, beta_bytes_per_us,
+                                             int(expert_bytes)))
+    L.check(n if n < 0 else L.FB_OK, "fb_swap_budget_from_cost")
+    return n

@@ -1,0 +1,175 @@
+// C ABI entry points of libfreebalance.so: argument validation, device check and dispatch to the
+// HIP launchers.  Validation happens before any HIP call, so invalid arguments are reported on a
+// machine without a GPU as well.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+
+#include "fb_internal.h"
+
+namespace fb {
+
+int check_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+    (void)hipGetLastError();
+    return FB_EDEVICE;
+  }
+  static std::atomic<int> cache[64];  // 0 unknown, 1 gfx950, 2 other
+  if (dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c == 1) return FB_OK;
+    if (c == 2) return FB_EUNSUPPORTED;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return FB_EDEVICE;
+  }
+  const bool ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+  if (dev < 64) cache[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+  return ok ? FB_OK : FB_EUNSUPPORTED;
+}
+
+}  // namespace fb
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+// Host-side checks of the routing rule; see fb_scoring in freebalance.h.
+int check_scoring(const fb_scoring& s, int32_t E, const float* select_bias) {
+  if (s.kind != FB_SOFTMAX && s.kind != FB_SIGMOID) return FB_EINVAL;
+  if (s.kind == FB_SOFTMAX && select_bias) return FB_EINVAL;
+  if (s.k < 1 || s.k > E) return FB_EINVAL;
+  if (s.n_group < 1 || E % s.n_group != 0) return FB_EINVAL;
+  if (s.n_group > 1) {
+    if (s.topk_group < 1 || s.topk_group > s.n_group) return FB_EINVAL;
+    if (s.group_topn != 1 && s.group_topn != 2) return FB_EINVAL;
+    const int gsz = E / s.n_group;
+    if ((int64_t)s.k > (int64_t)s.topk_group * gsz) return FB_EINVAL;
+    if (s.group_topn > gsz) return FB_EINVAL;
+    if (s.n_group > 32) return FB_EUNSUPPORTED;
+    const bool lanes_whole = gsz % 16 == 0 && is_pow2(gsz / 16);
+    const bool within_lane = gsz < 16 && 16 % gsz == 0;
+    if (!lanes_whole && !within_lane) return FB_EUNSUPPORTED;
+  }
+  if (s.k > FB_MAX_TOPK) return FB_EUNSUPPORTED;
+  return FB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fb_abi_version(void) { return FB_ABI_VERSION; }
+
+const char* fb_status_string(int status) {
+  switch (status) {
+    case FB_OK: return "FB_OK";
+    case FB_EINVAL: return "FB_EINVAL: invalid argument";
+    case FB_EUNSUPPORTED: return "FB_EUNSUPPORTED: unsupported shape, option or device";
+    case FB_EDEVICE: return "FB_EDEVICE: HIP runtime error";
+    case FB_ENOSPC: return "FB_ENOSPC: buffer or workspace too small";
+    default: return "unknown freebalance status";
+  }
+}
+
+size_t fb_predict_workspace_bytes(void) { return fb::kWsBytes; }
+
+int fb_predict_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace || !aligned16(workspace)) return FB_EINVAL;
+  if (workspace_bytes < fb::kWsBytes) return FB_ENOSPC;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  return fb::launch_workspace_zero(workspace, fb::kWsBytes, stream);
+}
+
+int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
+                    const void* router_w, int32_t E, const float* logit_bias,
+                    const float* select_bias, const fb_scoring* scoring,
+                    const int32_t* expert_to_rank, int32_t R, int32_t* counts,
+                    int32_t* rank_loads, double* max_mean, void* workspace,
+                    size_t workspace_bytes, int32_t* topk_idx, float* logits, void* stream) {
+  if (!scoring || !router_w || !expert_to_rank || !counts || !rank_loads || !max_mean || !workspace)
+    return FB_EINVAL;
+  if (T < 0 || H < 1 || E < 1 || R < 1 || ld_hidden < H) return FB_EINVAL;
+  if (T > 0 && !hidden) return FB_EINVAL;
+  if (dtype != FB_BF16 && dtype != FB_F32) return FB_EINVAL;
+  const int elem = dtype == FB_BF16 ? 2 : 4;
+  if (E > FB_MAX_EXPERTS || R > FB_MAX_RANKS) return FB_EUNSUPPORTED;
+  if (H % (dtype == FB_BF16 ? 32 : 16) != 0) return FB_EUNSUPPORTED;
+  if ((ld_hidden * elem) % 16 != 0 || (hidden && !aligned16(hidden)) || !aligned16(router_w))
+    return FB_EUNSUPPORTED;
+  // 32-bit buffer offsets: one 128-row tile of hidden states and the whole router weight
+  if (ld_hidden * elem * 128 >= ((int64_t)1 << 31) || (int64_t)E * H * elem >= ((int64_t)1 << 31))
+    return FB_EUNSUPPORTED;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return FB_EINVAL;
+  if (workspace_bytes < fb::kWsBytes) return FB_ENOSPC;
+  const int sc = check_scoring(*scoring, E, select_bias);
+  if (sc != FB_OK) return sc;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+
+  fb::PredictLaunch a;
+  a.hidden = hidden;
+  a.T = T;
+  a.H = H;
+  a.ld_hidden = ld_hidden;
+  a.dtype = dtype;
+  a.router_w = router_w;
+  a.E = E;
+  a.logit_bias = logit_bias;
+  a.select_bias = select_bias;
+  a.scoring = *scoring;
+  if (a.scoring.n_group == 1) { a.scoring.topk_group = 1; a.scoring.group_topn = 1; }
+  a.expert_to_rank = expert_to_rank;
+  a.R = R;
+  a.counts = counts;
+  a.rank_loads = rank_loads;
+  a.max_mean = max_mean;
+  a.workspace = workspace;
+  a.topk_idx = topk_idx;
+  a.logits = logits;
+  a.stream = stream;
+  return fb::launch_predict(a);
+}
+
+int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
+                         int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
+                         int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                         int64_t* new_rank_loads, int32_t* status, void* stream) {
+  if (!counts || !slot_expert || !budget || !n_swaps || !new_slot_expert || !new_expert_to_rank ||
+      !new_rank_loads || !status)
+    return FB_EINVAL;
+  if (E < 1 || R < 1 || S < 1) return FB_EINVAL;
+  if (R > FB_MAX_RANKS || (int64_t)R * S > FB_MAX_SLOTS_TOTAL) return FB_EUNSUPPORTED;
+  if (E > R * S) return FB_EINVAL;
+  const fb_budget bg = *budget;
+  if (bg.max_swaps < 0 || bg.per_rank_cap < 0 || bg.tau < 0 || bg.gamma_num < 0 || bg.gamma_den < 0)
+    return FB_EINVAL;
+  if (bg.mode != FB_FRONTIER && bg.mode != FB_FULL) return FB_EINVAL;
+  if (bg.max_swaps > 0 && !swaps) return FB_EINVAL;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  fb::PlanDeviceLaunch a;
+  a.counts = counts;
+  a.E = E;
+  a.slot_expert = slot_expert;
+  a.R = R;
+  a.S = S;
+  a.budget = bg;
+  a.swaps = swaps;
+  a.n_swaps = n_swaps;
+  a.new_slot_expert = new_slot_expert;
+  a.new_expert_to_rank = new_expert_to_rank;
+  a.new_rank_loads = new_rank_loads;
+  a.status = status;
+  a.stream = stream;
+  return fb::launch_plan_device(a);
+}
+
+}  // extern "C"

@@ -1,0 +1,63 @@
+// Internal declarations shared by the translation units of libfreebalance.so.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "freebalance.h"
+
+namespace fb {
+
+// Arguments of one fused predictor launch, validated by the ABI layer.
+struct PredictLaunch {
+  const void* hidden;
+  int64_t T;
+  int32_t H;
+  int64_t ld_hidden;  // elements
+  int32_t dtype;      // FB_BF16 | FB_F32
+  const void* router_w;
+  int32_t E;
+  const float* logit_bias;
+  const float* select_bias;
+  fb_scoring scoring;
+  const int32_t* expert_to_rank;
+  int32_t R;
+  int32_t* counts;
+  int32_t* rank_loads;
+  double* max_mean;
+  void* workspace;
+  int32_t* topk_idx;
+  float* logits;
+  void* stream;
+};
+
+// Workspace layout (device): per-expert accumulator and the completion ticket.  Every completed
+// launch leaves both at zero.
+constexpr size_t kWsAccOffset = 0;
+constexpr size_t kWsTicketOffset = 1024;
+constexpr size_t kWsBytes = 2048;
+
+int launch_predict(const PredictLaunch& a);
+int launch_workspace_zero(void* workspace, size_t bytes, void* stream);
+
+struct PlanDeviceLaunch {
+  const int32_t* counts;
+  int32_t E;
+  const int32_t* slot_expert;
+  int32_t R;
+  int32_t S;
+  fb_budget budget;
+  fb_swap* swaps;
+  int32_t* n_swaps;
+  int32_t* new_slot_expert;
+  int32_t* new_expert_to_rank;
+  int64_t* new_rank_loads;
+  int32_t* status;
+  void* stream;
+};
+int launch_plan_device(const PlanDeviceLaunch& a);
+
+// Current device must be gfx950; cached per device.  FB_OK, FB_EUNSUPPORTED or FB_EDEVICE.
+int check_device();
+
+}  // namespace fb

@@ -1,0 +1,244 @@
+"""C ABI checks that need no GPU: the library loads and exports every declared symbol, the host
+planner matches the oracle bit for bit, the cost helper matches the oracle, and argument validation
+rejects bad calls before any HIP call is made."""
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings
+from hypothesis import strategies as st
+
+import paper_2608_14205_amd as fb
+from paper_2608_14205_amd import _lib as L
+from oracle import cost as OC
+from oracle import planner as OP
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "freebalance.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fb_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    assert names == sorted(["fb_abi_version", "fb_status_string", "fb_predict_workspace_bytes",
+                            "fb_predict_workspace_init", "fb_predict_load", "fb_plan_swaps",
+                            "fb_plan_swaps_device", "fb_swap_budget_from_cost"])
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    assert set(L.SIGNATURES) == set(_declared_functions())
+
+
+def test_struct_layouts_match_header():
+    assert ctypes.sizeof(L.fb_scoring) == 20
+    assert ctypes.sizeof(L.fb_budget) == 40
+    assert ctypes.sizeof(L.fb_swap) == 32 == fb.api.SWAP_BYTES
+
+
+def test_version_and_status_strings():
+    lib = fb.lib()
+    assert lib.fb_abi_version() == 1
+    for code in (0, -1, -2, -3, -4):
+        assert L.status_string(code).startswith("FB_")
+    assert "unknown" in L.status_string(7)
+    assert lib.fb_predict_workspace_bytes() >= 1028
+
+
+def _host(counts, slots, **kw):
+    return fb.plan_swaps(counts, slots, fb.Budget(**kw))
+
+
+def _same(host, ref):
+    assert [tuple(s) for s in host.swaps] == [tuple(s) for s in ref.swaps]
+    assert np.array_equal(host.slots, ref.slots)
+    assert np.array_equal(host.expert_to_rank, ref.expert_to_rank)
+    assert np.array_equal(host.rank_loads, ref.rank_loads)
+
+
+def test_host_planner_hand_worked_plans(golden_dir):
+    with open(os.path.join(golden_dir, "planner_hand.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        h = _host(c["counts"], c["slots"], max_swaps=c["max_swaps"], mode=c["mode"],
+                  per_rank_cap=c.get("per_rank_cap", 0), tau=c.get("tau", 0),
+                  gamma=tuple(c["gamma"]) if "gamma" in c else None)
+        assert [list(s) for s in h.swaps] == c["swaps"], c["name"]
+        assert h.slots.tolist() == c["new_slots"], c["name"]
+        assert h.rank_loads.tolist() == c["rank_loads"], c["name"]
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.integers(1, 6), st.integers(1, 5), st.integers(0, 10 ** 9), st.integers(0, 6),
+       st.sampled_from(["frontier", "full"]), st.integers(0, 3), st.integers(0, 6),
+       st.sampled_from([None, (0, 1), (1, 7), (3, 2)]), st.integers(0, 5))
+def test_host_planner_matches_oracle(R, S, seed, B, mode, cap, tau, gamma, layer):
+    g = np.random.default_rng(seed)
+    E = int(g.integers(1, R * S + 1))
+    cells = g.permutation(R * S)[:E]
+    slots = np.full(R * S, -1, np.int32)
+    slots[cells] = np.arange(E)
+    slots = slots.reshape(R, S)
+    counts = (g.integers(0, 40, size=E) * (g.random(E) < 0.85)).astype(np.int32)
+    ref = OP.plan_swaps(counts, slots, B, gamma=gamma, tau=tau, mode=mode, per_rank_cap=cap,
+                        layer_id=layer)
+    host = _host(counts, slots, max_swaps=B, mode=mode, per_rank_cap=cap, tau=tau, gamma=gamma,
+                 layer_id=layer)
+    _same(host, ref)
+
+
+def test_host_planner_is_deterministic_and_pure():
+    g = np.random.default_rng(4)
+    slots = np.arange(256, dtype=np.int32).reshape(32, 8)
+    counts = g.integers(0, 3000, size=256).astype(np.int32)
+    before = (counts.copy(), slots.copy())
+    a = _host(counts, slots, max_swaps=16)
+    b = _host(counts, slots, max_swaps=16)
+    _same(a, b)
+    assert np.array_equal(counts, before[0]) and np.array_equal(slots, before[1])
+    assert len(a.swaps) > 0
+
+
+@pytest.mark.parametrize("bad", [
+    dict(slots=[[0, 1], [1, 3]]),   # expert placed twice
+    dict(slots=[[0, 1], [2, -1]]),  # expert missing
+    dict(slots=[[0, 1], [2, 9]]),   # id out of range
+    dict(counts=[1, -1, 1, 1]),     # negative count
+])
+def test_host_planner_rejects_bad_placement(bad):
+    counts = bad.get("counts", [1, 1, 1, 1])
+    slots = bad.get("slots", [[0, 1], [2, 3]])
+    with pytest.raises(fb.FreeBalanceError) as ei:
+        fb.plan_swaps(counts, slots, fb.Budget(1))
+    assert ei.value.status == L.FB_EINVAL
+
+
+def test_host_planner_argument_checks():
+    lib = fb.lib()
+    c = np.ones(4, np.int32)
+    sl = np.arange(4, dtype=np.int32)
+    n = ctypes.c_int32(-7)
+    sw = (L.fb_swap * 4)()
+    bg = fb.Budget(4).to_c()
+    # swaps_cap below the budget
+    assert lib.fb_plan_swaps(c.ctypes.data, 4, sl.ctypes.data, 2, 2, ctypes.byref(bg),
+                             ctypes.addressof(sw), 3, ctypes.addressof(n), None, None, None) == L.FB_ENOSPC
+    bad = fb.Budget(4, mode="full").to_c()
+    bad.mode = 5
+    assert lib.fb_plan_swaps(c.ctypes.data, 4, sl.ctypes.data, 2, 2, ctypes.byref(bad),
+                             ctypes.addressof(sw), 4, ctypes.addressof(n), None, None, None) == L.FB_EINVAL
+    neg = fb.Budget(-1).to_c()
+    assert lib.fb_plan_swaps(c.ctypes.data, 4, sl.ctypes.data, 2, 2, ctypes.byref(neg),
+                             ctypes.addressof(sw), 4, ctypes.addressof(n), None, None, None) == L.FB_EINVAL
+    assert lib.fb_plan_swaps(None, 4, sl.ctypes.data, 2, 2, ctypes.byref(bg),
+                             ctypes.addressof(sw), 4, ctypes.addressof(n), None, None, None) == L.FB_EINVAL
+    # outputs are optional; an empty plan leaves n_swaps = 0
+    zero = fb.Budget(0).to_c()
+    assert lib.fb_plan_swaps(c.ctypes.data, 4, sl.ctypes.data, 2, 2, ctypes.byref(zero),
+                             None, 0, ctypes.addressof(n), None, None, None) == L.FB_OK
+    assert n.value == 0
+
+
+def test_host_planner_overflow_guard():
+    # gamma_num * 4 N^2 beyond int64 is refused rather than wrapped
+    counts = np.full(4, 2 ** 28, np.int32)
+    with pytest.raises(fb.FreeBalanceError) as ei:
+        fb.plan_swaps(counts, [[0, 1], [2, 3]], fb.Budget(2, gamma=(2 ** 20, 1)))
+    assert ei.value.status == L.FB_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("args", [
+    (1000.0, 0.0, 10.0, 1.0, 450), (1830.0, 10.0, 10.0, 1.0, 450), (1829.0, 10.0, 10.0, 1.0, 450),
+    (36800.0, 500.0, 15.0, 153000.0, 9_000_000), (12550.0, 500.0, 15.0, 153000.0, 16_500_000),
+    (5.0, 10.0, 1.0, 1.0, 1), (0.3, 0.0, 0.1, 1.0, 0), (1e9, 0.0, 0.0, 3.0, 1),
+])
+def test_budget_helper_matches_oracle(args):
+    assert fb.swap_budget_from_cost(*args) == OC.swap_budget(*args)
+
+
+@pytest.mark.parametrize("args", [(1.0, 0.0, 1.0, 0.0, 1), (1.0, 0.0, -1.0, 1.0, 1),
+                                  (1.0, 0.0, 0.0, 1.0, 0), (float("nan"), 0.0, 1.0, 1.0, 1),
+                                  (1.0, 0.0, 1.0, 1.0, -5)])
+def test_budget_helper_rejects_invalid(args):
+    assert fb.lib().fb_swap_budget_from_cost(*args) == L.FB_EINVAL
+
+
+def _predict_call(**over):
+    """fb_predict_load with fake (never dereferenced) pointers; every case must fail validation."""
+    a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, w=0x2000, E=16, lb=None, sb=None,
+             sc=fb.Scoring("softmax", 2).to_c(), e2r=0x3000, R=4, counts=0x4000, rl=0x5000,
+             mm=0x6000, ws=0x7000, wsb=4096, topk=None, logits=None, stream=None)
+    a.update(over)
+    sc = a["sc"]
+    return fb.lib().fb_predict_load(a["hidden"], a["T"], a["H"], a["ld"], a["dtype"], a["w"], a["E"],
+                                    a["lb"], a["sb"], ctypes.byref(sc) if sc is not None else None,
+                                    a["e2r"], a["R"], a["counts"], a["rl"], a["mm"], a["ws"],
+                                    a["wsb"], a["topk"], a["logits"], a["stream"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(sc=None), L.FB_EINVAL),
+    (dict(T=-1), L.FB_EINVAL),
+    (dict(ld=32), L.FB_EINVAL),
+    (dict(hidden=None), L.FB_EINVAL),
+    (dict(dtype=7), L.FB_EINVAL),
+    (dict(E=0), L.FB_EINVAL),
+    (dict(E=300), L.FB_EUNSUPPORTED),
+    (dict(R=0), L.FB_EINVAL),
+    (dict(R=5000), L.FB_EUNSUPPORTED),
+    (dict(H=48), L.FB_EUNSUPPORTED),                     # bf16 needs H % 32 == 0
+    (dict(ld=68), L.FB_EUNSUPPORTED),                    # rows not 16-byte aligned
+    (dict(hidden=0x1008), L.FB_EUNSUPPORTED),            # base not 16-byte aligned
+    (dict(wsb=16), L.FB_ENOSPC),
+    (dict(ws=0x7004), L.FB_EINVAL),
+    (dict(sc=fb.Scoring("softmax", 0).to_c()), L.FB_EINVAL),
+    (dict(sc=fb.Scoring("softmax", 17).to_c()), L.FB_EINVAL),
+    (dict(sc=fb.Scoring("bogus", 2).to_c() if False else L.fb_scoring(9, 2, 1, 1, 1)), L.FB_EINVAL),
+    (dict(sb=0x8000), L.FB_EINVAL),                      # selection bias with softmax
+    (dict(sc=fb.Scoring("sigmoid", 2, 3, 1, 2).to_c()), L.FB_EINVAL),    # 16 % 3 != 0
+    (dict(sc=fb.Scoring("sigmoid", 9, 4, 2, 2).to_c()), L.FB_EINVAL),    # k > kept experts
+    (dict(sc=fb.Scoring("sigmoid", 2, 4, 5, 2).to_c()), L.FB_EINVAL),    # topk_group > n_group
+    (dict(sc=fb.Scoring("sigmoid", 2, 4, 2, 3).to_c()), L.FB_EINVAL),    # group_topn not 1 or 2
+    (dict(E=48, sc=fb.Scoring("sigmoid", 2, 2, 1, 2).to_c()), L.FB_EUNSUPPORTED),  # group of 24
+    (dict(E=64, sc=fb.Scoring("softmax", 33).to_c()), L.FB_EUNSUPPORTED),         # k > 32
+])
+def test_predict_validation_without_gpu(over, code):
+    assert _predict_call(**over) == code
+
+
+def test_device_planner_validation_without_gpu():
+    lib = fb.lib()
+    bg = fb.Budget(2).to_c()
+    args = [0x1000, 4, 0x2000, 2, 2, ctypes.byref(bg), 0x3000, 0x4000, 0x5000, 0x6000, 0x7000, 0x8000, None]
+    a = list(args); a[0] = None
+    assert lib.fb_plan_swaps_device(*a) == L.FB_EINVAL
+    a = list(args); a[1] = 5                    # E > R * S
+    assert lib.fb_plan_swaps_device(*a) == L.FB_EINVAL
+    a = list(args); a[3] = 2000                 # R above the device limit
+    assert lib.fb_plan_swaps_device(*a) == L.FB_EUNSUPPORTED
+    neg = fb.Budget(-3).to_c()
+    a = list(args); a[5] = ctypes.byref(neg)
+    assert lib.fb_plan_swaps_device(*a) == L.FB_EINVAL
+    a = list(args); a[6] = None                 # swaps required when max_swaps > 0
+    assert lib.fb_plan_swaps_device(*a) == L.FB_EINVAL
+
+
+def test_oracle_is_not_reachable_from_the_product_package():
+    import sys
+    pkg_dir = os.path.join(ROOT, "paper_2608_14205_amd")
+    for dirpath, _, files in os.walk(pkg_dir):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in re.findall(r"(?:import|from)\s+(\w+)", text), f
+    assert "paper_2608_14205_amd" in sys.modules

@@ -1,0 +1,98 @@
+"""The device planner (one workgroup kernel) against the host planner and the oracle, on MI355X."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_14205_amd as fb
+from oracle import planner as OP
+from workloads import CONFIGS, contiguous_placement, make_layer
+from gpu_util import run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev(counts, slots, budget):
+    c = torch.from_numpy(np.ascontiguousarray(counts, np.int32)).cuda()
+    s = torch.from_numpy(np.ascontiguousarray(slots, np.int32)).cuda()
+    return fb.plan_swaps_device(c, s, budget).to_host()
+
+
+def _same(a, b):
+    assert [tuple(x) for x in a.swaps] == [tuple(x) for x in b.swaps]
+    assert np.array_equal(a.slots, b.slots)
+    assert np.array_equal(a.expert_to_rank, b.expert_to_rank)
+    assert np.array_equal(a.rank_loads, b.rank_loads)
+
+
+def test_device_planner_random_instances():
+    print("[plan] random instances", flush=True)
+    g = np.random.default_rng(0)
+    for it in range(120):
+        R = int(g.integers(1, 9))
+        S = int(g.integers(1, 6))
+        E = int(g.integers(1, R * S + 1))
+        cells = g.permutation(R * S)[:E]
+        slots = np.full(R * S, -1, np.int32)
+        slots[cells] = np.arange(E)
+        slots = slots.reshape(R, S)
+        counts = (g.integers(0, 60, size=E) * (g.random(E) < 0.85)).astype(np.int32)
+        bg = fb.Budget(int(g.integers(0, 7)), per_rank_cap=int(g.integers(0, 3)),
+                       tau=int(g.integers(0, 5)),
+                       gamma=[None, (0, 1), (2, 5)][it % 3], mode=["frontier", "full"][it % 2])
+        host = fb.plan_swaps(counts, slots, bg)
+        dev = _dev(counts, slots, bg)
+        _same(dev, host)
+        ref = OP.plan_swaps(counts, slots, bg.max_swaps, gamma=bg.gamma, tau=bg.tau, mode=bg.mode,
+                            per_rank_cap=bg.per_rank_cap)
+        _same(dev, ref)
+
+
+@pytest.mark.parametrize("mode", ["frontier", "full"])
+def test_device_planner_on_predicted_counts(mode):
+    print(f"[plan] dsv3 counts {mode}", flush=True)
+    wl = CONFIGS["dsv3"].with_T(4096)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    li = make_layer(wl, 0)
+    gpu = run_gpu(li, wl, e2r, debug=False)
+    for B in (0, 4, 8, 16):
+        bg = fb.Budget(B, mode=mode, layer_id=3)
+        host = fb.plan_swaps(gpu["counts"], slots, bg)
+        dev = _dev(gpu["counts"], slots, bg)
+        _same(dev, host)
+        ref = OP.plan_swaps(gpu["counts"], slots, B, mode=mode, layer_id=3)
+        _same(host, ref)
+        if B > 0:
+            assert len(host.swaps) > 0
+            assert host.rank_loads.max() < gpu["rank_loads"].max()
+
+
+def test_device_planner_reports_bad_placement():
+    print("[plan] invalid slot table", flush=True)
+    slots = np.array([[0, 1], [1, 3]], np.int32)   # expert 1 twice, expert 2 missing
+    c = torch.ones(4, dtype=torch.int32, device="cuda")
+    out = fb.plan_swaps_device(c, torch.from_numpy(slots).cuda(), fb.Budget(2))
+    torch.cuda.synchronize()
+    assert int(out.status.item()) == -1 and int(out.n_swaps.item()) == 0
+
+
+def test_predict_then_plan_on_stream():
+    """The benchmark step: prediction and planning back to back on one stream, no host sync."""
+    print("[plan] predict -> plan on one stream", flush=True)
+    wl = CONFIGS["dsv3"].with_T(3000)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    li = make_layer(wl, 1)
+    from gpu_util import to_device, scoring_of
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        x, w = to_device(li.x, "bf16"), to_device(li.w, "bf16")
+        sb = torch.from_numpy(li.select_bias).cuda()
+        e2r_t = torch.from_numpy(e2r).cuda()
+        slots_t = torch.from_numpy(slots).cuda()
+        pred = fb.Predictor(stream=s)
+        out = pred.predict_load(x, w, scoring_of(wl), e2r_t, wl.R, select_bias=sb, stream=s)
+        plan = fb.plan_swaps_device(out.counts, slots_t, fb.Budget(wl.budget), stream=s)
+    s.synchronize()
+    host = fb.plan_swaps(out.counts.cpu().numpy(), slots, fb.Budget(wl.budget))
+    _same(plan.to_host(), host)
