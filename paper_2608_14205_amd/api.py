@@ -134,7 +134,7 @@ class Predictor:
                      stream: Optional[torch.cuda.Stream] = None) -> Prediction:
         if hidden.dim() != 2 or router_w.dim() != 2:
             raise ValueError("hidden must be T x H and router_w E x H")
-        if hidden.stride(1) != 1 or not router_w.is_contiguous():
+        if (hidden.numel() > 0 and hidden.stride(1) != 1) or not router_w.is_contiguous():
             raise ValueError("hidden rows and router_w must be contiguous in H")
         T, H = hidden.shape
         E = router_w.shape[0]
