@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define FB_ABI_VERSION 1
+#define FB_ABI_VERSION 2
 
 /* Status codes. */
 #define FB_OK 0
@@ -118,16 +118,40 @@ int fb_abi_version(void);
 /* Static text for a status code; never NULL. */
 const char* fb_status_string(int status);
 
-/* Bytes of device workspace fb_predict_load needs (independent of T, E and R). */
-size_t fb_predict_workspace_bytes(void);
+/* Bytes of the packed router weight fb_pack_router_weight writes for E experts of H elements of
+ * `dtype`: E rounded up to 32, 64, 128 or 256 rows times H * element size rounded up to a
+ * multiple of 128 bytes.  0 if E, H or dtype is invalid or E > FB_MAX_EXPERTS. */
+size_t fb_router_packed_bytes(int32_t E, int32_t H, int32_t dtype);
 
-/* Prepare a predictor workspace: zero-fills it with a kernel on `stream` (no memset node, so the
- * call may be captured into a HIP graph).  Required once before the workspace's first use; every
- * completed fb_predict_load call leaves the workspace zeroed again.
- *   workspace  device, >= fb_predict_workspace_bytes() bytes, 16-byte aligned. */
+/* Bytes of device workspace fb_predict_load needs: 2048 bytes of accumulators plus room for the
+ * router weight it packs on every call (fb_router_packed_bytes).  fb_predict_load_packed needs only
+ * the first 2048 bytes.  0 for invalid arguments as in fb_router_packed_bytes. */
+size_t fb_predict_workspace_bytes(int32_t E, int32_t H, int32_t dtype);
+
+/* Prepare a predictor workspace: zero-fills its first 2048 bytes with a kernel on `stream` (no
+ * memset node, so the call may be captured into a HIP graph).  Required once before the
+ * workspace's first use; every completed predictor call leaves those bytes zeroed again.
+ *   workspace  device, >= 2048 bytes, 16-byte aligned. */
 int fb_predict_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
 
-/* Early router pass + top-k + predicted workload + rank fold (Eq. 2, 4, 5; Alg. 1 steps 1-2).
+/* Rewrite a router weight into the layout the predictor kernel streams (one kernel on `stream`).
+ * The router weight is a fixed parameter of the routed model, so a caller packs it once when the
+ * model is loaded and calls fb_predict_load_packed per batch; fb_predict_load does the same packing
+ * into its workspace on every call.  Layout: for each 128-byte stage st of a row, a contiguous
+ * block of 1 KB chunks; chunk c = (w * 4 + q) * F + f holds, for lane l of 64, the 16 bytes at
+ * byte st * 128 + q * 32 + (l / 32) * 16 of row w * (EP / W) + f * 32 + (l % 32), where EP is E
+ * rounded as above, W the number of expert slices of the kernel's tile for EP (4 for EP >= 128, 2
+ * for 64, 1 for 32) and F = EP / (32 * W).  Rows >= E and bytes past H read as zero.
+ *   router_w      device, E x H row-major, element type `dtype`, 16-byte aligned.
+ *   packed        device out, >= fb_router_packed_bytes(E, H, dtype) bytes, 16-byte aligned.
+ * FB_EINVAL for null pointers, E < 1, H < 1 or a bad dtype; FB_EUNSUPPORTED for E >
+ * FB_MAX_EXPERTS, H not a multiple of 32 (FB_BF16) or 16 (FB_F32), misalignment or a packed
+ * weight of 2 GiB or more; FB_ENOSPC if packed_bytes is too small. */
+int fb_pack_router_weight(const void* router_w, int32_t E, int32_t H, int32_t dtype, void* packed,
+                          size_t packed_bytes, void* stream);
+
+/* Early router pass + top-k + predicted workload + rank fold (Eq. 2, 4, 5; Alg. 1, first two
+ * steps).  Packs router_w into the workspace (fb_pack_router_weight), then runs the fused kernel.
  *   hidden          device, T rows of H elements, row stride ld_hidden elements (>= H), element type
  *                   `dtype`; rows 16-byte aligned (ld_hidden * element size % 16 == 0).
  *   T               tokens, >= 0.  T == 0 yields zero counts and *max_mean = 1.0.
@@ -147,7 +171,7 @@ int fb_predict_workspace_init(void* workspace, size_t workspace_bytes, void* str
  *   counts          device int32[E] out: n^_e, tokens whose predicted top-k contains e.
  *   rank_loads      device int32[R] out: L_r = sum of counts of experts placed on r.
  *   max_mean        device double out: max_r L_r / (sum_r L_r / R), 1.0 if every load is 0.
- *   workspace       device, fb_predict_workspace_bytes() bytes, prepared by
+ *   workspace       device, fb_predict_workspace_bytes(E, H, dtype) bytes, prepared by
  *                   fb_predict_workspace_init; must not be used by an overlapping call.
  *   topk_idx        device int32[T * k] out or NULL: the selected experts of each token in
  *                   descending score order (lower index first on equal scores).
@@ -161,6 +185,21 @@ int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
                     const int32_t* expert_to_rank, int32_t R, int32_t* counts,
                     int32_t* rank_loads, double* max_mean, void* workspace,
                     size_t workspace_bytes, int32_t* topk_idx, float* logits, void* stream);
+
+/* fb_predict_load with a router weight packed beforehand by fb_pack_router_weight (same E, H and
+ * dtype): the per-batch call of a server that packs its routers at load time.  Results are
+ * identical to fb_predict_load's on the same inputs.
+ *   router_packed        device, as written by fb_pack_router_weight.
+ *   router_packed_bytes  its size; FB_ENOSPC if below fb_router_packed_bytes(E, H, dtype).
+ *   workspace            device, >= 2048 bytes, prepared by fb_predict_workspace_init.
+ * Every other argument, and every error, as in fb_predict_load. */
+int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                           int32_t dtype, const void* router_packed, size_t router_packed_bytes,
+                           int32_t E, const float* logit_bias, const float* select_bias,
+                           const fb_scoring* scoring, const int32_t* expert_to_rank, int32_t R,
+                           int32_t* counts, int32_t* rank_loads, double* max_mean,
+                           void* workspace, size_t workspace_bytes, int32_t* topk_idx,
+                           float* logits, void* stream);
 
 /* Budgeted greedy expert-swap planner on the host (Sec. Budgeted Expert-Swap Planning, Eq. 6-8,
  * Alg. 1).  Pure and deterministic: identical inputs give a byte-identical plan.

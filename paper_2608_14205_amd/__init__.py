@@ -7,10 +7,12 @@ absence raises an error: nothing here computes on the CPU in its place.
 from .api import (  # noqa: F401
     Budget,
     DevicePlan,
+    PackedRouter,
     Plan,
     Prediction,
     Predictor,
     Scoring,
+    pack_router_weight,
     plan_swaps,
     plan_swaps_device,
     predict_load,

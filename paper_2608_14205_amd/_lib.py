@@ -16,7 +16,7 @@ FB_OK, FB_EINVAL, FB_EUNSUPPORTED, FB_EDEVICE, FB_ENOSPC = 0, -1, -2, -3, -4
 FB_BF16, FB_F32 = 0, 1
 FB_SOFTMAX, FB_SIGMOID = 0, 1
 FB_FRONTIER, FB_FULL = 0, 1
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 
 class fb_scoring(ctypes.Structure):
@@ -49,11 +49,16 @@ _VP, _I32, _I64, _SZ, _D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctyp
 SIGNATURES = {
     "fb_abi_version": (ctypes.c_int, []),
     "fb_status_string": (ctypes.c_char_p, [ctypes.c_int]),
-    "fb_predict_workspace_bytes": (_SZ, []),
+    "fb_router_packed_bytes": (_SZ, [_I32, _I32, _I32]),
+    "fb_predict_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
     "fb_predict_workspace_init": (ctypes.c_int, [_VP, _SZ, _VP]),
     "fb_predict_load": (ctypes.c_int, [_VP, _I64, _I32, _I64, _I32, _VP, _I32, _VP, _VP,
                                        ctypes.POINTER(fb_scoring), _VP, _I32, _VP, _VP, _VP, _VP,
                                        _SZ, _VP, _VP, _VP]),
+    "fb_pack_router_weight": (ctypes.c_int, [_VP, _I32, _I32, _I32, _VP, _SZ, _VP]),
+    "fb_predict_load_packed": (ctypes.c_int, [_VP, _I64, _I32, _I64, _I32, _VP, _SZ, _I32, _VP,
+                                              _VP, ctypes.POINTER(fb_scoring), _VP, _I32, _VP,
+                                              _VP, _VP, _VP, _SZ, _VP, _VP, _VP]),
     "fb_plan_swaps": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32, ctypes.POINTER(fb_budget), _VP,
                                      _I32, _VP, _VP, _VP, _VP]),
     "fb_plan_swaps_device": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32, ctypes.POINTER(fb_budget),

@@ -109,45 +109,100 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError("hidden states and router weights must be bfloat16 or float32")
 
 
+@dataclasses.dataclass(frozen=True)
+class PackedRouter:
+    """A router weight rewritten once by fb_pack_router_weight into the predictor's streaming
+    layout (a load-time transform of a fixed parameter; see pack_router_weight)."""
+
+    data: torch.Tensor         # uint8 [fb_router_packed_bytes(E, H, dtype)]
+    E: int
+    H: int
+    dtype: torch.dtype
+
+
+def pack_router_weight(router_w: torch.Tensor,
+                       stream: Optional[torch.cuda.Stream] = None) -> PackedRouter:
+    """fb_pack_router_weight: E x H router weight -> PackedRouter on the same device."""
+    if router_w.dim() != 2 or not router_w.is_contiguous():
+        raise ValueError("router_w must be a contiguous E x H tensor")
+    E, H = router_w.shape
+    code = _dtype_code(router_w)
+    lib = L.lib()
+    nbytes = int(lib.fb_router_packed_bytes(E, H, code))
+    if nbytes == 0:
+        L.check(L.FB_EUNSUPPORTED if E > 0 and H > 0 else L.FB_EINVAL, "fb_router_packed_bytes")
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=router_w.device)
+    with torch.cuda.device(router_w.device):
+        L.check(lib.fb_pack_router_weight(_ptr(router_w), E, H, code, _ptr(packed), nbytes,
+                                          _stream_handle(router_w.device, stream)),
+                "fb_pack_router_weight")
+    return PackedRouter(packed, E, H, router_w.dtype)
+
+
 class Predictor:
     """Holds the device workspace of fb_predict_load for one device.
 
-    Calls on one Predictor must be ordered on one stream (they share the workspace)."""
+    Calls on one Predictor must be ordered on one stream (they share the workspace).  The workspace
+    grows on demand to what fb_predict_workspace_bytes asks for the largest unpacked router seen."""
 
     def __init__(self, device=None, stream: Optional[torch.cuda.Stream] = None):
         dev = torch.device(device) if device is not None else torch.device("cuda")
         if dev.index is None:
             dev = torch.device("cuda", torch.cuda.current_device())
         self.device = dev
-        lib = L.lib()
-        nbytes = int(lib.fb_predict_workspace_bytes())
-        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
-        with torch.cuda.device(self.device):
-            L.check(lib.fb_predict_workspace_init(self.workspace.data_ptr(), nbytes,
-                                                  _stream_handle(self.device, stream)),
-                    "fb_predict_workspace_init")
+        self.workspace = None
+        self._reserve(2048, stream)
 
-    def predict_load(self, hidden: torch.Tensor, router_w: torch.Tensor, scoring: Scoring,
+    def _reserve(self, nbytes: int, stream) -> None:
+        if self.workspace is not None and self.workspace.numel() >= nbytes:
+            return
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        with torch.cuda.device(self.device):
+            L.check(L.lib().fb_predict_workspace_init(ws.data_ptr(), nbytes,
+                                                      _stream_handle(self.device, stream)),
+                    "fb_predict_workspace_init")
+        self.workspace = ws
+
+    def predict_load(self, hidden: torch.Tensor, router_w, scoring: Scoring,
                      expert_to_rank: torch.Tensor, R: int, *, logit_bias=None, select_bias=None,
                      out: Optional[Prediction] = None, return_topk: bool = False,
                      return_logits: bool = False,
                      stream: Optional[torch.cuda.Stream] = None) -> Prediction:
-        if hidden.dim() != 2 or router_w.dim() != 2:
-            raise ValueError("hidden must be T x H and router_w E x H")
-        if (hidden.numel() > 0 and hidden.stride(1) != 1) or not router_w.is_contiguous():
-            raise ValueError("hidden rows and router_w must be contiguous in H")
+        """fb_predict_load (router_w an E x H tensor, packed on every call) or
+        fb_predict_load_packed (router_w a PackedRouter)."""
+        packed = isinstance(router_w, PackedRouter)
+        if hidden.dim() != 2:
+            raise ValueError("hidden must be T x H")
+        if hidden.numel() > 0 and hidden.stride(1) != 1:
+            raise ValueError("hidden rows must be contiguous in H")
         T, H = hidden.shape
-        E = router_w.shape[0]
-        if router_w.shape[1] != H or router_w.dtype != hidden.dtype:
-            raise ValueError("router_w must be E x H with the hidden states' dtype")
-        for t in (hidden, router_w, expert_to_rank, logit_bias, select_bias):
+        if packed:
+            E, wdev = router_w.E, router_w.data.device
+            if router_w.H != H or router_w.dtype != hidden.dtype:
+                raise ValueError("packed router was built for another H or dtype")
+        else:
+            if router_w.dim() != 2 or not router_w.is_contiguous():
+                raise ValueError("router_w must be a contiguous E x H tensor")
+            E, wdev = router_w.shape[0], router_w.device
+            if router_w.shape[1] != H or router_w.dtype != hidden.dtype:
+                raise ValueError("router_w must be E x H with the hidden states' dtype")
+        for t in (hidden, expert_to_rank, logit_bias, select_bias):
             if t is not None and t.device != self.device:
                 raise ValueError("all tensors must live on the predictor's device")
+        if wdev != self.device:
+            raise ValueError("all tensors must live on the predictor's device")
         if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
             raise ValueError("expert_to_rank must be int32[E]")
         for b in (logit_bias, select_bias):
             if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
                 raise ValueError("biases must be contiguous float32[E]")
+        code = _dtype_code(hidden)
+        lib = L.lib()
+        if not packed:
+            need = int(lib.fb_predict_workspace_bytes(E, H, code))
+            if need == 0:
+                L.check(L.FB_EUNSUPPORTED if E > 0 else L.FB_EINVAL, "fb_predict_workspace_bytes")
+            self._reserve(need, stream)
         if out is None:
             out = Prediction(torch.empty(E, dtype=torch.int32, device=self.device),
                              torch.empty(R, dtype=torch.int32, device=self.device),
@@ -158,14 +213,23 @@ class Predictor:
             out.logits = torch.empty((T, E), dtype=torch.float32, device=self.device)
         sc = scoring.to_c()
         ld = hidden.stride(0) if T > 0 else H
+        topk = _ptr(out.topk) if return_topk else None
+        logits = _ptr(out.logits) if return_logits else None
+        sh = _stream_handle(self.device, stream)
         with torch.cuda.device(self.device):
-            st = L.lib().fb_predict_load(
-                _ptr(hidden), T, H, ld, _dtype_code(hidden), _ptr(router_w), E, _ptr(logit_bias),
-                _ptr(select_bias), ctypes.byref(sc), _ptr(expert_to_rank), R, _ptr(out.counts),
-                _ptr(out.rank_loads), _ptr(out.max_mean), _ptr(self.workspace),
-                self.workspace.numel(), _ptr(out.topk) if return_topk else None,
-                _ptr(out.logits) if return_logits else None, _stream_handle(self.device, stream))
-        L.check(st, "fb_predict_load")
+            if packed:
+                st = lib.fb_predict_load_packed(
+                    _ptr(hidden), T, H, ld, code, _ptr(router_w.data), router_w.data.numel(), E,
+                    _ptr(logit_bias), _ptr(select_bias), ctypes.byref(sc), _ptr(expert_to_rank), R,
+                    _ptr(out.counts), _ptr(out.rank_loads), _ptr(out.max_mean),
+                    _ptr(self.workspace), self.workspace.numel(), topk, logits, sh)
+            else:
+                st = lib.fb_predict_load(
+                    _ptr(hidden), T, H, ld, code, _ptr(router_w), E, _ptr(logit_bias),
+                    _ptr(select_bias), ctypes.byref(sc), _ptr(expert_to_rank), R, _ptr(out.counts),
+                    _ptr(out.rank_loads), _ptr(out.max_mean), _ptr(self.workspace),
+                    self.workspace.numel(), topk, logits, sh)
+        L.check(st, "fb_predict_load_packed" if packed else "fb_predict_load")
         return out
 
 

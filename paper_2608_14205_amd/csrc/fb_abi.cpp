@@ -78,7 +78,15 @@ const char* fb_status_string(int status) {
   }
 }
 
-size_t fb_predict_workspace_bytes(void) { return fb::kWsBytes; }
+size_t fb_router_packed_bytes(int32_t E, int32_t H, int32_t dtype) {
+  if (E < 1 || E > FB_MAX_EXPERTS || H < 1 || (dtype != FB_BF16 && dtype != FB_F32)) return 0;
+  return fb::router_packed_bytes(E, H, dtype);
+}
+
+size_t fb_predict_workspace_bytes(int32_t E, int32_t H, int32_t dtype) {
+  const size_t packed = fb_router_packed_bytes(E, H, dtype);
+  return packed ? fb::kWsBytes + packed : 0;
+}
 
 int fb_predict_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
   if (!workspace || !aligned16(workspace)) return FB_EINVAL;
@@ -88,13 +96,32 @@ int fb_predict_workspace_init(void* workspace, size_t workspace_bytes, void* str
   return fb::launch_workspace_zero(workspace, fb::kWsBytes, stream);
 }
 
-int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
-                    const void* router_w, int32_t E, const float* logit_bias,
-                    const float* select_bias, const fb_scoring* scoring,
-                    const int32_t* expert_to_rank, int32_t R, int32_t* counts,
-                    int32_t* rank_loads, double* max_mean, void* workspace,
-                    size_t workspace_bytes, int32_t* topk_idx, float* logits, void* stream) {
-  if (!scoring || !router_w || !expert_to_rank || !counts || !rank_loads || !max_mean || !workspace)
+int fb_pack_router_weight(const void* router_w, int32_t E, int32_t H, int32_t dtype, void* packed,
+                          size_t packed_bytes, void* stream) {
+  if (!router_w || !packed || E < 1 || H < 1) return FB_EINVAL;
+  if (dtype != FB_BF16 && dtype != FB_F32) return FB_EINVAL;
+  if (E > FB_MAX_EXPERTS) return FB_EUNSUPPORTED;
+  if (H % (dtype == FB_BF16 ? 32 : 16) != 0) return FB_EUNSUPPORTED;
+  if (!aligned16(router_w) || !aligned16(packed)) return FB_EUNSUPPORTED;
+  const size_t need = fb::router_packed_bytes(E, H, dtype);
+  if (need >= ((size_t)1 << 31)) return FB_EUNSUPPORTED;   // 32-bit buffer offsets
+  if (packed_bytes < need) return FB_ENOSPC;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  return fb::launch_pack(router_w, E, H, dtype, packed, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Checks shared by both predictor entry points; FB_OK when a launch may proceed.
+int check_predict(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
+                  int32_t E, const float* select_bias, const fb_scoring* scoring,
+                  const int32_t* expert_to_rank, int32_t R, const int32_t* counts,
+                  const int32_t* rank_loads, const double* max_mean, const void* workspace,
+                  size_t workspace_bytes, size_t workspace_need) {
+  if (!scoring || !expert_to_rank || !counts || !rank_loads || !max_mean || !workspace)
     return FB_EINVAL;
   if (T < 0 || H < 1 || E < 1 || R < 1 || ld_hidden < H) return FB_EINVAL;
   if (T > 0 && !hidden) return FB_EINVAL;
@@ -102,25 +129,29 @@ int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
   const int elem = dtype == FB_BF16 ? 2 : 4;
   if (E > FB_MAX_EXPERTS || R > FB_MAX_RANKS) return FB_EUNSUPPORTED;
   if (H % (dtype == FB_BF16 ? 32 : 16) != 0) return FB_EUNSUPPORTED;
-  if ((ld_hidden * elem) % 16 != 0 || (hidden && !aligned16(hidden)) || !aligned16(router_w))
+  if ((ld_hidden * elem) % 16 != 0 || (hidden && !aligned16(hidden))) return FB_EUNSUPPORTED;
+  // 32-bit buffer offsets: one 128-row tile of hidden states and the whole packed router weight
+  if (ld_hidden * elem * 128 >= ((int64_t)1 << 31) ||
+      fb::router_packed_bytes(E, H, dtype) >= ((size_t)1 << 31))
     return FB_EUNSUPPORTED;
-  // 32-bit buffer offsets: one 128-row tile of hidden states and the whole router weight
-  if (ld_hidden * elem * 128 >= ((int64_t)1 << 31) || (int64_t)E * H * elem >= ((int64_t)1 << 31))
-    return FB_EUNSUPPORTED;
-  if ((reinterpret_cast<uintptr_t>(workspace) & 15u) != 0) return FB_EINVAL;
-  if (workspace_bytes < fb::kWsBytes) return FB_ENOSPC;
-  const int sc = check_scoring(*scoring, E, select_bias);
-  if (sc != FB_OK) return sc;
-  const int dc = fb::check_device();
-  if (dc != FB_OK) return dc;
+  if (!aligned16(workspace)) return FB_EINVAL;
+  if (workspace_bytes < workspace_need) return FB_ENOSPC;
+  return check_scoring(*scoring, E, select_bias);
+}
 
+fb::PredictLaunch make_launch(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                              int32_t dtype, const void* router_packed, int32_t E,
+                              const float* logit_bias, const float* select_bias,
+                              const fb_scoring* scoring, const int32_t* expert_to_rank, int32_t R,
+                              int32_t* counts, int32_t* rank_loads, double* max_mean,
+                              void* workspace, int32_t* topk_idx, float* logits, void* stream) {
   fb::PredictLaunch a;
   a.hidden = hidden;
   a.T = T;
   a.H = H;
   a.ld_hidden = ld_hidden;
   a.dtype = dtype;
-  a.router_w = router_w;
+  a.router_packed = router_packed;
   a.E = E;
   a.logit_bias = logit_bias;
   a.select_bias = select_bias;
@@ -135,7 +166,56 @@ int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
   a.topk_idx = topk_idx;
   a.logits = logits;
   a.stream = stream;
-  return fb::launch_predict(a);
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
+                    const void* router_w, int32_t E, const float* logit_bias,
+                    const float* select_bias, const fb_scoring* scoring,
+                    const int32_t* expert_to_rank, int32_t R, int32_t* counts,
+                    int32_t* rank_loads, double* max_mean, void* workspace,
+                    size_t workspace_bytes, int32_t* topk_idx, float* logits, void* stream) {
+  if (!router_w) return FB_EINVAL;
+  const size_t need = fb_predict_workspace_bytes(E, H, dtype);
+  const int vc = check_predict(hidden, T, H, ld_hidden, dtype, E, select_bias, scoring,
+                               expert_to_rank, R, counts, rank_loads, max_mean, workspace,
+                               workspace_bytes, need);
+  if (vc != FB_OK) return vc;
+  if (!aligned16(router_w)) return FB_EUNSUPPORTED;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  void* packed = static_cast<char*>(workspace) + fb::kWsBytes;
+  const int pc = fb::launch_pack(router_w, E, H, dtype, packed, stream);
+  if (pc != FB_OK) return pc;
+  return fb::launch_predict(make_launch(hidden, T, H, ld_hidden, dtype, packed, E, logit_bias,
+                                        select_bias, scoring, expert_to_rank, R, counts, rank_loads,
+                                        max_mean, workspace, topk_idx, logits, stream));
+}
+
+int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                           int32_t dtype, const void* router_packed, size_t router_packed_bytes,
+                           int32_t E, const float* logit_bias, const float* select_bias,
+                           const fb_scoring* scoring, const int32_t* expert_to_rank, int32_t R,
+                           int32_t* counts, int32_t* rank_loads, double* max_mean,
+                           void* workspace, size_t workspace_bytes, int32_t* topk_idx,
+                           float* logits, void* stream) {
+  if (!router_packed) return FB_EINVAL;
+  const int vc = check_predict(hidden, T, H, ld_hidden, dtype, E, select_bias, scoring,
+                               expert_to_rank, R, counts, rank_loads, max_mean, workspace,
+                               workspace_bytes, fb::kWsBytes);
+  if (vc != FB_OK) return vc;
+  if (!aligned16(router_packed)) return FB_EUNSUPPORTED;
+  if (router_packed_bytes < fb::router_packed_bytes(E, H, dtype)) return FB_ENOSPC;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  return fb::launch_predict(make_launch(hidden, T, H, ld_hidden, dtype, router_packed, E,
+                                        logit_bias, select_bias, scoring, expert_to_rank, R,
+                                        counts, rank_loads, max_mean, workspace, topk_idx, logits,
+                                        stream));
 }
 
 int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,

@@ -15,7 +15,7 @@ struct PredictLaunch {
   int32_t H;
   int64_t ld_hidden;  // elements
   int32_t dtype;      // FB_BF16 | FB_F32
-  const void* router_w;
+  const void* router_packed;  // router weight in the layout written by launch_pack
   int32_t E;
   const float* logit_bias;
   const float* select_bias;
@@ -37,6 +37,11 @@ constexpr size_t kWsAccOffset = 0;
 constexpr size_t kWsTicketOffset = 1024;
 constexpr size_t kWsBytes = 2048;
 
+// Bytes of the packed router weight for E experts of H elements of `dtype`.
+size_t router_packed_bytes(int32_t E, int32_t H, int32_t dtype);
+// Rewrites the E x H row-major router weight into the fragment-major layout the predictor kernel
+// streams (one kernel on `stream`).
+int launch_pack(const void* router_w, int32_t E, int32_t H, int32_t dtype, void* packed, void* stream);
 int launch_predict(const PredictLaunch& a);
 int launch_workspace_zero(void* workspace, size_t bytes, void* stream);
 

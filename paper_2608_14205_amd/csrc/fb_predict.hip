@@ -6,19 +6,25 @@
 // last workgroup to finish folds the histogram into per-rank loads under the expert-to-rank
 // placement (Alg. 1, second step) and computes the max-to-mean ratio (Sec. "Metrics").
 //
-// Data flow of one workgroup (4 waves, 256 threads, one workgroup per CU):
-//   * hidden rows stream from HBM through raw buffer loads (bounds-checked: rows past T read as
-//     zero) into registers, kDepth stages ahead, then into a double-buffered LDS stage that all
-//     waves share;
-//   * each wave owns a slice of the experts; its router-weight fragments come straight from L2
-//     into registers (same prefetch distance, so the in-order vmcnt waits never stall on a later
-//     hidden stage);
-//   * v_mfma_f32_16x16x32_bf16 (or 16x16x4 f32) with the router weight as the A operand
-//     (M = experts) and the hidden tile as B (N = tokens), so each lane ends with four consecutive
-//     experts of one token;
-//   * the logits never leave the chip: scores go to an LDS tile, EPAD/16 lanes cooperate on one
-//     token, and the histogram is privatised in LDS with one global atomic per expert per
-//     workgroup.
+// Workgroup: 8 waves (512 threads), one workgroup per CU.
+//   * Waves 0-3 are producers.  They stream the tile's hidden rows from HBM with full 128-byte
+//     line requests (8 rows x 128 B per instruction), two k-stages ahead, and store them row-major
+//     into a double-buffered LDS stage (row pitch 144 B, so both the stores and the fragment
+//     reads below stay close to conflict-free).
+//   * Waves 4-7 are consumers, one per SIMD next to a producer.  Each owns a slice of the
+//     experts.  It loads its router-weight fragments from the pre-packed weight (one contiguous
+//     1 KB per load instruction, one stage ahead, L2-resident) straight into registers, reads
+//     the hidden fragments from LDS, and runs v_mfma_f32_32x32x16_bf16 (or 32x32x2 f32).  The
+//     router weight is the A operand (M = experts) and the hidden tile is B (N = tokens), so
+//     each lane ends with groups of four consecutive experts of one token.  The 32x32 shape
+//     does the same contraction with half the instructions of the 16x16 one and, measured on
+//     MI355X, less time and energy per flop, which matters because this kernel runs at the
+//     board's power limit.
+//   * The two global streams (HBM hidden rows, L2 router weight) live in different waves, so a
+//     short-latency weight load never waits in the in-order vmcnt queue behind a hidden-row load.
+//   * One LDS barrier per k-stage couples producers and consumers.
+// The logits never leave the chip: scores go to an LDS tile, EPAD/16 lanes cooperate on one
+// token, and the histogram is privatised in LDS with one global atomic per expert per workgroup.
 //
 // Selection is exact in float32 with ties to the lower expert index.  The fast path ranks 32-bit
 // keys (top 24 bits of the order-preserving score encoding, then 255 - expert); its set equals the
@@ -34,32 +40,35 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
-constexpr int kSlabBytes = 64;                  // bytes of a row feeding one MFMA k-slab
-constexpr int kNSlab = 2;                       // k-slabs per pipeline stage
-constexpr int kStageRowBytes = kSlabBytes * kNSlab;
-constexpr int kDepth = 3;                       // pipeline stages in flight
-constexpr int kChunk = 1024;                    // one (slab, 16-token fragment): 64 lanes x 16 B
+constexpr int kThreads = 512;
+constexpr int kWaves = kThreads / 64;
+constexpr int kProducers = 4;
+constexpr int kStepBytes = 32;                  // bytes of a row feeding one MFMA k-step
+constexpr int kNStep = 4;                       // k-steps per pipeline stage
+constexpr int kStageRowBytes = kStepBytes * kNStep;
+constexpr int kPitch = kStageRowBytes + 16;     // LDS row pitch of a hidden stage
 constexpr int kMaxK = FB_MAX_TOPK;
 constexpr int kMaxGroups = 32;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;    // raw buffer, 32-bit dwords
+constexpr uint32_t kOobOffset = 0x80000000u;    // fails the buffer range check: load returns 0
 
-// Tile shapes: WE waves along experts x WT waves along tokens, BM tokens per workgroup.
+// Consumer tile shapes: WE waves along experts x WT waves along tokens, BM tokens per workgroup;
+// every wave tile is a whole number of 32 x 32 MFMA blocks.
 template <int EPAD> struct TileCfg;
 template <> struct TileCfg<256> { static constexpr int WE = 4, WT = 1, BM = 128; };
 template <> struct TileCfg<128> { static constexpr int WE = 4, WT = 1, BM = 64; };
-template <> struct TileCfg<64> { static constexpr int WE = 4, WT = 1, BM = 64; };
-template <> struct TileCfg<32> { static constexpr int WE = 2, WT = 2, BM = 64; };
-template <> struct TileCfg<16> { static constexpr int WE = 1, WT = 4, BM = 64; };
+template <> struct TileCfg<64> { static constexpr int WE = 2, WT = 2, BM = 64; };
+template <> struct TileCfg<32> { static constexpr int WE = 1, WT = 4, BM = 128; };
 
 struct Params {
   const char* x;
   int64_t T;
   int32_t Hbytes;
   int32_t ldx_bytes;
-  const char* w;
+  const char* wpack;   // packed router weight (see pack_kernel)
   int32_t E;
   const float* logit_bias;
   const float* select_bias;
@@ -75,7 +84,6 @@ struct Params {
   float* logits;
   uint32_t nblocks;
   int32_t nstages;
-  int32_t tail_half;
 };
 
 // Workgroup barrier that orders LDS only; outstanding global loads stay in flight across it.
@@ -142,198 +150,217 @@ __device__ __forceinline__ void top2_group(float& m1, float& m2, int g) {
   if (g >= 16) top2_merge_step<kMirror>(m1, m2);
 }
 
+// ---- packed router weight --------------------------------------------------------------------
+// Stage st (128 bytes of every row) occupies EPAD * 128 contiguous bytes.  Inside it, the 1 KB
+// chunk c = (we * 4 + q) * FE + fe holds, for lane l, the 16 bytes of row
+// e = we * EW + fe * 32 + (l & 31) at byte st * 128 + q * 32 + (l >> 5) * 16 of that row: exactly
+// the A-operand fragment consumer wave `we` loads for expert block fe of k-step q.  Rows >= E and
+// bytes past H are zero.
+template <int EPAD>
+__global__ void pack_kernel(const char* __restrict__ w, int32_t E, int32_t Hbytes, int32_t nstages,
+                            u32x4* __restrict__ out) {
+  using Cfg = TileCfg<EPAD>;
+  constexpr int EW = EPAD / Cfg::WE, FE = EW / 32;
+  const int64_t units = (int64_t)nstages * EPAD * 8;
+  for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < units;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int st = (int)(idx / (EPAD * 8));
+    const int rem = (int)(idx % (EPAD * 8));
+    const int c = rem >> 6, l = rem & 63;
+    const int fe = c % FE, q = (c / FE) % kNStep, we = c / (FE * kNStep);
+    const int e = we * EW + fe * 32 + (l & 31);
+    const int b = st * kStageRowBytes + q * kStepBytes + (l >> 5) * 16;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (e < E && b < Hbytes) v = *reinterpret_cast<const u32x4*>(w + (int64_t)e * Hbytes + b);
+    out[idx] = v;
+  }
+}
+
 template <bool BF16, int EPAD>
 __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   using Cfg = TileCfg<EPAD>;
   constexpr int WE = Cfg::WE, WT = Cfg::WT, BM = Cfg::BM;
   constexpr int EW = EPAD / WE, TW = BM / WT;
-  constexpr int FE = EW / 16, FT = TW / 16, NF = BM / 16;
-  constexpr int CPW = kNSlab * NF / 4;           // hidden chunks each wave loads per stage
-  constexpr int STAGE_BYTES = kNSlab * NF * kChunk;
+  constexpr int FE = EW / 32, FT = TW / 32;
+  constexpr int RPW = BM / kProducers;           // hidden rows per producer wave
+  constexpr int LPW = RPW / 8;                   // full-line loads per producer per stage
+  constexpr int XSTAGE = BM * kPitch;
+  constexpr int SB = EPAD * kStageRowBytes;      // packed weight bytes per stage
   constexpr int SROW = EPAD + 4;                 // score-tile row stride in floats
   constexpr int SCORE_BYTES = BM * SROW * 4;
-  constexpr int SMEM = (2 * STAGE_BYTES > SCORE_BYTES) ? 2 * STAGE_BYTES : SCORE_BYTES;
+  constexpr int SMEM = (2 * XSTAGE > SCORE_BYTES) ? 2 * XSTAGE : SCORE_BYTES;
   constexpr int LPT = EPAD / 16;                 // lanes per token in the selection phase
   constexpr int TPP = kThreads / LPT;            // tokens per selection pass
   constexpr int NPASS = (BM + TPP - 1) / TPP;
   constexpr int GSC_TOK = TPP < BM ? TPP : BM;
-  static_assert(CPW >= 1 && (kNSlab * NF) % 4 == 0, "stage must split over 4 waves");
+  static_assert(LPW >= 1 && RPW % 8 == 0, "producers split the tile in 8-row groups");
+  static_assert(WE * WT == kWaves - kProducers, "one consumer per SIMD");
+  static_assert(EW % 32 == 0 && TW % 32 == 0, "wave tiles are whole 32 x 32 MFMA blocks");
 
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   __shared__ int32_t hist[EPAD];
   __shared__ int32_t sel[BM][kMaxK + 1];
   __shared__ float gsc[GSC_TOK][kMaxGroups];
   __shared__ int32_t s_flag;
-  __shared__ int64_t s_red[kThreads / 64][2];
+  __shared__ int64_t s_red[kWaves][2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int we = wave % WE;
-  const int wt = wave / WE;
+  // wave-uniform by construction; readfirstlane keeps it (and every buffer-load offset derived
+  // from it) in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool consumer = wave >= kProducers;
+  const int cw = consumer ? wave - kProducers : 0;
+  const int we = cw % WE;
+  const int wt = cw / WE;
   const int64_t row0 = (int64_t)blockIdx.x * BM;
   const int E = p.E;
 
   for (int i = tid; i < EPAD; i += kThreads) hist[i] = 0;
 
-  f32x4 acc[FE][FT];
+  f32x16 acc[FE][FT];
 #pragma unroll
   for (int a = 0; a < FE; ++a)
 #pragma unroll
-    for (int b = 0; b < FT; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < FT; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
+  // Both roles run exactly NP stages with one barrier each (NP: nstages rounded up to the unroll
+  // factor 2).  Stages past the end load out of range, i.e. zeros.
+  const int nst = p.nstages;
+  const int NP = (nst + 1) & ~1;
   if (row0 < p.T) {
-    // ---- router GEMM: acc[e][t] = sum_h W[e,h] * X[t,h] -------------------------------------
-    const int64_t rows = (p.T - row0) < BM ? (p.T - row0) : BM;
-    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.x + row0 * (int64_t)p.ldx_bytes), (short)0, (int)(rows * p.ldx_bytes), kRsrcWord3);
-    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)p.w, (short)0, E * p.Hbytes, kRsrcWord3);
-
-    uint32_t xoff[CPW];
+    if (!consumer) {
+      // ---- producers: hidden rows, HBM -> registers -> LDS ----------------------------------
+      const int64_t rows = (p.T - row0) < BM ? (p.T - row0) : BM;
+      const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(p.x + row0 * (int64_t)p.ldx_bytes), (short)0, (int)(rows * p.ldx_bytes), kRsrcWord3);
+      const int col = (lane & 7) * 16;           // byte within the 128-byte stage segment
+      uint32_t xoff[LPW], loff[LPW];
 #pragma unroll
-    for (int i = 0; i < CPW; ++i) {
-      const int c = wave * CPW + i, s = c / NF, f = c % NF;
-      xoff[i] = (uint32_t)((f * 16 + (lane & 15)) * p.ldx_bytes + s * kSlabBytes + (lane >> 4) * 16);
-    }
-    uint32_t woff[FE];
+      for (int i = 0; i < LPW; ++i) {
+        const int r = wave * RPW + i * 8 + (lane >> 3);
+        xoff[i] = (uint32_t)(r * p.ldx_bytes + col);
+        loff[i] = (uint32_t)(r * kPitch + col);
+      }
+      u32x4 xa[2][LPW];
+      // bytes at or past H (tail of a half-width last stage, padded stages) are not fetched
+      auto load_x = [&](u32x4(&dst)[LPW], int st) {
+        const bool stage_ok = st < nst;
+        const bool ok = stage_ok && st * kStageRowBytes + col < p.Hbytes;
 #pragma unroll
-    for (int fe = 0; fe < FE; ++fe) {
-      const int erow = we * EW + fe * 16 + (lane & 15);
-      woff[fe] = (uint32_t)(erow * p.Hbytes + (lane >> 4) * 16);
-    }
-
-    u32x4 xa[kDepth][CPW];
-    u32x4 wa[kDepth][FE][kNSlab];
-    const int nst = p.nstages;
-    // A slab whose k-range starts at or past H (the padded stages of the last unrolled round and
-    // the second slab of a half-width last stage) is loaded with the top bit set in the per-lane
-    // offset: the hardware range check (which covers the per-lane offset) fails, the load returns
-    // zeros and no memory is touched.  Every load is then unconditional, which keeps the
-    // compiler's in-order vmcnt accounting exact (a conditional load would force it to assume the
-    // loop's later loads might be missing and to wait for everything).
-    const int nst_pad = ((nst + kDepth - 1) / kDepth) * kDepth;
-    auto slab_ok = [&](int st, int s) -> bool { return st * kStageRowBytes + s * kSlabBytes < p.Hbytes; };
-
-#define FB_LOAD_X(D, ST)                                                                        \
-  {                                                                                             \
-    const int st_ = (ST);                                                                       \
-    _Pragma("unroll") for (int i = 0; i < CPW; ++i) {                                           \
-      const int s_ = (wave * CPW + i) / NF;                                                     \
-      const bool ok_ = slab_ok(st_, s_);                                                        \
-      xa[D][i] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff[i] | (ok_ ? 0u : 0x80000000u),  \
-                                                       ok_ ? st_ * kStageRowBytes : 0, 2);      \
-    }                                                                                           \
-  }
-#define FB_LOAD_W(D, ST)                                                                        \
-  {                                                                                             \
-    const int st_ = (ST);                                                                       \
-    _Pragma("unroll") for (int s = 0; s < kNSlab; ++s) {                                        \
-      const bool ok_ = slab_ok(st_, s);                                                         \
-      _Pragma("unroll") for (int fe = 0; fe < FE; ++fe) wa[D][fe][s] =                          \
-          __builtin_amdgcn_raw_buffer_load_b128(                                                \
-              wr, (woff[fe] + s * kSlabBytes) | (ok_ ? 0u : 0x80000000u),                       \
-              ok_ ? st_ * kStageRowBytes : 0, 0);                                               \
-    }                                                                                           \
-  }
-
-    // Issue order X(0), W(0), X(1), W(1), ... matches the steady state below, so the wait counts
-    // the compiler derives at the loop header are exact.
+        for (int i = 0; i < LPW; ++i)
+          dst[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, ok ? xoff[i] : kOobOffset,
+                                                         stage_ok ? st * kStageRowBytes : 0, 2);
+      };
+      load_x(xa[0], 0);
+      load_x(xa[1], 1);
+      for (int st0 = 0; st0 < NP; st0 += 2) {
 #pragma unroll
-    for (int d = 0; d < kDepth; ++d) {
-      FB_LOAD_X(d, d)
-      __builtin_amdgcn_sched_barrier(0);
-      FB_LOAD_W(d, d)
-      __builtin_amdgcn_sched_barrier(0);
-    }
-
-    for (int st0 = 0; st0 < nst_pad; st0 += kDepth) {
+        for (int d = 0; d < 2; ++d) {
+          const int st = st0 + d;
+          char* buf = smem + (st & 1) * XSTAGE;
 #pragma unroll
-      for (int d = 0; d < kDepth; ++d) {
-        const int st = st0 + d;
-        char* buf = smem + (st & 1) * STAGE_BYTES;
+          for (int i = 0; i < LPW; ++i) *reinterpret_cast<u32x4*>(buf + loff[i]) = xa[d][i];
+          load_x(xa[d], st + 2);
+          __builtin_amdgcn_sched_barrier(0);
+          lds_barrier();                         // stage st is in LDS
+        }
+      }
+    } else {
+      // ---- consumers: packed router weight L2 -> registers, hidden fragments from LDS --------
+      const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)p.wpack, (short)0, nst * SB, kRsrcWord3);
+      uint32_t woff[FE][kNStep];
 #pragma unroll
-        for (int i = 0; i < CPW; ++i)
-          *reinterpret_cast<u32x4*>(buf + (wave * CPW + i) * kChunk + lane * 16) = xa[d][i];
-        FB_LOAD_X(d, st + kDepth)
-        __builtin_amdgcn_sched_barrier(0);
-        lds_barrier();
-        // the second slab of a half-width last stage lies past H: skip it (padded stages are zero)
-        const bool half = (st == nst - 1) && p.tail_half;
-        u32x4 bfr[kNSlab][FT];
+      for (int fe = 0; fe < FE; ++fe)
 #pragma unroll
-        for (int ft = 0; ft < FT; ++ft)
-          bfr[0][ft] = *reinterpret_cast<const u32x4*>(buf + (wt * FT + ft) * kChunk + lane * 16);
+        for (int q = 0; q < kNStep; ++q)
+          woff[fe][q] = (uint32_t)(((we * kNStep + q) * FE + fe) * 1024 + lane * 16);
+      const uint32_t boff = (uint32_t)((wt * TW + (lane & 31)) * kPitch + (lane >> 5) * 16);
+      u32x4 wa[2][FE][kNStep];
+      auto load_w = [&](u32x4(&dst)[FE][kNStep], int st) {
+        const bool ok = st < nst;
 #pragma unroll
-        for (int s = 0; s < kNSlab; ++s) {
-          if (s + 1 < kNSlab) {
+        for (int fe = 0; fe < FE; ++fe)
+#pragma unroll
+          for (int q = 0; q < kNStep; ++q)
+            dst[fe][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? woff[fe][q] : kOobOffset,
+                                                               ok ? st * SB : 0, 0);
+      };
+      load_w(wa[0], 0);
+      for (int st0 = 0; st0 < NP; st0 += 2) {
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const int st = st0 + d;
+          load_w(wa[d ^ 1], st + 1);
+          __builtin_amdgcn_sched_barrier(0);
+          lds_barrier();                         // stage st is in LDS
+          const char* buf = smem + (st & 1) * XSTAGE;
+#pragma unroll
+          for (int q = 0; q < kNStep; ++q) {
+            u32x4 bfr[FT];
 #pragma unroll
             for (int ft = 0; ft < FT; ++ft)
-              bfr[s + 1][ft] = *reinterpret_cast<const u32x4*>(
-                  buf + ((s + 1) * NF + wt * FT + ft) * kChunk + lane * 16);
-          }
-          if (s == 0 || !half) {
+              bfr[ft] = *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + q * kStepBytes + boff);
 #pragma unroll
-            for (int fe = 0; fe < FE; ++fe) {
+            for (int ft = 0; ft < FT; ++ft) {
 #pragma unroll
-              for (int ft = 0; ft < FT; ++ft) {
+              for (int fe = 0; fe < FE; ++fe) {
                 if constexpr (BF16) {
-                  acc[fe][ft] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                      __builtin_bit_cast(bf16x8, wa[d][fe][s]), __builtin_bit_cast(bf16x8, bfr[s][ft]),
+                  acc[fe][ft] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                      __builtin_bit_cast(bf16x8, wa[d][fe][q]), __builtin_bit_cast(bf16x8, bfr[ft]),
                       acc[fe][ft], 0, 0, 0);
                 } else {
-                  const f32x4 av = __builtin_bit_cast(f32x4, wa[d][fe][s]);
-                  const f32x4 bv = __builtin_bit_cast(f32x4, bfr[s][ft]);
+                  // four k-pairs per fragment; A and B take the same k for every lane
+                  const f32x4 av = __builtin_bit_cast(f32x4, wa[d][fe][q]);
+                  const f32x4 bv = __builtin_bit_cast(f32x4, bfr[ft]);
 #pragma unroll
-                  for (int q = 0; q < 4; ++q)
-                    acc[fe][ft] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[q], bv[q], acc[fe][ft], 0, 0, 0);
+                  for (int j = 0; j < 4; ++j)
+                    acc[fe][ft] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[j], bv[j], acc[fe][ft], 0, 0, 0);
                 }
               }
             }
           }
         }
-        __builtin_amdgcn_sched_barrier(0);
-        FB_LOAD_W(d, st + kDepth)
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
-#undef FB_LOAD_X
-#undef FB_LOAD_W
   }
   lds_barrier();
 
-  // ---- scores into an LDS tile S[token][expert] ------------------------------------------------
+  // ---- consumers: logits and scores into an LDS tile S[token][expert] ------------------------
+  // Lane l of a 32 x 32 block holds token (l & 31) and experts g * 8 + (l >> 5) * 4 + r in
+  // register g * 4 + r.
   float* S = reinterpret_cast<float*>(smem);
-  if (row0 < p.T) {
+  if (consumer && row0 < p.T) {
 #pragma unroll
     for (int fe = 0; fe < FE; ++fe) {
-      const int e0 = we * EW + fe * 16 + (lane >> 4) * 4;
-      float lb[4], sb[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int e = e0 + r;
-        lb[r] = (p.logit_bias && e < E) ? p.logit_bias[e] : 0.f;
-        sb[r] = (p.select_bias && e < E) ? p.select_bias[e] : 0.f;
-      }
-#pragma unroll
-      for (int ft = 0; ft < FT; ++ft) {
-        const int tl = wt * TW + ft * 16 + (lane & 15);
-        const int64_t t = row0 + tl;
-        f32x4 sv;
+      for (int g = 0; g < 4; ++g) {
+        const int e0 = we * EW + fe * 32 + g * 8 + (lane >> 5) * 4;
+        float lb[4], sb[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = e0 + r;
-          const float z = acc[fe][ft][r] + lb[r];
-          if (p.logits && t < p.T && e < E) p.logits[t * E + e] = z;
-          float s;
-          if (p.kind == FB_SIGMOID) {
-            s = __builtin_amdgcn_rcpf(1.0f + __expf(-z)) + sb[r];
-          } else {
-            s = z;
-          }
-          sv[r] = (e < E) ? s + 0.0f : -__builtin_inff();
+          lb[r] = (p.logit_bias && e < E) ? p.logit_bias[e] : 0.f;
+          sb[r] = (p.select_bias && e < E) ? p.select_bias[e] : 0.f;
         }
-        *reinterpret_cast<f32x4*>(S + tl * SROW + e0) = sv;
+#pragma unroll
+        for (int ft = 0; ft < FT; ++ft) {
+          const int tl = wt * TW + ft * 32 + (lane & 31);
+          const int64_t t = row0 + tl;
+          f32x4 sv;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int e = e0 + r;
+            const float z = acc[fe][ft][g * 4 + r] + lb[r];
+            if (p.logits && t < p.T && e < E) p.logits[t * E + e] = z;
+            const float s = (p.kind == FB_SIGMOID) ? __builtin_amdgcn_rcpf(1.0f + __expf(-z)) + sb[r] : z;
+            sv[r] = (e < E) ? s + 0.0f : -__builtin_inff();
+          }
+          *reinterpret_cast<f32x4*>(S + tl * SROW + e0) = sv;
+        }
       }
     }
   }
@@ -360,47 +387,46 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     if (p.n_group > 1) {
       const int gsz = E / p.n_group;
       float* gs = gsc[gslot];
+      // group scores: sum of the group's group_topn best scores, largest first
       if (gsz >= 16) {
         const int lpg = gsz >> 4;
         float m1 = -__builtin_inff(), m2 = -__builtin_inff();
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float v = s[i];
-          m2 = __builtin_amdgcn_fmed3f(m1, m2, v);
-          m1 = fmaxf(m1, v);
+          m2 = __builtin_amdgcn_fmed3f(m1, m2, s[i]);
+          m1 = fmaxf(m1, s[i]);
         }
         top2_group(m1, m2, lpg);
-        const int g = (jl * 16) / gsz;
-        const float score = p.group_topn == 2 ? m1 + m2 : m1;
-        if ((jl & (lpg - 1)) == 0 && jl * 16 < E) gs[g] = score;
+        if ((jl & (lpg - 1)) == 0 && jl * 16 < E) gs[(jl * 16) / gsz] = p.group_topn == 2 ? m1 + m2 : m1;
       } else {
         const int gpl = 16 / gsz;
         for (int u = 0; u < gpl; ++u) {
           float m1 = -__builtin_inff(), m2 = -__builtin_inff();
           for (int i = u * gsz; i < (u + 1) * gsz; ++i) {
-            const float v = s[i];
-            m2 = __builtin_amdgcn_fmed3f(m1, m2, v);
-            m1 = fmaxf(m1, v);
+            m2 = __builtin_amdgcn_fmed3f(m1, m2, s[i]);
+            m1 = fmaxf(m1, s[i]);
           }
-          const int g = jl * gpl + u;
-          if (jl * 16 + u * gsz < E) gs[g] = p.group_topn == 2 ? m1 + m2 : m1;
+          if (jl * 16 + u * gsz < E) gs[jl * gpl + u] = p.group_topn == 2 ? m1 + m2 : m1;
         }
       }
       wave_lds_sync();
-      keep = 0;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int e = jl * 16 + i;
-        if (e < E) {
-          const int g = e / gsz;
-          const float mine = gs[g];
-          int rank = 0;
-          for (int h = 0; h < p.n_group; ++h) {
-            const float o = gs[h];
-            rank += (o > mine) || (o == mine && h < g);
-          }
-          if (rank < p.topk_group) keep |= 1u << i;
+      // rank of each of this lane's groups among all groups (score desc, lower index first)
+      auto kept = [&](int g) -> bool {
+        const float mine = gs[g];
+        int rank = 0;
+        for (int h = 0; h < p.n_group; ++h) {
+          const float o = gs[h];
+          rank += (o > mine) || (o == mine && h < g);
         }
+        return rank < p.topk_group;
+      };
+      keep = 0;
+      if (gsz >= 16) {
+        if (jl * 16 < E && kept((jl * 16) / gsz)) keep = 0xFFFFu;
+      } else {
+        const int gpl = 16 / gsz;
+        for (int u = 0; u < gpl; ++u)
+          if (jl * 16 + u * gsz < E && kept(jl * gpl + u)) keep |= ((1u << gsz) - 1u) << (u * gsz);
       }
     }
 
@@ -423,8 +449,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     }
     int npop = 0;
     uint32_t last = 0xFFFFFFFFu, kth = 0, next = 0;
-    const int rounds = k + 1;
-    for (int r = 0; r < rounds; ++r) {
+    for (int r = 0; r <= k; ++r) {
       const uint32_t h = t1;
       const uint32_t m = group_max_u32<LPT>(h);
       if (r == k - 1) kth = m;
@@ -493,16 +518,22 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   lds_barrier();
 
   // ---- one global atomic per expert per workgroup, then the completion ticket ----------------
+  // Workgroups exchange data only through device-scope atomics, which are coherent across the
+  // XCDs' L2 caches without a fence.  Each thread waits for the pre-op values of its counter
+  // updates (so they have been performed) before the barrier; only then does thread 0 take the
+  // ticket.  The workgroup that takes the last ticket therefore reads complete counters with its
+  // own atomics.  This avoids an agent-scope fence per workgroup, which on gfx950 writes back and
+  // invalidates the whole L2 and serialises across the workgroups.
+  int done = 0;
   for (int e = tid; e < E; e += kThreads) {
     const int v = hist[e];
-    if (v) atomicAdd(&p.ws_acc[e], v);
+    if (v) done |= atomicAdd(&p.ws_acc[e], v);
   }
-  __threadfence();
+  if (done < 0) s_flag = -1;                   // never true (counters stay below 2^31); uses the values
   __syncthreads();
   if (tid == 0) s_flag = (atomicAdd(p.ws_ticket, 1u) == p.nblocks - 1) ? 1 : 0;
   __syncthreads();
-  if (!s_flag) return;
-  __threadfence();
+  if (s_flag != 1) return;
 
   // ---- last workgroup: counts, rank fold, max/mean; leaves the workspace zeroed -------------
   int32_t* rl = reinterpret_cast<int32_t*>(smem);
@@ -532,7 +563,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   if (lane == 0) { s_red[wave][0] = mx; s_red[wave][1] = sum; }
   __syncthreads();
   if (tid == 0) {
-    for (int w = 1; w < kThreads / 64; ++w) {
+    for (int w = 1; w < kWaves; ++w) {
       mx = s_red[w][0] > mx ? s_red[w][0] : mx;
       sum += s_red[w][1];
     }
@@ -547,6 +578,21 @@ __global__ void zero_kernel(uint32_t* p, size_t n) {
     p[i] = 0u;
 }
 
+int epad_of(int32_t E) {
+  return E <= 32 ? 32 : E <= 64 ? 64 : E <= 128 ? 128 : 256;
+}
+
+template <int EPAD>
+int launch_pack_cfg(const void* w, int32_t E, int32_t Hbytes, void* out, void* stream) {
+  const int32_t nst = (Hbytes + kStageRowBytes - 1) / kStageRowBytes;
+  const int64_t units = (int64_t)nst * EPAD * 8;
+  const int64_t blocks64 = (units + 255) / 256;
+  const int blocks = (int)(blocks64 < 4096 ? (blocks64 > 0 ? blocks64 : 1) : 4096);
+  hipLaunchKernelGGL((pack_kernel<EPAD>), dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<const char*>(w), E, Hbytes, nst, static_cast<u32x4*>(out));
+  return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
+}
+
 template <bool BF16, int EPAD>
 int launch_cfg(const PredictLaunch& a) {
   using Cfg = TileCfg<EPAD>;
@@ -556,7 +602,7 @@ int launch_cfg(const PredictLaunch& a) {
   p.T = a.T;
   p.Hbytes = a.H * elem;
   p.ldx_bytes = (int32_t)(a.ld_hidden * elem);
-  p.w = static_cast<const char*>(a.router_w);
+  p.wpack = static_cast<const char*>(a.router_packed);
   p.E = a.E;
   p.logit_bias = a.logit_bias;
   p.select_bias = a.select_bias;
@@ -577,7 +623,6 @@ int launch_cfg(const PredictLaunch& a) {
   const int64_t tiles = (a.T + Cfg::BM - 1) / Cfg::BM;
   p.nblocks = (uint32_t)(tiles > 0 ? tiles : 1);
   p.nstages = (p.Hbytes + kStageRowBytes - 1) / kStageRowBytes;
-  p.tail_half = (p.Hbytes % kStageRowBytes) != 0;
   hipLaunchKernelGGL((predict_kernel<BF16, EPAD>), dim3(p.nblocks), dim3(kThreads), 0,
                      static_cast<hipStream_t>(a.stream), p);
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
@@ -585,14 +630,32 @@ int launch_cfg(const PredictLaunch& a) {
 
 template <bool BF16>
 int launch_dtype(const PredictLaunch& a) {
-  if (a.E <= 16) return launch_cfg<BF16, 16>(a);
-  if (a.E <= 32) return launch_cfg<BF16, 32>(a);
-  if (a.E <= 64) return launch_cfg<BF16, 64>(a);
-  if (a.E <= 128) return launch_cfg<BF16, 128>(a);
-  return launch_cfg<BF16, 256>(a);
+  switch (epad_of(a.E)) {
+    case 32: return launch_cfg<BF16, 32>(a);
+    case 64: return launch_cfg<BF16, 64>(a);
+    case 128: return launch_cfg<BF16, 128>(a);
+    default: return launch_cfg<BF16, 256>(a);
+  }
 }
 
 }  // namespace
+
+size_t router_packed_bytes(int32_t E, int32_t H, int32_t dtype) {
+  const int64_t Hbytes = (int64_t)H * (dtype == FB_BF16 ? 2 : 4);
+  const int64_t nst = (Hbytes + kStageRowBytes - 1) / kStageRowBytes;
+  return (size_t)(nst * epad_of(E) * kStageRowBytes);
+}
+
+int launch_pack(const void* router_w, int32_t E, int32_t H, int32_t dtype, void* packed, void* stream) {
+  (void)hipGetLastError();
+  const int32_t Hbytes = H * (dtype == FB_BF16 ? 2 : 4);
+  switch (epad_of(E)) {
+    case 32: return launch_pack_cfg<32>(router_w, E, Hbytes, packed, stream);
+    case 64: return launch_pack_cfg<64>(router_w, E, Hbytes, packed, stream);
+    case 128: return launch_pack_cfg<128>(router_w, E, Hbytes, packed, stream);
+    default: return launch_pack_cfg<256>(router_w, E, Hbytes, packed, stream);
+  }
+}
 
 int launch_predict(const PredictLaunch& a) {
   (void)hipGetLastError();

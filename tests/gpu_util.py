@@ -37,7 +37,9 @@ def scoring_of(wl) -> fb.Scoring:
     return fb.Scoring(wl.kind, wl.k, wl.n_group, wl.topk_group, wl.group_topn)
 
 
-def run_gpu(li, wl, e2r=None, R=None, debug=True, predictor=None, logit_bias=None):
+def run_gpu(li, wl, e2r=None, R=None, debug=True, predictor=None, logit_bias=None, packed=False):
+    """One prediction through the binding; packed=True packs the router weight first and calls
+    fb_predict_load_packed (the launch the benchmark times), else fb_predict_load."""
     if e2r is None:
         _, e2r = contiguous_placement(wl.E, wl.R, wl.S)
     R = wl.R if R is None else R
@@ -47,6 +49,8 @@ def run_gpu(li, wl, e2r=None, R=None, debug=True, predictor=None, logit_bias=Non
     lb = None if logit_bias is None else torch.from_numpy(np.asarray(logit_bias, np.float32)).cuda()
     e2r_t = torch.from_numpy(np.asarray(e2r, np.int32)).cuda()
     pred = predictor or fb.Predictor()
+    if packed:
+        w = fb.pack_router_weight(w)
     out = pred.predict_load(x, w, scoring_of(wl), e2r_t, R, select_bias=sb, logit_bias=lb,
                             return_topk=debug, return_logits=debug)
     torch.cuda.synchronize()

@@ -28,9 +28,10 @@ def _declared_functions():
 
 def test_header_declares_the_boundary():
     names = _declared_functions()
-    assert names == sorted(["fb_abi_version", "fb_status_string", "fb_predict_workspace_bytes",
-                            "fb_predict_workspace_init", "fb_predict_load", "fb_plan_swaps",
-                            "fb_plan_swaps_device", "fb_swap_budget_from_cost"])
+    assert names == sorted(["fb_abi_version", "fb_status_string", "fb_router_packed_bytes",
+                            "fb_predict_workspace_bytes", "fb_predict_workspace_init",
+                            "fb_pack_router_weight", "fb_predict_load", "fb_predict_load_packed",
+                            "fb_plan_swaps", "fb_plan_swaps_device", "fb_swap_budget_from_cost"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -48,11 +49,52 @@ def test_struct_layouts_match_header():
 
 def test_version_and_status_strings():
     lib = fb.lib()
-    assert lib.fb_abi_version() == 1
+    assert lib.fb_abi_version() == 2
     for code in (0, -1, -2, -3, -4):
         assert L.status_string(code).startswith("FB_")
     assert "unknown" in L.status_string(7)
-    assert lib.fb_predict_workspace_bytes() >= 1028
+
+
+
+@pytest.mark.parametrize("E,H,dtype", [(1, 32, L.FB_BF16), (8, 4096, L.FB_BF16), (60, 2048, L.FB_BF16),
+                                       (128, 2048, L.FB_BF16), (256, 7168, L.FB_BF16),
+                                       (256, 7168, L.FB_F32), (33, 48, L.FB_F32)])
+def test_packed_router_and_workspace_sizes(E, H, dtype):
+    """The packed weight holds E rounded up to 32, 64, 128 or 256 rows of H elements rounded up
+    to whole 128-byte stages; the unpacked entry point's workspace adds 2 KB of accumulators."""
+    lib = fb.lib()
+    hb = H * (2 if dtype == L.FB_BF16 else 4)
+    epad = next(p for p in (32, 64, 128, 256) if E <= p)
+    packed = lib.fb_router_packed_bytes(E, H, dtype)
+    assert packed == epad * (-(-hb // 128)) * 128
+    assert lib.fb_predict_workspace_bytes(E, H, dtype) == packed + 2048
+
+
+def test_packed_sizes_reject_invalid():
+    lib = fb.lib()
+    assert lib.fb_router_packed_bytes(0, 64, L.FB_BF16) == 0
+    assert lib.fb_router_packed_bytes(257, 64, L.FB_BF16) == 0
+    assert lib.fb_router_packed_bytes(8, 0, L.FB_BF16) == 0
+    assert lib.fb_router_packed_bytes(8, 64, 5) == 0
+    assert lib.fb_predict_workspace_bytes(300, 64, L.FB_BF16) == 0
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(w=None), L.FB_EINVAL),
+    (dict(out=None), L.FB_EINVAL),
+    (dict(E=0), L.FB_EINVAL),
+    (dict(dtype=3), L.FB_EINVAL),
+    (dict(E=257), L.FB_EUNSUPPORTED),
+    (dict(H=48), L.FB_EUNSUPPORTED),
+    (dict(w=0x2004), L.FB_EUNSUPPORTED),
+    (dict(out=0x3008), L.FB_EUNSUPPORTED),
+    (dict(nbytes=4095), L.FB_ENOSPC),
+])
+def test_pack_validation_without_gpu(over, code):
+    a = dict(w=0x2000, E=16, H=64, dtype=L.FB_BF16, out=0x3000, nbytes=4096)
+    a.update(over)
+    assert fb.lib().fb_pack_router_weight(a["w"], a["E"], a["H"], a["dtype"], a["out"], a["nbytes"],
+                                          None) == code
 
 
 def _host(counts, slots, **kw):
@@ -177,7 +219,7 @@ def _predict_call(**over):
     """fb_predict_load with fake (never dereferenced) pointers; every case must fail validation."""
     a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, w=0x2000, E=16, lb=None, sb=None,
              sc=fb.Scoring("softmax", 2).to_c(), e2r=0x3000, R=4, counts=0x4000, rl=0x5000,
-             mm=0x6000, ws=0x7000, wsb=4096, topk=None, logits=None, stream=None)
+             mm=0x6000, ws=0x7000, wsb=1 << 20, topk=None, logits=None, stream=None)
     a.update(over)
     sc = a["sc"]
     return fb.lib().fb_predict_load(a["hidden"], a["T"], a["H"], a["ld"], a["dtype"], a["w"], a["E"],
@@ -214,6 +256,38 @@ def _predict_call(**over):
 ])
 def test_predict_validation_without_gpu(over, code):
     assert _predict_call(**over) == code
+
+
+def _predict_packed_call(**over):
+    """fb_predict_load_packed with fake (never dereferenced) pointers."""
+    a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, wp=0x2000, wpb=4096, E=16, lb=None,
+             sb=None, sc=fb.Scoring("softmax", 2).to_c(), e2r=0x3000, R=4, counts=0x4000,
+             rl=0x5000, mm=0x6000, ws=0x7000, wsb=2048, topk=None, logits=None, stream=None)
+    a.update(over)
+    sc = a["sc"]
+    return fb.lib().fb_predict_load_packed(
+        a["hidden"], a["T"], a["H"], a["ld"], a["dtype"], a["wp"], a["wpb"], a["E"], a["lb"],
+        a["sb"], ctypes.byref(sc) if sc is not None else None, a["e2r"], a["R"], a["counts"],
+        a["rl"], a["mm"], a["ws"], a["wsb"], a["topk"], a["logits"], a["stream"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(wp=None), L.FB_EINVAL),
+    (dict(wp=0x2008), L.FB_EUNSUPPORTED),
+    (dict(wpb=4095), L.FB_ENOSPC),                       # packed weight too small for E, H
+    (dict(E=33), L.FB_ENOSPC),                           # 33 experts pack into 64 rows
+    (dict(wsb=2047), L.FB_ENOSPC),                       # accumulators need 2 KB
+    (dict(sc=None), L.FB_EINVAL),
+    (dict(T=-2), L.FB_EINVAL),
+    (dict(H=48), L.FB_EUNSUPPORTED),
+    (dict(sb=0x8000), L.FB_EINVAL),
+])
+def test_predict_packed_validation_without_gpu(over, code):
+    assert _predict_packed_call(**over) == code
+
+
+def test_unpacked_predict_needs_room_for_the_packed_weight():
+    assert _predict_call(wsb=2048 + 4096 - 1) == L.FB_ENOSPC
 
 
 def test_device_planner_validation_without_gpu():

@@ -164,7 +164,7 @@ def test_workspace_is_left_clean_across_shapes():
         li = make_layer(wl, 0)
         a = run_gpu(li, wl, e2r, predictor=pred)
         check_counts_consistent(a, wl, e2r)
-    ws = pred.workspace.cpu().numpy()
+    ws = pred.workspace[:2048].cpu().numpy()    # accumulators + ticket; the rest holds the packed weight
     assert not ws.any()
 
 
@@ -175,8 +175,8 @@ def test_full_size_dsv3(layer):
     _, e2r = contiguous_placement(wl.E, wl.R, wl.S)
     _say(f"[full] dsv3 layer {layer}: generating inputs")
     li = make_layer(wl, layer)
-    _say("[full] bench-configuration run (no debug outputs)")
-    plain = run_gpu(li, wl, e2r, debug=False)
+    _say("[full] bench-configuration run (packed router, no debug outputs)")
+    plain = run_gpu(li, wl, e2r, debug=False, packed=True)
     dbg = run_gpu(li, wl, e2r, debug=True)
     assert np.array_equal(plain["counts"], dbg["counts"])
     check_counts_consistent(dbg, wl, e2r)
@@ -186,6 +186,50 @@ def test_full_size_dsv3(layer):
     _say(f"[full] oracle on {rows.size} sampled tokens")
     stats = check_prediction(dbg, li, wl, e2r, rows=rows, label="dsv3-full")
     _say(f"[full] ok {stats}")
+
+
+def _pack_reference(w_bytes: np.ndarray, E: int, row_bytes: int) -> np.ndarray:
+    """The packed layout of fb_pack_router_weight, written from its description in the header."""
+    epad = next(p for p in (32, 64, 128, 256) if E <= p)
+    W = 4 if epad >= 128 else (2 if epad == 64 else 1)
+    F = epad // (32 * W)
+    nst = -(-row_bytes // 128)
+    src = np.zeros((epad, nst * 128), np.uint8)
+    src[:E, :row_bytes] = w_bytes.reshape(E, row_bytes)
+    out = np.zeros((nst, epad // 8, 64, 16), np.uint8)
+    for st in range(nst):
+        for c in range(epad // 8):
+            f, q, w = c % F, (c // F) % 4, c // (4 * F)
+            for l in range(64):
+                row = w * (epad // W) + f * 32 + (l % 32)
+                b = st * 128 + q * 32 + (l // 32) * 16
+                out[st, c, l] = src[row, b:b + 16]
+    return out.reshape(-1)
+
+
+@pytest.mark.parametrize("E,H,dtype", [(8, 4096, "bf16"), (20, 96, "f32"), (60, 2048, "bf16"),
+                                       (128, 2080, "bf16"), (256, 7168, "bf16"), (256, 160, "f32")])
+def test_pack_layout_and_packed_predict(E, H, dtype):
+    """fb_pack_router_weight writes exactly the documented layout (byte-exact), and
+    fb_predict_load_packed returns bit-identical results to fb_predict_load."""
+    _say(f"[pack] E={E} H={H} {dtype}")
+    base = CONFIGS["dsv3" if E == 256 else "qwen3"]
+    wl = dataclasses.replace(base.with_T(300), H=H, E=E, dtype=dtype, n_clusters=E,
+                             k=min(base.k, max(1, E // 4)))
+    e2r = np.arange(E, dtype=np.int32) % wl.R
+    li = make_layer(wl, 0)
+    w = to_device(li.w, dtype)
+    pk = fb.pack_router_weight(w)
+    torch.cuda.synchronize()
+    got = pk.data.cpu().numpy()
+    ref = _pack_reference(np.ascontiguousarray(li.w).view(np.uint8), E, H * (2 if dtype == "bf16" else 4))
+    assert got.size == ref.size and np.array_equal(got, ref)
+    a = run_gpu(li, wl, e2r, packed=False)
+    b = run_gpu(li, wl, e2r, packed=True)
+    for key in ("counts", "rank_loads", "topk"):
+        assert np.array_equal(a[key], b[key]), key
+    assert a["max_mean"] == b["max_mean"]
+    assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
 
 
 def test_qwen3_layers_back_to_back():
