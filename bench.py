@@ -153,7 +153,16 @@ def main():
     k_end.record(stream)
     torch.cuda.synchronize()
     avg_kernel_s = k_start.elapsed_time(k_end) / K / 1e3
-    fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
+
+    # the device planner alone, K launches back to back on the final counts
+    p_start = torch.cuda.Event(enable_timing=True)
+    p_end = torch.cuda.Event(enable_timing=True)
+    p_start.record(stream)
+    for i in range(K):
+        fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
+    p_end.record(stream)
+    torch.cuda.synchronize()
+    plan_ms = p_start.elapsed_time(p_end) / K
 
     counts = out.counts.cpu().numpy()
     host_plan = plan.to_host()
@@ -200,7 +209,7 @@ def main():
                      "bytes_per_launch": nbytes, "kernel_ms": avg_kernel_s * 1e3,
                      "mfma": {"achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                               "frac": tflops / PEAK_BF16_TFLOPS}},
-        "plan": {"swaps": len(host_plan.swaps),
+        "plan": {"swaps": len(host_plan.swaps), "kernel_ms": plan_ms,
                  "max_mean_before": float(out.max_mean.item()),
                  "max_mean_after": float(host_plan.rank_loads.max() * wl.R / host_plan.rank_loads.sum())},
     }

@@ -1,11 +1,23 @@
 // Budgeted greedy expert-swap planner as one stream-ordered workgroup (gfx950).
 //
 // Same algorithm and tie-breaks as the host planner (Sec. "Budgeted Expert-Swap Planning",
-// Eq. 6-8, Alg. 1): every round finds the most and least loaded ranks, evaluates every admissible
-// candidate in parallel (one thread per candidate, exact integer benefit
-// den * (M - M') + num * 2d (L_b - L_a - d)), reduces to the best candidate under the ordering
-// (benefit desc, src rank, dst rank, item ids asc), and one thread applies it.  State lives in LDS;
-// the only global traffic is the input tables and the outputs.
+// Eq. 6-8, Alg. 1).  Every round: wave 0 finds the most and least loaded ranks and the loads the
+// benefit needs (64-bit wave reductions over packed (load, rank) keys), every thread evaluates its
+// share of the admissible candidates with the exact integer benefit
+//     den * (M - M') + num * 2d (L_b - L_a - d),
+// the best candidate under (benefit desc, src rank, dst rank, item ids asc) is found with two
+// packed-key reductions, and thread 0 applies it.  State lives in LDS.
+//
+// The benefit fits an int64: the launcher checks den N + 4 num N^2 <= INT64_MAX once, and each
+// term and partial product is bounded by it (0 <= M' <= N, |d| <= N, |L_b - L_a - d| <= N).
+//
+// Two kernels:
+//   * plan_frontier_wave, one wave, for frontier mode with S * S <= 64 (the common case).  Rank
+//     loads live in registers (ranks lane + 64 m), each lane owns one candidate (p, q), slot entries
+//     carry the item, its moved flag and its count so that a candidate costs one LDS round trip,
+//     and a round is a handful of wave reductions with no workgroup barrier.
+//   * plan_general<NT> for everything else (full mode, larger S): state in LDS, threads split the
+//     candidates by rank pair, per-wave reductions combined through LDS.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -14,198 +26,518 @@
 namespace fb {
 namespace {
 
-constexpr int kPlanThreads = 256;
 constexpr int kMaxRS = FB_MAX_SLOTS_TOTAL;
 constexpr int kMaxR = FB_MAX_RANKS;
+constexpr int kRankBits = 11;                 // R <= 1024 < 2^11
+constexpr int kItemBits = 13;                 // item ids < E + R * S <= 8192
+constexpr int64_t kLoadCap = (int64_t)1 << 43;  // loads <= 4096 experts * (2^31 - 1) < 2^43
 
-typedef __int128 i128;
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
+  return ((uint64_t)hi << 32) | lo;
+}
 
-struct Cand {
-  int64_t gain;   // exact: bounded by the host-side overflow check
-  int64_t i, j;   // item ids
-  int32_t a, b, p, q;
-  int32_t found;
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+// Maximum over the 64 lanes of a wave (every lane must be active); uniform result.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+  v = umax64(v, dpp_u64<0xB1>(v));    // quad_perm [1,0,3,2]
+  v = umax64(v, dpp_u64<0x4E>(v));    // quad_perm [2,3,0,1]
+  v = umax64(v, dpp_u64<0x141>(v));   // row_half_mirror
+  v = umax64(v, dpp_u64<0x140>(v));   // row_mirror
+  return umax64(umax64(readlane_u64(v, 0), readlane_u64(v, 16)),
+                umax64(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
+
+// (load, rank) keys: the largest key is the largest load, lowest rank id on ties.
+__device__ __forceinline__ uint64_t key_max(int64_t load, int r) {
+  return ((uint64_t)load << kRankBits) | (uint64_t)((1 << kRankBits) - 1 - r);
+}
+// ... and the smallest load, lowest rank id on ties.
+__device__ __forceinline__ uint64_t key_min(int64_t load, int r) {
+  return ((uint64_t)(kLoadCap - load) << kRankBits) | (uint64_t)((1 << kRankBits) - 1 - r);
+}
+__device__ __forceinline__ int key_rank(uint64_t key) {
+  return (1 << kRankBits) - 1 - (int)(key & ((1u << kRankBits) - 1));
+}
+
+// Tie order after the benefit: (src rank, dst rank, item i, item j) ascending, as one integer.
+__device__ __forceinline__ uint64_t tie_key(int a, int b, int i, int j) {
+  return ((uint64_t)a << (kRankBits + 2 * kItemBits)) | ((uint64_t)b << (2 * kItemBits)) |
+         ((uint64_t)i << kItemBits) | (uint64_t)j;
+}
+
+struct Shared {
+  int32_t item[kMaxRS];          // slot -> item (expert id, or E + slot for an empty slot)
+  int32_t pos[2 * kMaxRS];       // item -> slot
+  int32_t cnt[kMaxRS];           // expert -> count
+  int32_t seen[kMaxRS];
+  int64_t L[kMaxR];
+  int32_t part[kMaxR];
+  uint8_t moved[2 * kMaxRS];
+  uint64_t wgain[16], wtie[16];
+  int64_t N;
+  int32_t bad, stop, amax, amin, top[3], ns;
+  int64_t other;
 };
 
-__device__ __forceinline__ bool cand_better(const Cand& x, const Cand& y) {
-  if (!x.found) return false;
-  if (!y.found) return true;
-  if (x.gain != y.gain) return x.gain > y.gain;
-  if (x.a != y.a) return x.a < y.a;
-  if (x.b != y.b) return x.b < y.b;
-  if (x.i != y.i) return x.i < y.i;
-  return x.j < y.j;
-}
-
-// (value, rank) order used for the frontier: larger load first, lower rank id on ties.
-__device__ __forceinline__ bool load_before(int64_t lv, int32_t lr, int64_t rv, int32_t rr) {
-  return lv > rv || (lv == rv && lr < rr);
-}
-
-__global__ __launch_bounds__(kPlanThreads, 1) void plan_kernel(PlanDeviceLaunch a) {
-  __shared__ int32_t item[kMaxRS];
-  __shared__ int32_t cnt[kMaxRS];
-  __shared__ uint8_t moved[2 * kMaxRS];
-  __shared__ int64_t L[kMaxR];
-  __shared__ int32_t part[kMaxR];
-  __shared__ int32_t seen[kMaxRS];
-  __shared__ Cand red[kPlanThreads];
-  __shared__ int32_t s_bad, s_stop, s_amax, s_amin, s_top[3], s_ns;
-  __shared__ int64_t s_N;
-
+template <int NT>
+__global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
+  __shared__ Shared sh;
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int E = a.E, R = a.R, S = a.S, RS = R * S;
   const fb_budget bg = a.budget;
 
-  if (tid == 0) { s_bad = 0; s_ns = 0; s_N = 0; }
-  for (int e = tid; e < E; e += kPlanThreads) { seen[e] = 0; cnt[e] = a.counts[e]; }
-  for (int c = tid; c < E + RS; c += kPlanThreads) moved[c] = 0;
-  for (int r = tid; r < R; r += kPlanThreads) part[r] = 0;
+  if (tid == 0) { sh.bad = 0; sh.ns = 0; sh.N = 0; }
+  for (int e = tid; e < E; e += NT) { sh.seen[e] = 0; sh.cnt[e] = a.counts[e]; }
+  for (int c = tid; c < E + RS; c += NT) sh.moved[c] = 0;
+  for (int r = tid; r < R; r += NT) sh.part[r] = 0;
   __syncthreads();
-  for (int c = tid; c < RS; c += kPlanThreads) {
+  for (int c = tid; c < RS; c += NT) {
     const int e = a.slot_expert[c];
-    if (e == -1) item[c] = E + c;
-    else if (e < 0 || e >= E) s_bad = 1;
-    else { item[c] = e; atomicAdd(&seen[e], 1); }
+    if (e == -1) { sh.item[c] = E + c; sh.pos[E + c] = c; }
+    else if (e < 0 || e >= E) sh.bad = 1;
+    else { sh.item[c] = e; sh.pos[e] = c; atomicAdd(&sh.seen[e], 1); }
   }
   __syncthreads();
-  for (int e = tid; e < E; e += kPlanThreads)
-    if (seen[e] != 1 || cnt[e] < 0) s_bad = 1;
+  for (int e = tid; e < E; e += NT)
+    if (sh.seen[e] != 1 || sh.cnt[e] < 0) sh.bad = 1;
   __syncthreads();
-  if (s_bad) {
+  if (sh.bad) {
     if (tid == 0) { *a.n_swaps = 0; *a.status = FB_EINVAL; }
     return;
   }
 
-  auto load_of = [&](int64_t it) -> int64_t { return it < E ? (int64_t)cnt[it] : 0; };
-  for (int r = tid; r < R; r += kPlanThreads) {
+  auto load_of = [&](int it) -> int64_t { return it < E ? (int64_t)sh.cnt[it] : 0; };
+  for (int r = tid; r < R; r += NT) {
     int64_t v = 0;
-    for (int s = 0; s < S; ++s) v += load_of(item[r * S + s]);
-    L[r] = v;
-    atomicAdd((unsigned long long*)&s_N, (unsigned long long)v);
+    for (int s = 0; s < S; ++s) v += load_of(sh.item[r * S + s]);
+    sh.L[r] = v;
+    atomicAdd((unsigned long long*)&sh.N, (unsigned long long)v);
   }
   __syncthreads();
-  const int64_t N = s_N;
-  i128 g_num = bg.gamma_num, g_den = bg.gamma_den;
+  const int64_t N = sh.N;
+  int64_t g_num = bg.gamma_num, g_den = bg.gamma_den;
   if (g_den == 0) { g_num = N > 0 ? 1 : 0; g_den = N > 0 ? N : 1; }
-  const i128 bound = g_den * (i128)N + g_num * 4 * (i128)N * (i128)N;
-  if (bound > (i128)INT64_MAX) {
+  const __int128 bound = (__int128)g_den * N + (__int128)g_num * 4 * (__int128)N * N;
+  if (bound > (__int128)INT64_MAX) {
     if (tid == 0) { *a.n_swaps = 0; *a.status = FB_EUNSUPPORTED; }
     return;
   }
 
+  const bool frontier = bg.mode == FB_FRONTIER;
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
   for (int round = 0; active && round < bg.max_swaps; ++round) {
-    // ---- frontier: wave 0 finds argmax, argmin and the three largest loads --------------------
-    if (tid < 64) {
-      int64_t bv = INT64_MIN; int32_t br = 0x7fffffff;    // argmax (lowest id on ties)
-      int64_t mv = INT64_MAX; int32_t mr = 0x7fffffff;    // argmin (lowest id on ties)
-      for (int r = tid; r < R; r += 64) {
-        if (load_before(L[r], r, bv, br)) { bv = L[r]; br = r; }
-        if (L[r] < mv || (L[r] == mv && r < mr)) { mv = L[r]; mr = r; }
+    // ---- wave 0: argmax, argmin and the loads of the ranks outside a candidate pair ------------
+    if (wave == 0) {
+      uint64_t kmax = 0, kmin = 0;
+      for (int r = lane; r < R; r += 64) {
+        kmax = umax64(kmax, key_max(sh.L[r], r));
+        kmin = umax64(kmin, key_min(sh.L[r], r));
       }
-      for (int off = 32; off > 0; off >>= 1) {
-        const int64_t ov = __shfl_xor(bv, off); const int32_t orr = __shfl_xor(br, off);
-        if (load_before(ov, orr, bv, br)) { bv = ov; br = orr; }
-        const int64_t om = __shfl_xor(mv, off); const int32_t omr = __shfl_xor(mr, off);
-        if (om < mv || (om == mv && omr < mr)) { mv = om; mr = omr; }
+      kmax = wave_max_u64(kmax);
+      kmin = wave_max_u64(kmin);
+      const int amax = key_rank(kmax), amin = key_rank(kmin);
+      if (frontier) {
+        // the largest load among ranks other than amax and amin (0 = there is none)
+        uint64_t ko = 0;
+        for (int r = lane; r < R; r += 64)
+          if (r != amax && r != amin) ko = umax64(ko, (uint64_t)sh.L[r] + 1);
+        ko = wave_max_u64(ko);
+        if (lane == 0) sh.other = ko ? (int64_t)ko - 1 : INT64_MIN;
+      } else {
+        // the three largest (load, rank) keys, for the largest load outside any pair
+        uint64_t k1 = 0, k2 = 0;
+        const int t0 = amax;
+        for (int r = lane; r < R; r += 64)
+          if (r != t0) k1 = umax64(k1, key_max(sh.L[r], r));
+        k1 = wave_max_u64(k1);
+        const int t1 = k1 ? key_rank(k1) : -1;
+        for (int r = lane; r < R; r += 64)
+          if (r != t0 && r != t1) k2 = umax64(k2, key_max(sh.L[r], r));
+        k2 = wave_max_u64(k2);
+        if (lane == 0) { sh.top[0] = t0; sh.top[1] = t1; sh.top[2] = k2 ? key_rank(k2) : -1; }
       }
-      int32_t top[3] = {br, -1, -1};
-      for (int u = 1; u < 3; ++u) {
-        int64_t tv = INT64_MIN; int32_t tr = 0x7fffffff;
-        for (int r = tid; r < R; r += 64) {
-          bool used = false;
-          for (int w = 0; w < u; ++w) used |= (top[w] == r);
-          if (!used && load_before(L[r], r, tv, tr)) { tv = L[r]; tr = r; }
-        }
-        for (int off = 32; off > 0; off >>= 1) {
-          const int64_t ov = __shfl_xor(tv, off); const int32_t orr = __shfl_xor(tr, off);
-          if (load_before(ov, orr, tv, tr)) { tv = ov; tr = orr; }
-        }
-        top[u] = (tr == 0x7fffffff) ? -1 : tr;
-      }
-      if (tid == 0) {
-        s_amax = br; s_amin = mr;
-        s_top[0] = top[0]; s_top[1] = top[1]; s_top[2] = top[2];
-        s_stop = (L[br] - L[mr] <= bg.tau) ? 1 : 0;
+      if (lane == 0) {
+        sh.amax = amax;
+        sh.amin = amin;
+        sh.stop = (sh.L[amax] - sh.L[amin] <= bg.tau) ? 1 : 0;
       }
     }
     __syncthreads();
-    if (s_stop) break;
+    if (sh.stop) break;
 
-    // ---- candidates, one per thread-iteration --------------------------------------------------
-    const int amax = s_amax, amin = s_amin;
-    const int64_t M = L[amax];
-    Cand best; best.found = 0; best.gain = 0; best.i = best.j = 0; best.a = best.b = best.p = best.q = 0;
-    const int64_t ncand = bg.mode == FB_FRONTIER ? (int64_t)S * S : (int64_t)R * R * S * S;
-    for (int64_t idx = tid; idx < ncand; idx += kPlanThreads) {
-      int ra, rb, p, q;
-      if (bg.mode == FB_FRONTIER) {
-        ra = amax; rb = amin; p = (int)(idx / S); q = (int)(idx % S);
-      } else {
-        const int64_t pair = idx / ((int64_t)S * S), pq = idx % ((int64_t)S * S);
-        ra = (int)(pair / R); rb = (int)(pair % R); p = (int)(pq / S); q = (int)(pq % S);
-        if (!(L[ra] > L[rb])) continue;
-      }
-      if (bg.per_rank_cap && (part[ra] >= bg.per_rank_cap || part[rb] >= bg.per_rank_cap)) continue;
-      const int64_t i = item[ra * S + p], j = item[rb * S + q];
-      if (moved[i] || moved[j] || (i >= E && j >= E)) continue;
-      int64_t other = INT64_MIN;
-      for (int u = 0; u < 3; ++u) {
-        const int tr = s_top[u];
-        if (tr >= 0 && tr != ra && tr != rb) { other = L[tr]; break; }
-      }
+    // ---- candidates ----------------------------------------------------------------------------
+    const int amax = sh.amax, amin = sh.amin;
+    const int64_t M = sh.L[amax];
+    uint64_t bgain = 0, btie = 0;     // gain 0: nothing found (every accepted gain is > 0)
+    auto consider = [&](int ra, int rb, int p, int q, int64_t other) {
+      const int i = sh.item[ra * S + p], j = sh.item[rb * S + q];
+      if (sh.moved[i] || sh.moved[j] || (i >= E && j >= E)) return;
+      const int64_t La = sh.L[ra], Lb = sh.L[rb];
       const int64_t d = load_of(j) - load_of(i);
-      const int64_t la = L[ra] + d, lb = L[rb] - d;
+      const int64_t la = La + d, lb = Lb - d;
       int64_t m2 = la > lb ? la : lb;
       if (other > m2) m2 = other;
-      const i128 gain = g_den * (i128)(M - m2) + g_num * 2 * (i128)d * (i128)(L[rb] - L[ra] - d);
-      if (gain <= 0) continue;
-      Cand c; c.found = 1; c.gain = (int64_t)gain; c.i = i; c.j = j; c.a = ra; c.b = rb; c.p = p; c.q = q;
-      if (cand_better(c, best)) best = c;
+      const int64_t spread = g_num ? g_num * (2 * d * (Lb - La - d)) : 0;
+      const int64_t gain = g_den * (M - m2) + spread;
+      if (gain <= 0) return;
+      const uint64_t tk = tie_key(ra, rb, i, j);
+      if ((uint64_t)gain > bgain || ((uint64_t)gain == bgain && tk < btie)) { bgain = (uint64_t)gain; btie = tk; }
+    };
+    const bool capped = bg.per_rank_cap != 0;
+    if (frontier) {
+      if (!(capped && (sh.part[amax] >= bg.per_rank_cap || sh.part[amin] >= bg.per_rank_cap))) {
+        const int64_t other = sh.other;
+        for (int idx = tid; idx < S * S; idx += NT) {
+          const int p = idx / S;
+          consider(amax, amin, p, idx - p * S, other);
+        }
+      }
+    } else {
+      for (int pair = tid; pair < R * R; pair += NT) {
+        const int ra = pair / R, rb = pair - ra * R;
+        if (!(sh.L[ra] > sh.L[rb])) continue;
+        if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) continue;
+        int64_t other = INT64_MIN;
+        for (int u = 0; u < 3; ++u) {
+          const int tr = sh.top[u];
+          if (tr >= 0 && tr != ra && tr != rb) { other = sh.L[tr]; break; }
+        }
+        for (int p = 0; p < S; ++p)
+          for (int q = 0; q < S; ++q) consider(ra, rb, p, q, other);
+      }
     }
-    red[tid] = best;
-    __syncthreads();
-    for (int stride = kPlanThreads / 2; stride > 0; stride >>= 1) {
-      if (tid < stride && cand_better(red[tid + stride], red[tid])) red[tid] = red[tid + stride];
+    // best of the wave: largest gain, then smallest tie key
+    const uint64_t wg = wave_max_u64(bgain);
+    const uint64_t wt = ~wave_max_u64((wg != 0 && bgain == wg) ? ~btie : 0ull);
+    uint64_t g = wg, t = wt;
+    if (NT > 64) {
+      if (lane == 0) { sh.wgain[wave] = wg; sh.wtie[wave] = wt; }
       __syncthreads();
+      g = sh.wgain[0]; t = sh.wtie[0];
+      for (int w = 1; w < NT / 64; ++w) {
+        const uint64_t og = sh.wgain[w], ot = sh.wtie[w];
+        if (og > g || (og == g && og != 0 && ot < t)) { g = og; t = ot; }
+      }
     }
-    if (!red[0].found) break;
+    if (g == 0) break;                          // no admissible candidate with positive benefit
     if (tid == 0) {
-      const Cand c = red[0];
-      const int64_t d = load_of(c.j) - load_of(c.i);
-      item[c.a * S + c.p] = (int32_t)c.j;
-      item[c.b * S + c.q] = (int32_t)c.i;
-      L[c.a] += d;
-      L[c.b] -= d;
-      moved[c.i] = 1; moved[c.j] = 1;
-      ++part[c.a]; ++part[c.b];
+      const int ca = (int)(t >> (kRankBits + 2 * kItemBits)) & ((1 << kRankBits) - 1);
+      const int cb = (int)(t >> (2 * kItemBits)) & ((1 << kRankBits) - 1);
+      const int ci = (int)(t >> kItemBits) & ((1 << kItemBits) - 1);
+      const int cj = (int)t & ((1 << kItemBits) - 1);
+      const int sa = sh.pos[ci], sb = sh.pos[cj];
+      const int64_t d = load_of(cj) - load_of(ci);
+      sh.item[sa] = cj; sh.pos[cj] = sa;
+      sh.item[sb] = ci; sh.pos[ci] = sb;
+      sh.L[ca] += d;
+      sh.L[cb] -= d;
+      sh.moved[ci] = 1; sh.moved[cj] = 1;
+      ++sh.part[ca]; ++sh.part[cb];
       fb_swap sw;
-      sw.src_rank = c.a; sw.dst_rank = c.b; sw.src_slot = c.p; sw.dst_slot = c.q;
-      sw.expert_src = c.i < E ? (int32_t)c.i : -1;
-      sw.expert_dst = c.j < E ? (int32_t)c.j : -1;
-      sw.gain = c.gain;
-      a.swaps[s_ns] = sw;
-      s_ns = s_ns + 1;
+      sw.src_rank = ca; sw.dst_rank = cb; sw.src_slot = sa - ca * S; sw.dst_slot = sb - cb * S;
+      sw.expert_src = ci < E ? ci : -1;
+      sw.expert_dst = cj < E ? cj : -1;
+      sw.gain = (int64_t)g;
+      a.swaps[sh.ns] = sw;
+      sh.ns = sh.ns + 1;
     }
     __syncthreads();
   }
 
   __syncthreads();
-  for (int c = tid; c < RS; c += kPlanThreads) {
-    const int it = item[c];
+  for (int c = tid; c < RS; c += NT) {
+    const int it = sh.item[c];
     a.new_slot_expert[c] = it < E ? it : -1;
     if (it < E) a.new_expert_to_rank[it] = c / S;
   }
-  for (int r = tid; r < R; r += kPlanThreads) a.new_rank_loads[r] = L[r];
-  if (tid == 0) { *a.n_swaps = s_ns; *a.status = FB_OK; }
+  for (int r = tid; r < R; r += NT) a.new_rank_loads[r] = sh.L[r];
+  if (tid == 0) { *a.n_swaps = sh.ns; *a.status = FB_OK; }
+}
+
+// ---- one-wave frontier planner ------------------------------------------------------------------
+constexpr uint32_t kMovedBit = 0x80000000u;
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  v += dpp_u64<0xB1>(v);
+  v += dpp_u64<0x4E>(v);
+  v += dpp_u64<0x141>(v);
+  v += dpp_u64<0x140>(v);
+  return readlane_u64(v, 0) + readlane_u64(v, 16) + readlane_u64(v, 32) + readlane_u64(v, 48);
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));
+  return max(max((uint32_t)__builtin_amdgcn_readlane((int)v, 0), (uint32_t)__builtin_amdgcn_readlane((int)v, 16)),
+             max((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48)));
+}
+
+// Rounds of the one-wave planner when every rank sits in its own lane (R <= 64) and every load fits
+// 31 bits: loads, extremes and tie keys are 32-bit, rank ties are resolved by the lowest lane of a
+// ballot, and the tie key reduction runs only when two candidates share the best benefit.
+// Returns the number of swaps written.
+__device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* slot, int32_t* part,
+                                            uint32_t& Lu, int64_t g_num, int64_t g_den) {
+  const int lane = threadIdx.x;
+  const int E = a.E, R = a.R, S = a.S;
+  const fb_budget bg = a.budget;
+  const bool valid = lane < R;
+  const int pl = lane / S, ql = lane - pl * S;
+  const bool has_cand = lane < S * S;
+  const bool capped = bg.per_rank_cap != 0;
+  constexpr uint32_t kMoved = 0x80000000u;
+  int ns = 0;
+  for (int round = 0; round < bg.max_swaps; ++round) {
+    const uint32_t M32 = wave_max_u32(valid ? Lu : 0u);
+    const uint32_t Lmin32 = ~wave_max_u32(valid ? ~Lu : 0u);
+    const int amax = (int)__builtin_ctzll(__ballot(valid && Lu == M32));
+    const int amin = (int)__builtin_ctzll(__ballot(valid && Lu == Lmin32));
+    const int64_t M = M32, Lmin = Lmin32;
+    if (M - Lmin <= bg.tau) break;
+    const uint32_t ko = wave_max_u32(valid && lane != amax && lane != amin ? Lu + 1u : 0u);
+    const int64_t other = ko ? (int64_t)ko - 1 : INT64_MIN;
+
+    bool ok = false;
+    int64_t gain = 0;
+    uint32_t tk = 0;
+    uint2 ea = {0u, 0u}, eb = {0u, 0u};
+    if (has_cand) {
+      ea = slot[amax * S + pl];
+      eb = slot[amin * S + ql];
+      const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
+      const uint32_t i = ea.x & ~kMoved, j = eb.x & ~kMoved;
+      const int64_t d = (int64_t)(int32_t)eb.y - (int64_t)(int32_t)ea.y;
+      const int64_t la = M + d, lb = Lmin - d;
+      int64_t m2 = la > lb ? la : lb;
+      if (other > m2) m2 = other;
+      const int64_t spread = g_num ? g_num * (2 * d * (Lmin - M - d)) : 0;
+      gain = g_den * (M - m2) + spread;
+      ok = !cap_hit && !((ea.x | eb.x) & kMoved) && !(i >= (uint32_t)E && j >= (uint32_t)E) && gain > 0;
+      tk = (i << kItemBits) | j;
+    }
+    // largest benefit as two 32-bit reductions, then the smallest (i, j) among equal benefits
+    const uint32_t ghi = wave_max_u32(ok ? (uint32_t)((uint64_t)gain >> 32) : 0u);
+    const uint32_t glo = wave_max_u32(ok && (uint32_t)((uint64_t)gain >> 32) == ghi ? (uint32_t)gain : 0u);
+    const uint64_t g = ((uint64_t)ghi << 32) | glo;
+    if (g == 0) break;                          // no admissible candidate with positive benefit
+    const bool best = ok && (uint64_t)gain == g;
+    uint64_t win = __ballot(best);
+    if (__builtin_popcountll(win) > 1) {
+      const uint32_t tmin = ~wave_max_u32(best ? ~tk : 0u);
+      win = __ballot(best && tk == tmin);
+    }
+    const int wl = (int)__builtin_ctzll(win);
+    const int wp = __builtin_amdgcn_readlane(pl, wl), wq = __builtin_amdgcn_readlane(ql, wl);
+    const uint32_t wi = (uint32_t)__builtin_amdgcn_readlane((int)(ea.x & ~kMoved), wl);
+    const uint32_t wj = (uint32_t)__builtin_amdgcn_readlane((int)(eb.x & ~kMoved), wl);
+    const int32_t ci = __builtin_amdgcn_readlane((int)ea.y, wl), cj = __builtin_amdgcn_readlane((int)eb.y, wl);
+    const int32_t d = cj - ci;
+    if (lane == 0) {
+      slot[amax * S + wp] = make_uint2(wj | kMoved, (uint32_t)cj);
+      slot[amin * S + wq] = make_uint2(wi | kMoved, (uint32_t)ci);
+      ++part[amax];
+      ++part[amin];
+      fb_swap sw;
+      sw.src_rank = amax; sw.dst_rank = amin; sw.src_slot = wp; sw.dst_slot = wq;
+      sw.expert_src = wi < (uint32_t)E ? (int32_t)wi : -1;
+      sw.expert_dst = wj < (uint32_t)E ? (int32_t)wj : -1;
+      sw.gain = (int64_t)g;
+      a.swaps[ns] = sw;
+    }
+    Lu += (uint32_t)((lane == amax ? d : 0) - (lane == amin ? d : 0));
+    ++ns;
+    __syncthreads();
+  }
+  return ns;
+}
+
+// RPL: ranks per lane (R <= 64 * RPL); rank r lives in lane r % 64, register r / 64.
+template <int RPL>
+__global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) {
+  __shared__ int32_t cnt[kMaxRS];
+  __shared__ int32_t seen[kMaxRS];
+  __shared__ uint2 slot[kMaxRS];     // x: item id | moved flag, y: the item's count
+  __shared__ int32_t part[kMaxR];
+  const int lane = threadIdx.x;
+  const int E = a.E, R = a.R, S = a.S, RS = R * S;
+  const fb_budget bg = a.budget;
+
+  // both input tables are fetched before the first wait
+  for (int e = lane; e < E; e += 64) { cnt[e] = a.counts[e]; seen[e] = 0; }
+  for (int c = lane; c < RS; c += 64) slot[c].x = (uint32_t)a.slot_expert[c];
+  for (int r = lane; r < R; r += 64) part[r] = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int c = lane; c < RS; c += 64) {
+    const int e = (int)slot[c].x;
+    if (e == -1) slot[c].x = (uint32_t)(E + c);
+    else if (e < 0 || e >= E) bad = 1;
+    else atomicAdd(&seen[e], 1);
+  }
+  __syncthreads();
+  for (int e = lane; e < E; e += 64) bad |= (seen[e] != 1) | (cnt[e] < 0);
+  if (__ballot(bad)) {
+    if (lane == 0) { *a.n_swaps = 0; *a.status = FB_EINVAL; }
+    return;
+  }
+  for (int c = lane; c < RS; c += 64) {
+    const uint32_t it = slot[c].x;
+    slot[c].y = it < (uint32_t)E ? cnt[it] : 0;
+  }
+  __syncthreads();
+  int64_t Lr[RPL];                   // load of rank lane + 64 m (0 past R)
+  int64_t mine = 0;
+#pragma unroll
+  for (int m = 0; m < RPL; ++m) {
+    const int r = lane + 64 * m;
+    int64_t v = 0;
+    if (r < R)
+      for (int s = 0; s < S; ++s) v += slot[r * S + s].y;
+    Lr[m] = v;
+    mine += v;
+  }
+  const int64_t N = (int64_t)wave_sum_u64((uint64_t)mine);
+  int64_t g_num = bg.gamma_num, g_den = bg.gamma_den;
+  if (g_den == 0) { g_num = N > 0 ? 1 : 0; g_den = N > 0 ? N : 1; }
+  const __int128 bound = (__int128)g_den * N + (__int128)g_num * 4 * (__int128)N * N;
+  if (bound > (__int128)INT64_MAX) {
+    if (lane == 0) { *a.n_swaps = 0; *a.status = FB_EUNSUPPORTED; }
+    return;
+  }
+
+  const int pl = lane / S, ql = lane - pl * S;   // this lane's candidate slots
+  const bool has_cand = lane < S * S;
+  const bool capped = bg.per_rank_cap != 0;
+  int ns = 0;
+  const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
+  bool small_done = false;
+  if constexpr (RPL == 1) {
+    if (active && N < (int64_t)0x7fffffff) {
+      uint32_t Lu = (uint32_t)Lr[0];
+      ns = rounds_small(a, slot, part, Lu, g_num, g_den);
+      Lr[0] = Lu;
+      small_done = true;
+    }
+  }
+  for (int round = 0; active && !small_done && round < bg.max_swaps; ++round) {
+    uint64_t kmax = 0, kmin = 0;
+#pragma unroll
+    for (int m = 0; m < RPL; ++m) {
+      const int r = lane + 64 * m;
+      const bool in = r < R;
+      kmax = umax64(kmax, in ? key_max(Lr[m], r) : 0ull);
+      kmin = umax64(kmin, in ? key_min(Lr[m], r) : 0ull);
+    }
+    kmax = wave_max_u64(kmax);
+    kmin = wave_max_u64(kmin);
+    const int amax = key_rank(kmax), amin = key_rank(kmin);
+    const int64_t M = (int64_t)(kmax >> kRankBits);
+    const int64_t Lmin = kLoadCap - (int64_t)(kmin >> kRankBits);
+    if (M - Lmin <= bg.tau) break;
+    uint64_t ko = 0;                  // largest load among the other ranks, plus one (0: none)
+#pragma unroll
+    for (int m = 0; m < RPL; ++m) {
+      const int r = lane + 64 * m;
+      const bool in = r < R && r != amax && r != amin;
+      ko = umax64(ko, in ? (uint64_t)Lr[m] + 1 : 0ull);
+    }
+    ko = wave_max_u64(ko);
+    const int64_t other = ko ? (int64_t)ko - 1 : INT64_MIN;
+
+    uint64_t gk = 0, tk = 0;
+    int64_t dl = 0;
+    uint2 ea = {0u, 0u}, eb = {0u, 0u};
+    if (has_cand) {
+      ea = slot[amax * S + pl];
+      eb = slot[amin * S + ql];
+      const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
+      const uint32_t i = ea.x & ~kMovedBit, j = eb.x & ~kMovedBit;
+      const bool ok = !cap_hit && !((ea.x | eb.x) & kMovedBit) && !(i >= (uint32_t)E && j >= (uint32_t)E);
+      const int64_t d = (int64_t)(int32_t)eb.y - (int64_t)(int32_t)ea.y;
+      const int64_t la = M + d, lb = Lmin - d;
+      int64_t m2 = la > lb ? la : lb;
+      if (other > m2) m2 = other;
+      const int64_t spread = g_num ? g_num * (2 * d * (Lmin - M - d)) : 0;
+      const int64_t gain = g_den * (M - m2) + spread;
+      if (ok && gain > 0) {
+        gk = (uint64_t)gain;
+        // tie order inside the fixed pair (amax, amin): item ids; the slots ride along below them
+        tk = ((((uint64_t)i << kItemBits) | j) << 6) | ((uint64_t)pl << 3) | (uint64_t)ql;
+        dl = d;
+      }
+    }
+    const uint64_t g = wave_max_u64(gk);
+    if (g == 0) break;                          // no admissible candidate with positive benefit
+    const uint64_t t = ~wave_max_u64(gk == g ? ~tk : 0ull);
+    const int wp = (int)(t >> 3) & 7, wq = (int)t & 7;
+    const int wi = (int)(t >> (6 + kItemBits)) & ((1 << kItemBits) - 1);
+    const int wj = (int)(t >> 6) & ((1 << kItemBits) - 1);
+    const int wl = __builtin_amdgcn_readfirstlane(wp * S + wq);
+    const int64_t d = (int64_t)readlane_u64((uint64_t)dl, wl);
+    const int32_t ci = __builtin_amdgcn_readlane((int)ea.y, wl), cj = __builtin_amdgcn_readlane((int)eb.y, wl);
+    if (lane == 0) {
+      slot[amax * S + wp] = make_uint2((uint32_t)wj | kMovedBit, (uint32_t)cj);
+      slot[amin * S + wq] = make_uint2((uint32_t)wi | kMovedBit, (uint32_t)ci);
+      ++part[amax];
+      ++part[amin];
+      fb_swap sw;
+      sw.src_rank = amax; sw.dst_rank = amin; sw.src_slot = wp; sw.dst_slot = wq;
+      sw.expert_src = wi < E ? wi : -1;
+      sw.expert_dst = wj < E ? wj : -1;
+      sw.gain = (int64_t)g;
+      a.swaps[ns] = sw;
+    }
+#pragma unroll
+    for (int m = 0; m < RPL; ++m) {
+      const int r = lane + 64 * m;
+      Lr[m] += (r == amax ? d : 0) - (r == amin ? d : 0);
+    }
+    ++ns;
+    __syncthreads();
+  }
+
+  for (int c = lane; c < RS; c += 64) {
+    const int it = (int)(slot[c].x & ~kMovedBit);
+    a.new_slot_expert[c] = it < E ? it : -1;
+    if (it < E) a.new_expert_to_rank[it] = c / S;
+  }
+#pragma unroll
+  for (int m = 0; m < RPL; ++m) {
+    const int r = lane + 64 * m;
+    if (r < R) a.new_rank_loads[r] = Lr[m];
+  }
+  if (lane == 0) { *a.n_swaps = ns; *a.status = FB_OK; }
 }
 
 }  // namespace
 
 int launch_plan_device(const PlanDeviceLaunch& a) {
   (void)hipGetLastError();
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, static_cast<hipStream_t>(a.stream), a);
+  hipStream_t st = static_cast<hipStream_t>(a.stream);
+  if (a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 64) {
+    if (a.R <= 64) hipLaunchKernelGGL(plan_frontier_wave<1>, dim3(1), dim3(64), 0, st, a);
+    else if (a.R <= 128) hipLaunchKernelGGL(plan_frontier_wave<2>, dim3(1), dim3(64), 0, st, a);
+    else if (a.R <= 256) hipLaunchKernelGGL(plan_frontier_wave<4>, dim3(1), dim3(64), 0, st, a);
+    else hipLaunchKernelGGL(plan_frontier_wave<16>, dim3(1), dim3(64), 0, st, a);
+  }
+  else if (a.budget.mode == FB_FRONTIER)
+    hipLaunchKernelGGL(plan_general<256>, dim3(1), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(plan_general<1024>, dim3(1), dim3(1024), 0, st, a);
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
 }
 

@@ -68,6 +68,46 @@ def test_device_planner_on_predicted_counts(mode):
             assert host.rank_loads.max() < gpu["rank_loads"].max()
 
 
+@pytest.mark.parametrize("R,S,mode", [(100, 4, "frontier"), (1024, 4, "frontier"), (16, 12, "frontier"),
+                                      (64, 8, "frontier"), (3, 9, "full"), (40, 2, "full")])
+def test_device_planner_launch_shapes(R, S, mode):
+    """Every launch shape of the device planner: one wave with up to 16 ranks per lane, the
+    four-wave frontier kernel for S * S > 64, the full-mode kernel."""
+    print(f"[plan] R={R} S={S} {mode}", flush=True)
+    g = np.random.default_rng(R * 100 + S)
+    E = max(1, R * S - R // 3)
+    for it in range(3):
+        cells = g.permutation(R * S)[:E]
+        slots = np.full(R * S, -1, np.int32)
+        slots[cells] = np.arange(E)
+        slots = slots.reshape(R, S)
+        counts = (g.zipf(1.3, size=E) % 5000).astype(np.int32) * (g.random(E) < 0.9)
+        bg = fb.Budget(int(g.integers(4, 40)), per_rank_cap=[0, 2][it % 2], mode=mode, layer_id=it)
+        host = fb.plan_swaps(counts, slots, bg)
+        dev = _dev(counts, slots, bg)
+        _same(dev, host)
+        assert len(host.swaps) > 0
+
+
+@pytest.mark.parametrize("R", [4, 64, 100])
+def test_device_planner_loads_beyond_31_bits(R):
+    """Total load above 2^31 (max-only objective, gamma = 0, so the benefit still fits 64 bits):
+    the one-wave kernel leaves its 32-bit fast rounds for the 64-bit ones."""
+    print(f"[plan] loads beyond 31 bits, R={R}", flush=True)
+    g = np.random.default_rng(R)
+    S = 2
+    E = R * S
+    slots = g.permutation(E).astype(np.int32).reshape(R, S)
+    counts = g.integers(1 << 20, (1 << 31) - 1, size=E, dtype=np.int64).astype(np.int32)
+    assert int(counts.astype(np.int64).sum()) > (1 << 31)
+    for mode in ("frontier", "full"):
+        bg = fb.Budget(6, gamma=(0, 1), mode=mode)
+        host = fb.plan_swaps(counts, slots, bg)
+        _same(_dev(counts, slots, bg), host)
+        ref = OP.plan_swaps(counts, slots, 6, gamma=(0, 1), mode=mode)
+        _same(host, ref)
+
+
 def test_device_planner_reports_bad_placement():
     print("[plan] invalid slot table", flush=True)
     slots = np.array([[0, 1], [1, 3]], np.int32)   # expert 1 twice, expert 2 missing
