@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
-PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "predict_dsv3_counters.json")
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "predict_dsv3_counters.txt")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_14205_amd", "csrc", "fb_predict.hip")
 
 
@@ -44,15 +44,19 @@ def algorithmic_bytes(wl) -> int:
 
 
 def traffic_from_profile():
-    """HBM bytes per launch measured with rocprofv3 counters, if taken on the current kernel."""
+    """HBM bytes per launch from the committed rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE
+    scaled by a plain copy of known size), or None if it was taken on another kernel source."""
     try:
         with open(PROFILE_COUNTERS) as f:
-            rec = json.load(f)
-    except (OSError, ValueError):
+            rec = dict(l.split(":", 1) for l in f if ":" in l and not l.startswith("#"))
+    except OSError:
         return None
-    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+    if rec.get("kernel_source_sha256_16", "").strip() != kernel_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    try:
+        return int(rec["hbm_bytes_per_launch"].strip())
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(wl, li, e2r, slots, target_s: float):
