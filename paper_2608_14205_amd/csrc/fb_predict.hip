@@ -54,6 +54,20 @@ constexpr int kMaxK = FB_MAX_TOPK;
 constexpr int kMaxGroups = 32;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;    // raw buffer, 32-bit dwords
 constexpr uint32_t kOobOffset = 0x80000000u;    // fails the buffer range check: load returns 0
+#ifndef FB_PRODUCER_DEPTH
+#define FB_PRODUCER_DEPTH 2
+#endif
+#ifndef FB_STAGE_ROTATE
+#define FB_STAGE_ROTATE 0
+#endif
+#ifndef FB_B_PIPELINE
+#define FB_B_PIPELINE 1
+#endif
+#ifndef FB_W_INTERLEAVE
+#define FB_W_INTERLEAVE 1
+#endif
+constexpr int kDX = FB_PRODUCER_DEPTH;          // stages of hidden rows in flight per producer
+constexpr int kStageUnroll = kDX % 2 == 0 ? kDX : 2 * kDX;  // multiple of kDX and of 2
 
 // Consumer tile shapes: WE waves along experts x WT waves along tokens, BM tokens per workgroup;
 // every wave tile is a whole number of 32 x 32 MFMA blocks.
@@ -189,18 +203,21 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   constexpr int SROW = EPAD + 4;                 // score-tile row stride in floats
   constexpr int SCORE_BYTES = BM * SROW * 4;
   constexpr int SMEM = (2 * XSTAGE > SCORE_BYTES) ? 2 * XSTAGE : SCORE_BYTES;
-  constexpr int LPT = EPAD / 16;                 // lanes per token in the selection phase
+  constexpr int LPT = EPAD / 32;                 // lanes per token in the selection phase
   constexpr int TPP = kThreads / LPT;            // tokens per selection pass
   constexpr int NPASS = (BM + TPP - 1) / TPP;
   constexpr int GSC_TOK = TPP < BM ? TPP : BM;
   static_assert(LPW >= 1 && RPW % 8 == 0, "producers split the tile in 8-row groups");
   static_assert(WE * WT == kWaves - kProducers, "one consumer per SIMD");
   static_assert(EW % 32 == 0 && TW % 32 == 0, "wave tiles are whole 32 x 32 MFMA blocks");
+  static_assert(TPP % 64 == 0, "selection passes cover whole waves");
 
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   __shared__ int32_t hist[EPAD];
+  __shared__ __attribute__((aligned(16))) float s_lbias[EPAD];   // router bias (-inf past E)
+  __shared__ __attribute__((aligned(16))) float s_sbias[EPAD];   // selection bias (-inf past E)
   __shared__ int32_t sel[BM][kMaxK + 1];
-  __shared__ float gsc[GSC_TOK][kMaxGroups];
+  __shared__ __attribute__((aligned(16))) float gsc[GSC_TOK][kMaxGroups];
   __shared__ int32_t s_flag;
   __shared__ int64_t s_red[kWaves][2];
 
@@ -216,7 +233,12 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   const int64_t row0 = (int64_t)blockIdx.x * BM;
   const int E = p.E;
 
-  for (int i = tid; i < EPAD; i += kThreads) hist[i] = 0;
+  for (int i = tid; i < EPAD; i += kThreads) {
+    hist[i] = 0;
+    // padding experts get -inf in both, so their score is -inf without a per-element test
+    s_lbias[i] = i < E ? (p.logit_bias ? p.logit_bias[i] : 0.f) : -__builtin_inff();
+    s_sbias[i] = i < E ? (p.select_bias ? p.select_bias[i] : 0.f) : -__builtin_inff();
+  }
 
   f32x16 acc[FE][FT];
 #pragma unroll
@@ -226,10 +248,18 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  // Both roles run exactly NP stages with one barrier each (NP: nstages rounded up to the unroll
-  // factor 2).  Stages past the end load out of range, i.e. zeros.
+  // Both roles run exactly NP stages with one barrier each (NP: nstages rounded up to a multiple
+  // of both loops' unroll factors).  Stages past the end load out of range, i.e. zeros.
   const int nst = p.nstages;
-  const int NP = (nst + 1) & ~1;
+  const int NP = (nst + kStageUnroll - 1) / kStageUnroll * kStageUnroll;
+#if FB_STAGE_ROTATE
+  // Workgroups on one XCD (blockIdx = x mod 8) start the k-loop at different stages, so the
+  // router-weight stages they read at any moment are spread over the L2 channels.
+  const int rot = nst > 0 ? (int)(((blockIdx.x >> 3) * 5u) % (unsigned)nst) : 0;
+#else
+  const int rot = 0;
+#endif
+  auto phys = [&](int st) { const int v = st + rot; return v >= nst ? v - nst : v; };
   if (row0 < p.T) {
     if (!consumer) {
       // ---- producers: hidden rows, HBM -> registers -> LDS ----------------------------------
@@ -244,26 +274,27 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
         xoff[i] = (uint32_t)(r * p.ldx_bytes + col);
         loff[i] = (uint32_t)(r * kPitch + col);
       }
-      u32x4 xa[2][LPW];
+      u32x4 xa[kDX][LPW];
       // bytes at or past H (tail of a half-width last stage, padded stages) are not fetched
       auto load_x = [&](u32x4(&dst)[LPW], int st) {
         const bool stage_ok = st < nst;
-        const bool ok = stage_ok && st * kStageRowBytes + col < p.Hbytes;
+        const int ps = phys(st);
+        const bool ok = stage_ok && ps * kStageRowBytes + col < p.Hbytes;
 #pragma unroll
         for (int i = 0; i < LPW; ++i)
           dst[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, ok ? xoff[i] : kOobOffset,
-                                                         stage_ok ? st * kStageRowBytes : 0, 2);
+                                                         stage_ok ? ps * kStageRowBytes : 0, 2);
       };
-      load_x(xa[0], 0);
-      load_x(xa[1], 1);
-      for (int st0 = 0; st0 < NP; st0 += 2) {
 #pragma unroll
-        for (int d = 0; d < 2; ++d) {
+      for (int d = 0; d < kDX; ++d) load_x(xa[d], d);
+      for (int st0 = 0; st0 < NP; st0 += kDX) {
+#pragma unroll
+        for (int d = 0; d < kDX; ++d) {
           const int st = st0 + d;
           char* buf = smem + (st & 1) * XSTAGE;
 #pragma unroll
           for (int i = 0; i < LPW; ++i) *reinterpret_cast<u32x4*>(buf + loff[i]) = xa[d][i];
-          load_x(xa[d], st + 2);
+          load_x(xa[d], st + kDX);
           __builtin_amdgcn_sched_barrier(0);
           lds_barrier();                         // stage st is in LDS
         }
@@ -287,23 +318,54 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
           for (int q = 0; q < kNStep; ++q)
             dst[fe][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? woff[fe][q] : kOobOffset,
-                                                               ok ? st * SB : 0, 0);
+                                                               ok ? phys(st) * SB : 0, 0);
       };
       load_w(wa[0], 0);
       for (int st0 = 0; st0 < NP; st0 += 2) {
 #pragma unroll
         for (int d = 0; d < 2; ++d) {
           const int st = st0 + d;
+#if !FB_W_INTERLEAVE
           load_w(wa[d ^ 1], st + 1);
           __builtin_amdgcn_sched_barrier(0);
+#endif
           lds_barrier();                         // stage st is in LDS
           const char* buf = smem + (st & 1) * XSTAGE;
+#if FB_B_PIPELINE
+          // hidden fragments one k-step ahead, so only the first read of a stage waits on LDS
+          u32x4 bq[2][FT];
+#pragma unroll
+          for (int ft = 0; ft < FT; ++ft)
+            bq[0][ft] = *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + boff);
+#endif
 #pragma unroll
           for (int q = 0; q < kNStep; ++q) {
+#if FB_B_PIPELINE
+            if (q + 1 < kNStep) {
+#pragma unroll
+              for (int ft = 0; ft < FT; ++ft)
+                bq[(q + 1) & 1][ft] =
+                    *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + (q + 1) * kStepBytes + boff);
+            }
+#endif
+#if FB_W_INTERLEAVE
+            // the next stage's fragments for this k-step, spread between the MFMA groups
+            {
+              const bool ok = st + 1 < nst;
+#pragma unroll
+              for (int fe = 0; fe < FE; ++fe)
+                wa[d ^ 1][fe][q] = __builtin_amdgcn_raw_buffer_load_b128(
+                    wr, ok ? woff[fe][q] : kOobOffset, ok ? phys(st + 1) * SB : 0, 0);
+            }
+#endif
+#if FB_B_PIPELINE
+            const u32x4* bfr = bq[q & 1];
+#else
             u32x4 bfr[FT];
 #pragma unroll
             for (int ft = 0; ft < FT; ++ft)
               bfr[ft] = *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + q * kStepBytes + boff);
+#endif
 #pragma unroll
             for (int ft = 0; ft < FT; ++ft) {
 #pragma unroll
@@ -322,6 +384,9 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
                 }
               }
             }
+#if FB_W_INTERLEAVE || FB_B_PIPELINE
+            __builtin_amdgcn_sched_barrier(0);
+#endif
           }
         }
       }
@@ -334,30 +399,40 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   // register g * 4 + r.
   float* S = reinterpret_cast<float*>(smem);
   if (consumer && row0 < p.T) {
+    if (p.logits) {                              // debug output of the early logits
+#pragma unroll
+      for (int fe = 0; fe < FE; ++fe)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int e0 = we * EW + fe * 32 + g * 8 + (lane >> 5) * 4;
+#pragma unroll
+          for (int ft = 0; ft < FT; ++ft) {
+            const int64_t t = row0 + wt * TW + ft * 32 + (lane & 31);
+            if (t < p.T) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (e0 + r < E) p.logits[t * E + e0 + r] = acc[fe][ft][g * 4 + r] + s_lbias[e0 + r];
+            }
+          }
+        }
+    }
+    const bool sig = p.kind == FB_SIGMOID;
 #pragma unroll
     for (int fe = 0; fe < FE; ++fe) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int e0 = we * EW + fe * 32 + g * 8 + (lane >> 5) * 4;
-        float lb[4], sb[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int e = e0 + r;
-          lb[r] = (p.logit_bias && e < E) ? p.logit_bias[e] : 0.f;
-          sb[r] = (p.select_bias && e < E) ? p.select_bias[e] : 0.f;
-        }
+        const f32x4 lb = *reinterpret_cast<const f32x4*>(s_lbias + e0);
+        const f32x4 sb = *reinterpret_cast<const f32x4*>(s_sbias + e0);
 #pragma unroll
         for (int ft = 0; ft < FT; ++ft) {
           const int tl = wt * TW + ft * 32 + (lane & 31);
-          const int64_t t = row0 + tl;
           f32x4 sv;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int e = e0 + r;
             const float z = acc[fe][ft][g * 4 + r] + lb[r];
-            if (p.logits && t < p.T && e < E) p.logits[t * E + e] = z;
-            const float s = (p.kind == FB_SIGMOID) ? __builtin_amdgcn_rcpf(1.0f + __expf(-z)) + sb[r] : z;
-            sv[r] = (e < E) ? s + 0.0f : -__builtin_inff();
+            const float sc = sig ? __builtin_amdgcn_rcpf(1.0f + __expf(-z)) + sb[r] : z;
+            sv[r] = sc + 0.0f;                   // -0 -> +0; padding experts stay -inf
           }
           *reinterpret_cast<f32x4*>(S + tl * SROW + e0) = sv;
         }
@@ -366,82 +441,103 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   }
   lds_barrier();
 
-  // ---- selection: LPT lanes per token, 16 contiguous experts per lane ------------------------
+  // ---- selection: LPT lanes per token, 32 contiguous experts per lane ------------------------
+  // Lane jl reads its eight 4-expert chunks starting at chunk jl, which keeps the 16 lanes of a
+  // DPP row (two tokens) on distinct LDS banks; element 4q + j of the lane is expert
+  // 32 jl + 4 ((q + jl) mod 8) + j.  Tokens past T take part with no selectable expert.
   const int k = p.k;
   const int jl = tid % LPT;      // lane within the token group
   const int gslot = tid / LPT;   // token slot within a pass
+  const int ng = p.n_group;
+  const int gsz = E / ng;
+  const int gshift = __builtin_ctz((unsigned)gsz);   // group sizes below 32 are powers of two
+  auto local_of = [&](int i) { return ((((i >> 2) + jl) & 7) << 2) | (i & 3); };  // expert - 32 jl
+  uint32_t lane_live = 0;                    // bit i: element i is a real expert (< E)
+#pragma unroll
+  for (int i = 0; i < 32; ++i) lane_live |= (uint32_t)(jl * 32 + local_of(i) < E) << i;
 #pragma unroll 1
   for (int pass = 0; pass < NPASS; ++pass) {
     const int tl = pass * TPP + gslot;
-    if (tl >= BM) continue;                    // uniform per token group
+    if (tl >= BM) continue;                    // whole waves (TPP is a multiple of 64)
     const int64_t t = row0 + tl;
-    if (t >= p.T) continue;                    // uniform per token group
+    const bool tvalid = t < p.T;
 
-    float s[16];
+    float s[32];
+    const float* srow = S + tl * SROW + jl * 32;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(S + tl * SROW + jl * 16 + q * 4);
+    for (int q = 0; q < 8; ++q) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(srow + ((q + jl) & 7) * 4);
       s[q * 4 + 0] = v[0]; s[q * 4 + 1] = v[1]; s[q * 4 + 2] = v[2]; s[q * 4 + 3] = v[3];
     }
-    uint32_t keep = 0xFFFFu;                   // bit i: expert jl*16+i survives the group limit
-    if (p.n_group > 1) {
-      const int gsz = E / p.n_group;
+    uint32_t keep = 0xFFFFFFFFu;               // bit i: element i survives the group limit
+    if (ng > 1) {
       float* gs = gsc[gslot];
       // group scores: sum of the group's group_topn best scores, largest first
-      if (gsz >= 16) {
-        const int lpg = gsz >> 4;
+      if (gsz >= 32) {
+        const int lpg = gsz >> 5;
         float m1 = -__builtin_inff(), m2 = -__builtin_inff();
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
+        for (int i = 0; i < 32; ++i) {
           m2 = __builtin_amdgcn_fmed3f(m1, m2, s[i]);
           m1 = fmaxf(m1, s[i]);
         }
         top2_group(m1, m2, lpg);
-        if ((jl & (lpg - 1)) == 0 && jl * 16 < E) gs[(jl * 16) / gsz] = p.group_topn == 2 ? m1 + m2 : m1;
+        if ((jl & (lpg - 1)) == 0 && jl * 32 < E) gs[(jl * 32) >> gshift] = p.group_topn == 2 ? m1 + m2 : m1;
       } else {
-        const int gpl = 16 / gsz;
+        const int gpl = 32 >> gshift;
         for (int u = 0; u < gpl; ++u) {
           float m1 = -__builtin_inff(), m2 = -__builtin_inff();
-          for (int i = u * gsz; i < (u + 1) * gsz; ++i) {
-            m2 = __builtin_amdgcn_fmed3f(m1, m2, s[i]);
-            m1 = fmaxf(m1, s[i]);
+#pragma unroll
+          for (int i = 0; i < 32; ++i) {
+            const bool in = (local_of(i) >> gshift) == u;
+            m2 = in ? __builtin_amdgcn_fmed3f(m1, m2, s[i]) : m2;
+            m1 = in ? fmaxf(m1, s[i]) : m1;
           }
-          if (jl * 16 + u * gsz < E) gs[jl * gpl + u] = p.group_topn == 2 ? m1 + m2 : m1;
+          if (jl * 32 + u * gsz < E) gs[jl * gpl + u] = p.group_topn == 2 ? m1 + m2 : m1;
         }
       }
       wave_lds_sync();
-      // rank of each of this lane's groups among all groups (score desc, lower index first)
+      // rank of a group among all groups (score desc, lower index first), four scores per read
+      // (rows hold kMaxGroups entries, so the reads stay in bounds)
       auto kept = [&](int g) -> bool {
         const float mine = gs[g];
         int rank = 0;
-        for (int h = 0; h < p.n_group; ++h) {
-          const float o = gs[h];
-          rank += (o > mine) || (o == mine && h < g);
+#pragma unroll 1
+        for (int h4 = 0; h4 < ng; h4 += 4) {
+          const f32x4 o = *reinterpret_cast<const f32x4*>(gs + h4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int h = h4 + j;
+            rank += (h < ng) & ((o[j] > mine) | ((o[j] == mine) & (h < g)));
+          }
         }
         return rank < p.topk_group;
       };
-      keep = 0;
-      if (gsz >= 16) {
-        if (jl * 16 < E && kept((jl * 16) / gsz)) keep = 0xFFFFu;
+      if (gsz >= 32) {
+        keep = (jl * 32 < E && kept((jl * 32) >> gshift)) ? 0xFFFFFFFFu : 0u;
       } else {
-        const int gpl = 16 / gsz;
-        for (int u = 0; u < gpl; ++u)
-          if (jl * 16 + u * gsz < E && kept(jl * gpl + u)) keep |= ((1u << gsz) - 1u) << (u * gsz);
+        keep = 0;
+        const int gpl = 32 >> gshift;
+        for (int u = 0; u < gpl; ++u) {
+          if (jl * 32 + u * gsz < E && kept(jl * gpl + u)) {
+#pragma unroll
+            for (int i = 0; i < 32; ++i) keep |= (uint32_t)((local_of(i) >> gshift) == u) << i;
+          }
+        }
       }
     }
 
-    uint32_t key[16];
-    int nvalid = 0;
+    keep = tvalid ? keep & lane_live : 0u;
+    const int nvalid = __builtin_popcount(keep);
+    uint32_t key[32];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int e = jl * 16 + i;
-      const bool valid = (e < E) && ((keep >> i) & 1u);
-      key[i] = valid ? ((ord_bits(s[i]) & 0xFFFFFF00u) | (uint32_t)(255 - e)) : 0u;
-      nvalid += valid;
+    for (int i = 0; i < 32; ++i) {
+      const uint32_t e = (uint32_t)(jl * 32 + local_of(i));
+      key[i] = ((ord_bits(s[i]) & 0xFFFFFF00u) | (255u - e)) & (0u - ((keep >> i) & 1u));
     }
     uint32_t t1 = 0, t2 = 0, t3 = 0;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < 32; ++i) {
       const uint32_t v = key[i];
       const uint32_t n3 = umed3(t2, t3, v);
       const uint32_t n2 = umed3(t1, t2, v);
@@ -454,17 +550,20 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       const uint32_t m = group_max_u32<LPT>(h);
       if (r == k - 1) kth = m;
       if (r == k) next = m;
-      if (m != 0 && h == m) {
-        if (r < k) sel[tl][r] = 255 - (int)(m & 0xFFu);
-        t1 = t2; t2 = t3; t3 = 0; ++npop; last = m;
-        if (t1 == 0 && npop < nvalid) {        // this lane's cached top-3 ran dry: rescan below `last`
+      const bool mine = m != 0 && h == m;
+      if (mine && r < k) sel[tl][r] = 255 - (int)(m & 0xFFu);
+      t1 = mine ? t2 : t1;
+      t2 = mine ? t3 : t2;
+      t3 = mine ? 0u : t3;
+      npop += mine;
+      last = mine ? m : last;
+      if (mine && t1 == 0 && npop < nvalid) {  // this lane's cached top-3 ran dry: rescan below `last`
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const uint32_t v = key[i] < last ? key[i] : 0u;
-            const uint32_t n3 = umed3(t2, t3, v);
-            const uint32_t n2 = umed3(t1, t2, v);
-            t1 = max(t1, v); t2 = n2; t3 = n3;
-          }
+        for (int i = 0; i < 32; ++i) {
+          const uint32_t v = key[i] < last ? key[i] : 0u;
+          const uint32_t n3 = umed3(t2, t3, v);
+          const uint32_t n2 = umed3(t1, t2, v);
+          t1 = max(t1, v); t2 = n2; t3 = n3;
         }
       }
     }
@@ -475,9 +574,10 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       for (int r = 0; r < k; ++r) {
         uint64_t best = 0;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int e = jl * 16 + i;
-          const uint64_t kk = ((uint64_t)ord_bits(s[i]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)e);
+        for (int i = 0; i < 32; ++i) {
+          const int e = jl * 32 + local_of(i);
+          const float se = srow[local_of(i)];     // re-read: the scores are not kept in registers
+          const uint64_t kk = ((uint64_t)ord_bits(se + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)e);
           const bool ok = key[i] != 0 && kk < lastk && kk > best;
           best = ok ? kk : best;
         }
@@ -492,11 +592,13 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       }
     }
     wave_lds_sync();
-    for (int r = jl; r < k; r += LPT) {
-      const int e = sel[tl][r];
-      if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
+    if (tvalid) {
+      for (int r = jl; r < k; r += LPT) {
+        const int e = sel[tl][r];
+        if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
+      }
     }
-    if (p.topk_idx && jl == 0) {
+    if (p.topk_idx && jl == 0 && tvalid) {
       // debug output in exact descending score order: insertion sort of the k selected in place
       int* list = sel[tl];
       for (int r = 1; r < k; ++r) {

@@ -254,3 +254,44 @@ def test_mixtral_full_size():
     check_counts_consistent(gpu, wl, e2r)
     stats = check_prediction(gpu, li, wl, e2r, label="mixtral-full")
     _say(f"[mixtral] ok {stats}")
+
+
+@pytest.mark.parametrize("T,layers", [(4096, (0, 29, 57)), (16384, (0, 57)), (65536, (0,))])
+def test_sweep_config(T, layers):
+    """Multi-task skew sweep: DeepSeek-V3 shapes, 4-task mixture, per-layer routers.  Predicted and
+    actual passes (H_l = h_{l-1} + residual) on the GPU, oracle parity on sampled tokens, and the
+    plans for every budget of the sweep: device = host = oracle on the predicted counts."""
+    from oracle import planner as OPL
+    from workloads import sweep_workload
+    wl = sweep_workload(T)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    pred = fb.Predictor()
+    for layer in layers:
+        _say(f"[sweep] T={T} layer {layer}: generating inputs")
+        li = make_layer(wl, layer, with_target=True)
+        got = run_gpu(li, wl, e2r, predictor=pred, packed=True)
+        check_counts_consistent(got, wl, e2r)
+        rows = np.arange(T) if T <= 4096 else np.sort(
+            np.random.default_rng(layer).choice(T, size=2048, replace=False))
+        stats = check_prediction(got, li, wl, e2r, rows=rows, label=f"sweep T={T} l{layer}")
+        act_li = dataclasses.replace(li, x=li.h_target)
+        act = run_gpu(act_li, wl, e2r, predictor=pred, debug=False, packed=True)
+        assert act["counts"].sum() == T * wl.k
+        counts_d = torch.from_numpy(got["counts"].astype(np.int32)).cuda()
+        slots_d = torch.from_numpy(slots).cuda()
+        for B in wl.budgets:
+            bg = fb.Budget(B, layer_id=layer)
+            dev = fb.plan_swaps_device(counts_d, slots_d, bg).to_host()
+            host = fb.plan_swaps(got["counts"], slots, bg)
+            ref = OPL.plan_swaps(got["counts"], slots, B, layer_id=layer)
+            for p in (dev, ref):
+                assert [tuple(s) for s in p.swaps] == [tuple(s) for s in host.swaps]
+                assert np.array_equal(p.slots, host.slots)
+            assert len(host.swaps) <= B
+            assert host.rank_loads.max() <= got["rank_loads"].max()
+            # realised balance of the actual pass under the planned placement (diagnostic)
+            act_after = OP.max_to_mean(OP.rank_loads(act["counts"], host.expert_to_rank, wl.R))
+            _say(f"[sweep] T={T} l{layer} B={B}: predicted max/mean {got['max_mean']:.3f} -> "
+                 f"{host.rank_loads.max() * wl.R / host.rank_loads.sum():.3f}; actual {act['max_mean']:.3f} "
+                 f"-> {act_after:.3f}")
+        _say(f"[sweep] T={T} l{layer} ok {stats}")
