@@ -60,6 +60,10 @@ constexpr uint32_t kOobOffset = 0x80000000u;    // fails the buffer range check:
 #ifndef FB_STAGE_ROTATE
 #define FB_STAGE_ROTATE 0
 #endif
+#ifndef FB_SEL_CACHE
+#define FB_SEL_CACHE 5
+#endif
+constexpr int kCache = FB_SEL_CACHE;            // per-lane cached keys in the top-k extraction
 #ifndef FB_B_PIPELINE
 #define FB_B_PIPELINE 1
 #endif
@@ -452,9 +456,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   const int gsz = E / ng;
   const int gshift = __builtin_ctz((unsigned)gsz);   // group sizes below 32 are powers of two
   auto local_of = [&](int i) { return ((((i >> 2) + jl) & 7) << 2) | (i & 3); };  // expert - 32 jl
-  uint32_t lane_live = 0;                    // bit i: element i is a real expert (< E)
-#pragma unroll
-  for (int i = 0; i < 32; ++i) lane_live |= (uint32_t)(jl * 32 + local_of(i) < E) << i;
+  const int idx_base = 255 - jl * 32;        // key index bits of element i: idx_base - local_of(i)
 #pragma unroll 1
   for (int pass = 0; pass < NPASS; ++pass) {
     const int tl = pass * TPP + gslot;
@@ -527,47 +529,57 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       }
     }
 
-    keep = tvalid ? keep & lane_live : 0u;
-    const int nvalid = __builtin_popcount(keep);
+    // 32-bit keys: the top 24 bits of the order-preserving score encoding, then 255 - expert.
+    // Experts outside the kept groups (and every expert of a token past T) keep only their index
+    // bits, which ranks them below every selectable expert; padding experts score -inf.
     uint32_t key[32];
+    if (ng == 1 || gsz >= 32) {                // the lane's experts are kept or dropped together
+      const uint32_t m = tvalid && keep ? 0xFFFFFF00u : 0u;
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const uint32_t e = (uint32_t)(jl * 32 + local_of(i));
-      key[i] = ((ord_bits(s[i]) & 0xFFFFFF00u) | (255u - e)) & (0u - ((keep >> i) & 1u));
-    }
-    uint32_t t1 = 0, t2 = 0, t3 = 0;
+      for (int i = 0; i < 32; ++i) {
+        const uint32_t u = __float_as_uint(s[i]);
+        key[i] = ((u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u)) & m) | (uint32_t)(idx_base - local_of(i));
+      }
+    } else {
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const uint32_t v = key[i];
-      const uint32_t n3 = umed3(t2, t3, v);
-      const uint32_t n2 = umed3(t1, t2, v);
-      t1 = max(t1, v); t2 = n2; t3 = n3;
+      for (int i = 0; i < 32; ++i) {
+        const uint32_t u = __float_as_uint(s[i]);
+        const uint32_t m = tvalid && ((keep >> i) & 1u) ? 0xFFFFFF00u : 0u;
+        key[i] = ((u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u)) & m) | (uint32_t)(idx_base - local_of(i));
+      }
     }
+    // per-lane cache of the kCache largest keys (descending), refilled by a rescan below the last
+    // popped key when it runs dry
+    uint32_t c[kCache];
+#pragma unroll
+    for (int d = 0; d < kCache; ++d) c[d] = 0;
+    auto insert = [&](uint32_t v) {
+#pragma unroll
+      for (int d = kCache - 1; d >= 1; --d) c[d] = umed3(c[d - 1], c[d], v);
+      c[0] = max(c[0], v);
+    };
+#pragma unroll
+    for (int i = 0; i < 32; ++i) insert(key[i]);
     int npop = 0;
     uint32_t last = 0xFFFFFFFFu, kth = 0, next = 0;
     for (int r = 0; r <= k; ++r) {
-      const uint32_t h = t1;
+      const uint32_t h = c[0];
       const uint32_t m = group_max_u32<LPT>(h);
       if (r == k - 1) kth = m;
       if (r == k) next = m;
       const bool mine = m != 0 && h == m;
       if (mine && r < k) sel[tl][r] = 255 - (int)(m & 0xFFu);
-      t1 = mine ? t2 : t1;
-      t2 = mine ? t3 : t2;
-      t3 = mine ? 0u : t3;
+#pragma unroll
+      for (int d = 0; d < kCache - 1; ++d) c[d] = mine ? c[d + 1] : c[d];
+      c[kCache - 1] = mine ? 0u : c[kCache - 1];
       npop += mine;
       last = mine ? m : last;
-      if (mine && t1 == 0 && npop < nvalid) {  // this lane's cached top-3 ran dry: rescan below `last`
+      if (mine && c[0] == 0 && npop < 32) {    // this lane's cache ran dry: rescan below `last`
 #pragma unroll
-        for (int i = 0; i < 32; ++i) {
-          const uint32_t v = key[i] < last ? key[i] : 0u;
-          const uint32_t n3 = umed3(t2, t3, v);
-          const uint32_t n2 = umed3(t1, t2, v);
-          t1 = max(t1, v); t2 = n2; t3 = n3;
-        }
+        for (int i = 0; i < 32; ++i) insert(key[i] < last ? key[i] : 0u);
       }
     }
-    const bool tie = next != 0 && (next >> 8) == (kth >> 8);
+    const bool tie = tvalid && (next >> 8) != 0 && (next >> 8) == (kth >> 8);
     if (tie) {
       // exact path: 64-bit keys (full order-preserving score bits, then the inverted index)
       uint64_t lastk = ~0ull;
@@ -578,7 +590,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
           const int e = jl * 32 + local_of(i);
           const float se = srow[local_of(i)];     // re-read: the scores are not kept in registers
           const uint64_t kk = ((uint64_t)ord_bits(se + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)e);
-          const bool ok = key[i] != 0 && kk < lastk && kk > best;
+          const bool ok = (key[i] >> 8) != 0 && kk < lastk && kk > best;   // selectable only
           best = ok ? kk : best;
         }
 #pragma unroll
