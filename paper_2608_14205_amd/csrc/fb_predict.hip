@@ -67,6 +67,9 @@ constexpr int kCache = FB_SEL_CACHE;            // per-lane cached keys in the t
 #ifndef FB_B_PIPELINE
 #define FB_B_PIPELINE 1
 #endif
+#ifndef FB_W_RING
+#define FB_W_RING 1
+#endif
 #ifndef FB_W_INTERLEAVE
 #define FB_W_INTERLEAVE 1
 #endif
@@ -324,12 +327,27 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
             dst[fe][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? woff[fe][q] : kOobOffset,
                                                                ok ? phys(st) * SB : 0, 0);
       };
+#if FB_W_RING
+      // The two stage buffers form a ring of eight k-step slices; each k-step refills the slice the
+      // previous one consumed with the slice seven k-steps ahead.
       load_w(wa[0], 0);
+      {
+        const bool ok = 1 < nst;
+#pragma unroll
+        for (int fe = 0; fe < FE; ++fe)
+#pragma unroll
+          for (int q = 0; q < kNStep - 1; ++q)
+            wa[1][fe][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? woff[fe][q] : kOobOffset,
+                                                                 ok ? phys(1) * SB : 0, 0);
+      }
+#else
+      load_w(wa[0], 0);
+#endif
       for (int st0 = 0; st0 < NP; st0 += 2) {
 #pragma unroll
         for (int d = 0; d < 2; ++d) {
           const int st = st0 + d;
-#if !FB_W_INTERLEAVE
+#if !FB_W_INTERLEAVE && !FB_W_RING
           load_w(wa[d ^ 1], st + 1);
           __builtin_amdgcn_sched_barrier(0);
 #endif
@@ -352,7 +370,17 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
                     *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + (q + 1) * kStepBytes + boff);
             }
 #endif
-#if FB_W_INTERLEAVE
+#if FB_W_RING
+            {
+              const int tst = st + (q + 7) / kNStep;   // k-step 4 st + q + 7
+              const int tq = (q + 7) % kNStep;
+              const bool ok = tst < nst;
+#pragma unroll
+              for (int fe = 0; fe < FE; ++fe)
+                wa[q > 0 ? d : d ^ 1][fe][q > 0 ? q - 1 : kNStep - 1] = __builtin_amdgcn_raw_buffer_load_b128(
+                    wr, ok ? woff[fe][tq] : kOobOffset, ok ? phys(tst) * SB : 0, 0);
+            }
+#elif FB_W_INTERLEAVE
             // the next stage's fragments for this k-step, spread between the MFMA groups
             {
               const bool ok = st + 1 < nst;
@@ -388,7 +416,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
                 }
               }
             }
-#if FB_W_INTERLEAVE || FB_B_PIPELINE
+#if FB_W_INTERLEAVE || FB_B_PIPELINE || FB_W_RING
             __builtin_amdgcn_sched_barrier(0);
 #endif
           }
