@@ -201,6 +201,46 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
                            void* workspace, size_t workspace_bytes, int32_t* topk_idx,
                            float* logits, void* stream);
 
+/* ---- Prediction-quality diagnostics (Sec. "Metrics" and the prediction-quality study) ----------
+ * Device-side measurements of how well the early pass predicts the actual routing: run
+ * fb_predict_load on h_{l-1} and on the actual router input H_l with topk_idx / logits requested,
+ * then compare. All three calls are stream-ordered and deterministic. */
+
+/* Top-k hit count: hits = sum over tokens of |predicted set intersect actual set|; the hit rate is
+ * hits / (T * k).
+ *   topk_pred, topk_actual  device int32[T * k], rows of k distinct expert ids in [0, 256).
+ *   hits                    device int64 out (overwritten).
+ * FB_EINVAL for null pointers, T < 0 or k < 1; FB_EUNSUPPORTED for k > FB_MAX_TOPK. */
+int fb_topk_hits(const int32_t* topk_pred, const int32_t* topk_actual, int64_t T, int32_t k,
+                 int64_t* hits, void* stream);
+
+/* Bytes of device workspace fb_row_cosine_mean needs. */
+size_t fb_cosine_workspace_bytes(void);
+
+/* Mean over rows of the cosine similarity of matching rows of a and b (hidden-state cosine for
+ * h_{l-1} vs H_l, logit cosine for early vs actual logits). Products and sums in double; per-row
+ * cosine = dot / (|a| |b|); the mean sums the rows in a fixed order, so results are reproducible.
+ * A zero row gives NaN, as 0/0.
+ *   a, b        device, rows x cols row-major with row strides ld_a / ld_b elements, element type
+ *               dtype (FB_BF16 or FB_F32), 16-byte aligned rows; cols * element size and the row
+ *               strides in bytes must be multiples of 16 (FB_EUNSUPPORTED otherwise).
+ *   rows        >= 1.
+ *   out         device double out.
+ *   workspace   device, >= fb_cosine_workspace_bytes() bytes, 16-byte aligned; no contents kept. */
+int fb_row_cosine_mean(const void* a, const void* b, int64_t rows, int32_t cols, int64_t ld_a,
+                       int64_t ld_b, int32_t dtype, double* out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* Rank loads and max-to-mean ratio of a count vector under a placement (Alg. 1 aggregation, Sec.
+ * "Metrics"): the realised balance of the actual routing under the current or the planned
+ * placement.
+ *   counts          device int32[E] (>= 0).
+ *   expert_to_rank  device int32[E]; an entry outside [0, R) makes *max_mean = -1.0.
+ *   rank_loads      device int32[R] out; max_mean device double out (1.0 if every load is 0).
+ * FB_EINVAL for null pointers, E < 1 or R < 1; FB_EUNSUPPORTED for R > FB_MAX_RANKS. */
+int fb_fold_rank_loads(const int32_t* counts, int32_t E, const int32_t* expert_to_rank, int32_t R,
+                       int32_t* rank_loads, double* max_mean, void* stream);
+
 /* Budgeted greedy expert-swap planner on the host (Sec. Budgeted Expert-Swap Planning, Eq. 6-8,
  * Alg. 1).  Pure and deterministic: identical inputs give a byte-identical plan.
  *   counts            host int32[E] (>= 0): the predicted per-expert workload, not rank loads.

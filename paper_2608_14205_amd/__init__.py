@@ -8,11 +8,16 @@ from .api import (  # noqa: F401
     Budget,
     DevicePlan,
     PackedRouter,
+    Quality,
     Plan,
     Prediction,
     Predictor,
     Scoring,
+    fold_rank_loads,
     pack_router_weight,
+    prediction_quality,
+    row_cosine_mean,
+    topk_hits,
     plan_swaps,
     plan_swaps_device,
     predict_load,

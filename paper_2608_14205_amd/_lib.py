@@ -64,6 +64,10 @@ SIGNATURES = {
     "fb_plan_swaps_device": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32, ctypes.POINTER(fb_budget),
                                             _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "fb_swap_budget_from_cost": (_I64, [_D, _D, _D, _D, _I64]),
+    "fb_topk_hits": (ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
+    "fb_cosine_workspace_bytes": (_SZ, []),
+    "fb_row_cosine_mean": (ctypes.c_int, [_VP, _VP, _I64, _I32, _I64, _I64, _I32, _VP, _VP, _SZ, _VP]),
+    "fb_fold_rank_loads": (ctypes.c_int, [_VP, _I32, _VP, _I32, _VP, _VP, _VP]),
 }
 
 _lock = threading.Lock()

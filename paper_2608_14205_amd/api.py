@@ -306,3 +306,89 @@ def swap_budget_from_cost(t_attn_us: float, delta_us: float, alpha_us: float,
                                              int(expert_bytes)))
     L.check(n if n < 0 else L.FB_OK, "fb_swap_budget_from_cost")
     return n
+
+
+@dataclasses.dataclass
+class Quality:
+    """Prediction quality of one layer (device-computed)."""
+
+    hits: int
+    hit_rate: float
+    logit_cosine: Optional[float]
+    hidden_cosine: Optional[float]
+
+
+_cosine_workspaces = {}
+
+
+def _cosine_workspace(device: torch.device) -> torch.Tensor:
+    key = device.index if device.index is not None else torch.cuda.current_device()
+    ws = _cosine_workspaces.get(key)
+    if ws is None:
+        n = int(L.lib().fb_cosine_workspace_bytes())
+        ws = _cosine_workspaces[key] = torch.empty(n, dtype=torch.uint8, device=device)
+    return ws
+
+
+def row_cosine_mean(a: torch.Tensor, b: torch.Tensor,
+                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """fb_row_cosine_mean: mean over rows of cos(a[r], b[r]) as a device float64 scalar."""
+    if a.dim() != 2 or a.shape != b.shape or a.dtype != b.dtype or a.device != b.device:
+        raise ValueError("a and b must be matching 2-D tensors on one device")
+    if a.stride(1) != 1 or b.stride(1) != 1:
+        raise ValueError("rows must be contiguous")
+    out = torch.empty(1, dtype=torch.float64, device=a.device)
+    ws = _cosine_workspace(a.device)
+    with torch.cuda.device(a.device):
+        L.check(L.lib().fb_row_cosine_mean(_ptr(a), _ptr(b), a.shape[0], a.shape[1], a.stride(0),
+                                           b.stride(0), _dtype_code(a), _ptr(out), _ptr(ws), ws.numel(),
+                                           _stream_handle(a.device, stream)), "fb_row_cosine_mean")
+    return out
+
+
+def topk_hits(topk_pred: torch.Tensor, topk_actual: torch.Tensor,
+              stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """fb_topk_hits: sum over tokens of the predicted and actual sets' intersection size (device int64)."""
+    if topk_pred.shape != topk_actual.shape or topk_pred.dim() != 2:
+        raise ValueError("top-k tables must both be T x k")
+    for t in (topk_pred, topk_actual):
+        if t.dtype != torch.int32 or not t.is_contiguous():
+            raise ValueError("top-k tables must be contiguous int32")
+    out = torch.empty(1, dtype=torch.int64, device=topk_pred.device)
+    with torch.cuda.device(topk_pred.device):
+        L.check(L.lib().fb_topk_hits(_ptr(topk_pred), _ptr(topk_actual), topk_pred.shape[0],
+                                     topk_pred.shape[1], _ptr(out),
+                                     _stream_handle(topk_pred.device, stream)), "fb_topk_hits")
+    return out
+
+
+def fold_rank_loads(counts: torch.Tensor, expert_to_rank: torch.Tensor, R: int,
+                    stream: Optional[torch.cuda.Stream] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """fb_fold_rank_loads: (rank_loads int32[R], max_mean float64[1]) on the device."""
+    if counts.dtype != torch.int32 or expert_to_rank.dtype != torch.int32:
+        raise ValueError("counts and expert_to_rank must be int32")
+    if counts.numel() != expert_to_rank.numel():
+        raise ValueError("counts and expert_to_rank must have E entries each")
+    dev = counts.device
+    loads = torch.empty(R, dtype=torch.int32, device=dev)
+    mm = torch.empty(1, dtype=torch.float64, device=dev)
+    with torch.cuda.device(dev):
+        L.check(L.lib().fb_fold_rank_loads(_ptr(counts), counts.numel(), _ptr(expert_to_rank), R,
+                                           _ptr(loads), _ptr(mm), _stream_handle(dev, stream)),
+                "fb_fold_rank_loads")
+    return loads, mm
+
+
+def prediction_quality(pred: Prediction, actual: Prediction, hidden_prev: Optional[torch.Tensor] = None,
+                       hidden_target: Optional[torch.Tensor] = None) -> Quality:
+    """Hit rate and cosines of an early pass against the actual routing; both Predictions must
+    carry topk (and logits for the logit cosine)."""
+    if pred.topk is None or actual.topk is None:
+        raise ValueError("both passes need return_topk=True")
+    hits = topk_hits(pred.topk, actual.topk)
+    lc = row_cosine_mean(pred.logits, actual.logits) if pred.logits is not None and actual.logits is not None else None
+    hc = row_cosine_mean(hidden_prev, hidden_target) if hidden_prev is not None and hidden_target is not None else None
+    T, k = pred.topk.shape
+    h = int(hits.item())
+    return Quality(h, h / float(T * k) if T else 1.0, None if lc is None else float(lc.item()),
+                   None if hc is None else float(hc.item()))

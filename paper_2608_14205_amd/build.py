@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libfreebalance.so")
 
-HIP_SOURCES = ["fb_predict.hip", "fb_plan_device.hip", "fb_abi.cpp"]
+HIP_SOURCES = ["fb_predict.hip", "fb_plan_device.hip", "fb_quality.hip", "fb_abi.cpp"]
 HOST_SOURCES = ["fb_plan_host.cpp"]
 ARCH = "gfx950"
 

@@ -252,4 +252,42 @@ int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_e
   return fb::launch_plan_device(a);
 }
 
+size_t fb_cosine_workspace_bytes(void) { return fb::cosine_workspace_bytes(); }
+
+int fb_topk_hits(const int32_t* topk_pred, const int32_t* topk_actual, int64_t T, int32_t k,
+                 int64_t* hits, void* stream) {
+  if (!hits || T < 0 || k < 1) return FB_EINVAL;
+  if (T > 0 && (!topk_pred || !topk_actual)) return FB_EINVAL;
+  if (k > FB_MAX_TOPK) return FB_EUNSUPPORTED;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  return fb::launch_hits(topk_pred, topk_actual, T, k, hits, stream);
+}
+
+int fb_row_cosine_mean(const void* a, const void* b, int64_t rows, int32_t cols, int64_t ld_a,
+                       int64_t ld_b, int32_t dtype, double* out, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  if (!a || !b || !out || !workspace || rows < 1 || cols < 1 || ld_a < cols || ld_b < cols)
+    return FB_EINVAL;
+  if (dtype != FB_BF16 && dtype != FB_F32) return FB_EINVAL;
+  const int elem = dtype == FB_BF16 ? 2 : 4;
+  if ((int64_t)cols * elem % 16 != 0 || ld_a * elem % 16 != 0 || ld_b * elem % 16 != 0 ||
+      !aligned16(a) || !aligned16(b))
+    return FB_EUNSUPPORTED;
+  if (!aligned16(workspace)) return FB_EINVAL;
+  if (workspace_bytes < fb::cosine_workspace_bytes()) return FB_ENOSPC;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  return fb::launch_cosine(a, b, rows, cols, ld_a, ld_b, dtype, out, workspace, stream);
+}
+
+int fb_fold_rank_loads(const int32_t* counts, int32_t E, const int32_t* expert_to_rank, int32_t R,
+                       int32_t* rank_loads, double* max_mean, void* stream) {
+  if (!counts || !expert_to_rank || !rank_loads || !max_mean || E < 1 || R < 1) return FB_EINVAL;
+  if (R > FB_MAX_RANKS) return FB_EUNSUPPORTED;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  return fb::launch_fold(counts, E, expert_to_rank, R, rank_loads, max_mean, stream);
+}
+
 }  // extern "C"

@@ -31,7 +31,9 @@ def test_header_declares_the_boundary():
     assert names == sorted(["fb_abi_version", "fb_status_string", "fb_router_packed_bytes",
                             "fb_predict_workspace_bytes", "fb_predict_workspace_init",
                             "fb_pack_router_weight", "fb_predict_load", "fb_predict_load_packed",
-                            "fb_plan_swaps", "fb_plan_swaps_device", "fb_swap_budget_from_cost"])
+                            "fb_plan_swaps", "fb_plan_swaps_device", "fb_swap_budget_from_cost",
+                            "fb_topk_hits", "fb_cosine_workspace_bytes", "fb_row_cosine_mean",
+                            "fb_fold_rank_loads"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -288,6 +290,34 @@ def test_predict_packed_validation_without_gpu(over, code):
 
 def test_unpacked_predict_needs_room_for_the_packed_weight():
     assert _predict_call(wsb=2048 + 4096 - 1) == L.FB_ENOSPC
+
+
+def test_diagnostics_validation_without_gpu():
+    lib = fb.lib()
+    h = 0x5000
+    assert lib.fb_topk_hits(0x1000, 0x2000, -1, 8, h, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 0, h, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(None, 0x2000, 4, 8, h, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 8, None, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 33, h, None) == L.FB_EUNSUPPORTED
+    ws = lib.fb_cosine_workspace_bytes()
+    assert ws >= 8
+    def cos(**o):
+        a = dict(a=0x1000, b=0x2000, rows=4, cols=64, lda=64, ldb=64, dtype=L.FB_BF16, out=0x3000,
+                 ws=0x4000, wsb=ws)
+        a.update(o)
+        return lib.fb_row_cosine_mean(a["a"], a["b"], a["rows"], a["cols"], a["lda"], a["ldb"], a["dtype"],
+                                      a["out"], a["ws"], a["wsb"], None)
+    assert cos(rows=0) == L.FB_EINVAL
+    assert cos(a=None) == L.FB_EINVAL
+    assert cos(lda=32) == L.FB_EINVAL
+    assert cos(dtype=9) == L.FB_EINVAL
+    assert cos(cols=12) == L.FB_EUNSUPPORTED          # 24 bytes per bf16 row
+    assert cos(a=0x1008) == L.FB_EUNSUPPORTED
+    assert cos(wsb=ws - 1) == L.FB_ENOSPC
+    assert lib.fb_fold_rank_loads(0x1000, 0, 0x2000, 4, 0x3000, 0x4000, None) == L.FB_EINVAL
+    assert lib.fb_fold_rank_loads(0x1000, 8, 0x2000, 2000, 0x3000, 0x4000, None) == L.FB_EUNSUPPORTED
+    assert lib.fb_fold_rank_loads(None, 8, 0x2000, 4, 0x3000, 0x4000, None) == L.FB_EINVAL
 
 
 def test_device_planner_validation_without_gpu():

@@ -221,3 +221,16 @@ def test_topk_requires_enough_allowed():
     s = np.zeros((1, 4), np.float32)
     with pytest.raises(ValueError):
         P.topk_experts(s, 3, np.array([[True, True, False, False]]))
+
+
+def test_quality_metrics_hand_worked():
+    """Hand-worked values of the prediction-quality metrics (Sec. "Metrics"): the hit rate counts set
+    intersections, the cosine is the mean of the per-row cosines."""
+    tp = np.array([[0, 1], [2, 3], [1, 0]])
+    ta = np.array([[1, 0], [2, 4], [3, 2]])
+    # row 0: {0,1} & {0,1} = 2; row 1: {2,3} & {2,4} = 1; row 2: {0,1} & {2,3} = 0 -> 3 / 6
+    assert P.hit_rate(tp, ta) == 0.5
+    a = np.array([[1.0, 0.0], [1.0, 1.0], [3.0, 4.0]])
+    b = np.array([[2.0, 0.0], [1.0, 0.0], [-3.0, -4.0]])
+    # cosines 1, 1/sqrt(2), -1
+    assert P.mean_cosine(a, b) == pytest.approx((1.0 + 2 ** -0.5 - 1.0) / 3.0, rel=1e-15)
