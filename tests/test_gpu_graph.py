@@ -1,0 +1,119 @@
+"""The per-layer device sequence (predict -> plan) captured in a HIP graph and replayed, and the
+predictor running on a side stream next to other work, on MI355X.  Every replay is checked against
+the eager result, with eager work and synchronisations between replays."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_14205_amd as fb
+from workloads import CONFIGS, contiguous_placement, make_layer
+from gpu_util import scoring_of, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _setup(T=8192, layer=0):
+    wl = CONFIGS["dsv3"].with_T(T)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    li = make_layer(wl, layer)
+    x = to_device(li.x, wl.dtype)
+    w = to_device(li.w, wl.dtype)
+    sb = torch.from_numpy(li.select_bias).cuda()
+    return wl, slots, e2r, x, w, sb
+
+
+def _plan_tuple(plan):
+    h = plan.to_host()
+    return [tuple(s) for s in h.swaps], h.slots.copy(), h.rank_loads.copy()
+
+
+def test_graph_replay_matches_eager():
+    _say("[graph] capture predict -> plan")
+    wl, slots, e2r, x, w, sb = _setup()
+    e2r_t = torch.from_numpy(e2r).cuda()
+    slots_t = torch.from_numpy(slots).cuda()
+    wp = fb.pack_router_weight(w)
+    sc, bg = scoring_of(wl), fb.Budget(wl.budget)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        pred = fb.Predictor(stream=side)
+        out = pred.predict_load(x, wp, sc, e2r_t, wl.R, select_bias=sb)
+        plan = fb.plan_swaps_device(out.counts, slots_t, bg)
+    side.synchronize()
+    eager = (out.counts.clone(), out.rank_loads.clone(), out.max_mean.clone(), _plan_tuple(plan))
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        pred.predict_load(x, wp, sc, e2r_t, wl.R, select_bias=sb, out=out)
+        fb.plan_swaps_device(out.counts, slots_t, bg, out=plan)
+    torch.cuda.synchronize()
+
+    x2 = to_device(make_layer(wl, 1).x, wl.dtype)   # eager work on other data between replays
+    for rep in range(4):
+        out.counts.fill_(-7)
+        plan.n_swaps.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.counts, eager[0]), f"replay {rep}: counts"
+        assert torch.equal(out.rank_loads, eager[1])
+        assert torch.equal(out.max_mean, eager[2])
+        pt = _plan_tuple(plan)
+        assert pt[0] == eager[3][0] and np.array_equal(pt[1], eager[3][1]) and np.array_equal(pt[2], eager[3][2])
+        other = fb.predict_load(x2, w, sc, e2r_t, wl.R, select_bias=sb)
+        torch.cuda.synchronize()
+        assert int(other.counts.sum().item()) == x2.shape[0] * wl.k
+    # the captured workspace is still clean for eager use
+    assert not pred.workspace[:2048].any().item()
+
+
+def test_side_stream_next_to_other_work():
+    """The predictor on its own stream while a dense bf16 GEMM runs on another (the early pass shares
+    the GPU with other layer work): both results stay correct.  The timings are printed."""
+    _say("[overlap] predictor next to a GEMM")
+    wl, slots, e2r, x, w, sb = _setup(T=16384)
+    e2r_t = torch.from_numpy(e2r).cuda()
+    wp = fb.pack_router_weight(w)
+    sc = scoring_of(wl)
+    a = torch.randn(8192, 7168, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(7168, 4096, device="cuda", dtype=torch.bfloat16)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    pred = fb.Predictor(stream=s2)
+    ref = pred.predict_load(x, wp, sc, e2r_t, wl.R, select_bias=sb, stream=s2)
+    s2.synchronize()
+    ref_counts = ref.counts.clone()
+    c_ref = torch.matmul(a, b)
+    c = torch.empty_like(c_ref)
+    torch.cuda.synchronize()
+
+    def timed(use_gemm, use_pred, reps=10):
+        st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e1, e2 = torch.cuda.Event(), torch.cuda.Event()
+        torch.cuda.synchronize()
+        st.record()
+        s1.wait_event(st)
+        s2.wait_event(st)
+        for _ in range(reps):
+            if use_gemm:
+                with torch.cuda.stream(s1):
+                    torch.matmul(a, b, out=c)
+            if use_pred:
+                pred.predict_load(x, wp, sc, e2r_t, wl.R, select_bias=sb, out=ref, stream=s2)
+        e1.record(s1)
+        e2.record(s2)
+        torch.cuda.current_stream().wait_event(e1)
+        torch.cuda.current_stream().wait_event(e2)
+        en.record()
+        torch.cuda.synchronize()
+        return st.elapsed_time(en) / reps
+
+    for _ in range(2):
+        timed(True, True, 2)
+    t_gemm, t_pred, t_both = timed(True, False), timed(False, True), timed(True, True)
+    _say(f"[overlap] gemm {t_gemm:.3f} ms, predictor {t_pred:.3f} ms, both {t_both:.3f} ms "
+         f"(sum {t_gemm + t_pred:.3f} ms)")
+    assert torch.equal(ref.counts, ref_counts)
+    assert torch.allclose(c.float(), c_ref.float(), rtol=1e-3, atol=1e-2)
