@@ -11,15 +11,19 @@
 
 namespace fb {
 
+namespace {
+std::atomic<int> g_arch_cache[64];  // 0 unknown, 1 gfx950, 2 other
+std::atomic<int> g_cu_cache[64];    // compute units, 0 unknown
+}  // namespace
+
 int check_device() {
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
     (void)hipGetLastError();
     return FB_EDEVICE;
   }
-  static std::atomic<int> cache[64];  // 0 unknown, 1 gfx950, 2 other
   if (dev < 64) {
-    const int c = cache[dev].load(std::memory_order_relaxed);
+    const int c = g_arch_cache[dev].load(std::memory_order_relaxed);
     if (c == 1) return FB_OK;
     if (c == 2) return FB_EUNSUPPORTED;
   }
@@ -29,8 +33,21 @@ int check_device() {
     return FB_EDEVICE;
   }
   const bool ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
-  if (dev < 64) cache[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+  if (dev < 64) {
+    g_cu_cache[dev].store(prop.multiProcessorCount, std::memory_order_relaxed);
+    g_arch_cache[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+  }
   return ok ? FB_OK : FB_EUNSUPPORTED;
+}
+
+int device_cu_count() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  const int n = g_cu_cache[dev].load(std::memory_order_relaxed);
+  return n > 0 ? n : 256;
 }
 
 }  // namespace fb
@@ -166,6 +183,7 @@ fb::PredictLaunch make_launch(const void* hidden, int64_t T, int32_t H, int64_t 
   a.topk_idx = topk_idx;
   a.logits = logits;
   a.stream = stream;
+  a.num_cus = fb::device_cu_count();
   return a;
 }
 

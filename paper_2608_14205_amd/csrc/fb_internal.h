@@ -29,6 +29,7 @@ struct PredictLaunch {
   int32_t* topk_idx;
   float* logits;
   void* stream;
+  int32_t num_cus;    // compute units of the device (tile-height choice)
 };
 
 // Workspace layout (device): per-expert accumulator and the completion ticket.  Every completed
@@ -73,5 +74,7 @@ int launch_fold(const int32_t* counts, int32_t E, const int32_t* e2r, int32_t R,
 
 // Current device must be gfx950; cached per device.  FB_OK, FB_EUNSUPPORTED or FB_EDEVICE.
 int check_device();
+// Compute units of the current device (cached by check_device; 256 if unknown).
+int device_cu_count();
 
 }  // namespace fb

@@ -197,10 +197,11 @@ __global__ void pack_kernel(const char* __restrict__ w, int32_t E, int32_t Hbyte
   }
 }
 
-template <bool BF16, int EPAD>
+// BM_: tokens per workgroup (the configuration's own, or half of it when that fills the chip better)
+template <bool BF16, int EPAD, int BM_>
 __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   using Cfg = TileCfg<EPAD>;
-  constexpr int WE = Cfg::WE, WT = Cfg::WT, BM = Cfg::BM;
+  constexpr int WE = Cfg::WE, WT = Cfg::WT, BM = BM_;
   constexpr int EW = EPAD / WE, TW = BM / WT;
   constexpr int FE = EW / 32, FT = TW / 32;
   constexpr int RPW = BM / kProducers;           // hidden rows per producer wave
@@ -735,9 +736,8 @@ int launch_pack_cfg(const void* w, int32_t E, int32_t Hbytes, void* out, void* s
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
 }
 
-template <bool BF16, int EPAD>
-int launch_cfg(const PredictLaunch& a) {
-  using Cfg = TileCfg<EPAD>;
+template <bool BF16, int EPAD, int BM>
+int launch_cfg_bm(const PredictLaunch& a) {
   const int elem = BF16 ? 2 : 4;
   Params p;
   p.x = static_cast<const char*>(a.hidden);
@@ -762,12 +762,24 @@ int launch_cfg(const PredictLaunch& a) {
   p.ws_ticket = reinterpret_cast<uint32_t*>(static_cast<char*>(a.workspace) + kWsTicketOffset);
   p.topk_idx = a.topk_idx;
   p.logits = a.logits;
-  const int64_t tiles = (a.T + Cfg::BM - 1) / Cfg::BM;
+  const int64_t tiles = (a.T + BM - 1) / BM;
   p.nblocks = (uint32_t)(tiles > 0 ? tiles : 1);
   p.nstages = (p.Hbytes + kStageRowBytes - 1) / kStageRowBytes;
-  hipLaunchKernelGGL((predict_kernel<BF16, EPAD>), dim3(p.nblocks), dim3(kThreads), 0,
+  hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM>), dim3(p.nblocks), dim3(kThreads), 0,
                      static_cast<hipStream_t>(a.stream), p);
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
+}
+
+template <bool BF16, int EPAD>
+int launch_cfg(const PredictLaunch& a) {
+  constexpr int BM = TileCfg<EPAD>::BM;
+  // Half-height tiles when the full-height grid would leave CUs idle and the half-height one still
+  // fits in a single wave of workgroups: every CU then streams the weight for fewer tokens.
+  if constexpr (EPAD == 256) {
+    const int64_t half_tiles = (a.T + BM / 2 - 1) / (BM / 2);
+    if (a.T > 0 && half_tiles <= a.num_cus) return launch_cfg_bm<BF16, EPAD, BM / 2>(a);
+  }
+  return launch_cfg_bm<BF16, EPAD, BM>(a);
 }
 
 template <bool BF16>
