@@ -120,7 +120,7 @@ const char* fb_status_string(int status);
 
 /* Bytes of the packed router weight fb_pack_router_weight writes for E experts of H elements of
  * `dtype`: E rounded up to 32, 64, 128 or 256 rows times H * element size rounded up to a
- * multiple of 128 bytes.  0 if E, H or dtype is invalid or E > FB_MAX_EXPERTS. */
+ * multiple of 256 bytes.  0 if E, H or dtype is invalid or E > FB_MAX_EXPERTS. */
 size_t fb_router_packed_bytes(int32_t E, int32_t H, int32_t dtype);
 
 /* Bytes of device workspace fb_predict_load needs: 2048 bytes of accumulators plus room for the
@@ -137,9 +137,9 @@ int fb_predict_workspace_init(void* workspace, size_t workspace_bytes, void* str
 /* Rewrite a router weight into the layout the predictor kernel streams (one kernel on `stream`).
  * The router weight is a fixed parameter of the routed model, so a caller packs it once when the
  * model is loaded and calls fb_predict_load_packed per batch; fb_predict_load does the same packing
- * into its workspace on every call.  Layout: for each 128-byte stage st of a row, a contiguous
- * block of 1 KB chunks; chunk c = (w * 4 + q) * F + f holds, for lane l of 64, the 16 bytes at
- * byte st * 128 + q * 32 + (l / 32) * 16 of row w * (EP / W) + f * 32 + (l % 32), where EP is E
+ * into its workspace on every call.  Layout: for each 256-byte stage st of a row, a contiguous
+ * block of 1 KB chunks; chunk c = (w * 8 + q) * F + f holds, for lane l of 64, the 16 bytes at
+ * byte st * 256 + q * 32 + (l / 32) * 16 of row w * (EP / W) + f * 32 + (l % 32), where EP is E
  * rounded as above, W the number of expert slices of the kernel's tile for EP (4 for EP >= 128, 2
  * for 64, 1 for 32) and F = EP / (32 * W).  Rows >= E and bytes past H read as zero.
  *   router_w      device, E x H row-major, element type `dtype`, 16-byte aligned.

@@ -6,24 +6,25 @@
 // last workgroup to finish folds the histogram into per-rank loads under the expert-to-rank
 // placement (Alg. 1, second step) and computes the max-to-mean ratio (Sec. "Metrics").
 //
-// Workgroup: 8 waves (512 threads), one workgroup per CU.
+// Workgroup: 8 waves (512 threads), one workgroup per CU.  The contraction runs in k-stages of
+// 256 bytes of every row (128 bf16 / 64 f32 elements).
 //   * Waves 0-3 are producers.  They stream the tile's hidden rows from HBM with full 128-byte
-//     line requests (8 rows x 128 B per instruction), two k-stages ahead, and store them row-major
-//     into a double-buffered LDS stage (row pitch 144 B, so both the stores and the fragment
-//     reads below stay close to conflict-free).
+//     line requests (4 rows x 256 B per instruction), two stages ahead, and store them row-major
+//     into a double-buffered LDS stage (row pitch 272 B, so both the stores and the fragment reads
+//     below stay conflict-free).
 //   * Waves 4-7 are consumers, one per SIMD next to a producer.  Each owns a slice of the
 //     experts.  It loads its router-weight fragments from the pre-packed weight (one contiguous
-//     1 KB per load instruction, one stage ahead, L2-resident) straight into registers, reads
-//     the hidden fragments from LDS, and runs v_mfma_f32_32x32x16_bf16 (or 32x32x2 f32).  The
-//     router weight is the A operand (M = experts) and the hidden tile is B (N = tokens), so
-//     each lane ends with groups of four consecutive experts of one token.  The 32x32 shape
-//     does the same contraction with half the instructions of the 16x16 one and, measured on
-//     MI355X, less time and energy per flop, which matters because this kernel runs at the
-//     board's power limit.
+//     1 KB per load instruction, L2-resident) straight into registers through a ring of eight
+//     k-step slices that runs seven k-steps ahead of the MFMAs, reads the hidden fragments from
+//     LDS one k-step ahead, and runs v_mfma_f32_32x32x16_bf16 (or 32x32x2 f32).  The router weight
+//     is the A operand (M = experts) and the hidden tile is B (N = tokens), so each lane ends with
+//     groups of four consecutive experts of one token.  The 32x32 shape does the same contraction
+//     with half the instructions of the 16x16 one and, measured on MI355X, less time and energy per
+//     flop, which matters because this kernel runs at the board's power limit.
 //   * The two global streams (HBM hidden rows, L2 router weight) live in different waves, so a
 //     short-latency weight load never waits in the in-order vmcnt queue behind a hidden-row load.
-//   * One LDS barrier per k-stage couples producers and consumers.
-// The logits never leave the chip: scores go to an LDS tile, EPAD/16 lanes cooperate on one
+//   * One LDS barrier per stage couples producers and consumers.
+// The logits never leave the chip: scores go to an LDS tile, EPAD/32 lanes cooperate on one
 // token, and the histogram is privatised in LDS with one global atomic per expert per workgroup.
 //
 // Selection is exact in float32 with ties to the lower expert index.  The fast path ranks 32-bit
@@ -46,8 +47,12 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int kProducers = 4;
+#ifndef FB_STAGE_BYTES
+#define FB_STAGE_BYTES 256
+#endif
 constexpr int kStepBytes = 32;                  // bytes of a row feeding one MFMA k-step
-constexpr int kNStep = 4;                       // k-steps per pipeline stage
+constexpr int kNStep = FB_STAGE_BYTES / kStepBytes;  // k-steps per pipeline stage
+constexpr int kRing = 8;                        // router-weight k-step slices held per consumer
 constexpr int kStageRowBytes = kStepBytes * kNStep;
 constexpr int kPitch = kStageRowBytes + 16;     // LDS row pitch of a hidden stage
 constexpr int kMaxK = FB_MAX_TOPK;
@@ -64,15 +69,6 @@ constexpr uint32_t kOobOffset = 0x80000000u;    // fails the buffer range check:
 #define FB_SEL_CACHE 5
 #endif
 constexpr int kCache = FB_SEL_CACHE;            // per-lane cached keys in the top-k extraction
-#ifndef FB_B_PIPELINE
-#define FB_B_PIPELINE 1
-#endif
-#ifndef FB_W_RING
-#define FB_W_RING 1
-#endif
-#ifndef FB_W_INTERLEAVE
-#define FB_W_INTERLEAVE 1
-#endif
 constexpr int kDX = FB_PRODUCER_DEPTH;          // stages of hidden rows in flight per producer
 constexpr int kStageUnroll = kDX % 2 == 0 ? kDX : 2 * kDX;  // multiple of kDX and of 2
 
@@ -172,21 +168,22 @@ __device__ __forceinline__ void top2_group(float& m1, float& m2, int g) {
 }
 
 // ---- packed router weight --------------------------------------------------------------------
-// Stage st (128 bytes of every row) occupies EPAD * 128 contiguous bytes.  Inside it, the 1 KB
-// chunk c = (we * 4 + q) * FE + fe holds, for lane l, the 16 bytes of row
-// e = we * EW + fe * 32 + (l & 31) at byte st * 128 + q * 32 + (l >> 5) * 16 of that row: exactly
-// the A-operand fragment consumer wave `we` loads for expert block fe of k-step q.  Rows >= E and
-// bytes past H are zero.
+// Stage st (kStageRowBytes of every row) occupies EPAD * kStageRowBytes contiguous bytes.  Inside
+// it, the 1 KB chunk c = (we * kNStep + q) * FE + fe holds, for lane l, the 16 bytes of row
+// e = we * EW + fe * 32 + (l & 31) at byte st * kStageRowBytes + q * 32 + (l >> 5) * 16 of that row:
+// exactly the A-operand fragment consumer wave `we` loads for expert block fe of k-step q.  Rows >= E
+// and bytes past H are zero.
 template <int EPAD>
 __global__ void pack_kernel(const char* __restrict__ w, int32_t E, int32_t Hbytes, int32_t nstages,
                             u32x4* __restrict__ out) {
   using Cfg = TileCfg<EPAD>;
   constexpr int EW = EPAD / Cfg::WE, FE = EW / 32;
-  const int64_t units = (int64_t)nstages * EPAD * 8;
+  constexpr int kUnitsPerStage = EPAD * (kStageRowBytes / 16);   // 16-byte units
+  const int64_t units = (int64_t)nstages * kUnitsPerStage;
   for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < units;
        idx += (int64_t)gridDim.x * blockDim.x) {
-    const int st = (int)(idx / (EPAD * 8));
-    const int rem = (int)(idx % (EPAD * 8));
+    const int st = (int)(idx / kUnitsPerStage);
+    const int rem = (int)(idx % kUnitsPerStage);
     const int c = rem >> 6, l = rem & 63;
     const int fe = c % FE, q = (c / FE) % kNStep, we = c / (FE * kNStep);
     const int e = we * EW + fe * 32 + (l & 31);
@@ -205,7 +202,9 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   constexpr int EW = EPAD / WE, TW = BM / WT;
   constexpr int FE = EW / 32, FT = TW / 32;
   constexpr int RPW = BM / kProducers;           // hidden rows per producer wave
-  constexpr int LPW = RPW / 8;                   // full-line loads per producer per stage
+  constexpr int LPR = kStageRowBytes / 16;       // lanes per row of a stage (16 bytes each)
+  constexpr int RPI = 64 / LPR;                  // rows per load instruction
+  constexpr int LPW = RPW / RPI;                 // loads per producer per stage
   constexpr int XSTAGE = BM * kPitch;
   constexpr int SB = EPAD * kStageRowBytes;      // packed weight bytes per stage
   constexpr int SROW = EPAD + 4;                 // score-tile row stride in floats
@@ -215,7 +214,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   constexpr int TPP = kThreads / LPT;            // tokens per selection pass
   constexpr int NPASS = (BM + TPP - 1) / TPP;
   constexpr int GSC_TOK = TPP < BM ? TPP : BM;
-  static_assert(LPW >= 1 && RPW % 8 == 0, "producers split the tile in 8-row groups");
+  static_assert(LPW >= 1 && RPW % RPI == 0, "producers split the tile in whole load instructions");
   static_assert(WE * WT == kWaves - kProducers, "one consumer per SIMD");
   static_assert(EW % 32 == 0 && TW % 32 == 0, "wave tiles are whole 32 x 32 MFMA blocks");
   static_assert(TPP % 64 == 0, "selection passes cover whole waves");
@@ -274,11 +273,11 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       const int64_t rows = (p.T - row0) < BM ? (p.T - row0) : BM;
       const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
           (void*)(p.x + row0 * (int64_t)p.ldx_bytes), (short)0, (int)(rows * p.ldx_bytes), kRsrcWord3);
-      const int col = (lane & 7) * 16;           // byte within the 128-byte stage segment
+      const int col = (lane % LPR) * 16;         // byte within the stage segment of a row
       uint32_t xoff[LPW], loff[LPW];
 #pragma unroll
       for (int i = 0; i < LPW; ++i) {
-        const int r = wave * RPW + i * 8 + (lane >> 3);
+        const int r = wave * RPW + i * RPI + lane / LPR;
         xoff[i] = (uint32_t)(r * p.ldx_bytes + col);
         loff[i] = (uint32_t)(r * kPitch + col);
       }
@@ -309,107 +308,57 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       }
     } else {
       // ---- consumers: packed router weight L2 -> registers, hidden fragments from LDS --------
+      // Weight fragments live in a ring of kRing k-step slices (global k-step g in slot g % kRing);
+      // each k-step refills the slot the previous one consumed with the slice kRing - 1 k-steps
+      // ahead, so weight loads lead the MFMAs by kRing - 1 k-steps.
       const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
           (void*)p.wpack, (short)0, nst * SB, kRsrcWord3);
-      uint32_t woff[FE][kNStep];
-#pragma unroll
-      for (int fe = 0; fe < FE; ++fe)
-#pragma unroll
-        for (int q = 0; q < kNStep; ++q)
-          woff[fe][q] = (uint32_t)(((we * kNStep + q) * FE + fe) * 1024 + lane * 16);
+      const uint32_t wbase = (uint32_t)(we * kNStep * FE * 1024 + lane * 16);
       const uint32_t boff = (uint32_t)((wt * TW + (lane & 31)) * kPitch + (lane >> 5) * 16);
-      u32x4 wa[2][FE][kNStep];
-      auto load_w = [&](u32x4(&dst)[FE][kNStep], int st) {
+      u32x4 ring[kRing][FE];
+      auto load_slice = [&](u32x4(&dst)[FE], int st, int q) {
         const bool ok = st < nst;
 #pragma unroll
         for (int fe = 0; fe < FE; ++fe)
-#pragma unroll
-          for (int q = 0; q < kNStep; ++q)
-            dst[fe][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? woff[fe][q] : kOobOffset,
-                                                               ok ? phys(st) * SB : 0, 0);
+          dst[fe] = __builtin_amdgcn_raw_buffer_load_b128(
+              wr, ok ? wbase + (uint32_t)((q * FE + fe) * 1024) : kOobOffset, ok ? phys(st) * SB : 0, 0);
       };
-#if FB_W_RING
-      // The two stage buffers form a ring of eight k-step slices; each k-step refills the slice the
-      // previous one consumed with the slice seven k-steps ahead.
-      load_w(wa[0], 0);
-      {
-        const bool ok = 1 < nst;
 #pragma unroll
-        for (int fe = 0; fe < FE; ++fe)
-#pragma unroll
-          for (int q = 0; q < kNStep - 1; ++q)
-            wa[1][fe][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? woff[fe][q] : kOobOffset,
-                                                                 ok ? phys(1) * SB : 0, 0);
-      }
-#else
-      load_w(wa[0], 0);
-#endif
+      for (int g = 0; g < kRing - 1; ++g) load_slice(ring[g], g / kNStep, g % kNStep);
       for (int st0 = 0; st0 < NP; st0 += 2) {
 #pragma unroll
         for (int d = 0; d < 2; ++d) {
           const int st = st0 + d;
-#if !FB_W_INTERLEAVE && !FB_W_RING
-          load_w(wa[d ^ 1], st + 1);
-          __builtin_amdgcn_sched_barrier(0);
-#endif
           lds_barrier();                         // stage st is in LDS
           const char* buf = smem + (st & 1) * XSTAGE;
-#if FB_B_PIPELINE
           // hidden fragments one k-step ahead, so only the first read of a stage waits on LDS
           u32x4 bq[2][FT];
 #pragma unroll
           for (int ft = 0; ft < FT; ++ft)
             bq[0][ft] = *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + boff);
-#endif
 #pragma unroll
           for (int q = 0; q < kNStep; ++q) {
-#if FB_B_PIPELINE
             if (q + 1 < kNStep) {
 #pragma unroll
               for (int ft = 0; ft < FT; ++ft)
                 bq[(q + 1) & 1][ft] =
                     *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + (q + 1) * kStepBytes + boff);
             }
-#endif
-#if FB_W_RING
-            {
-              const int tst = st + (q + 7) / kNStep;   // k-step 4 st + q + 7
-              const int tq = (q + 7) % kNStep;
-              const bool ok = tst < nst;
-#pragma unroll
-              for (int fe = 0; fe < FE; ++fe)
-                wa[q > 0 ? d : d ^ 1][fe][q > 0 ? q - 1 : kNStep - 1] = __builtin_amdgcn_raw_buffer_load_b128(
-                    wr, ok ? woff[fe][tq] : kOobOffset, ok ? phys(tst) * SB : 0, 0);
-            }
-#elif FB_W_INTERLEAVE
-            // the next stage's fragments for this k-step, spread between the MFMA groups
-            {
-              const bool ok = st + 1 < nst;
-#pragma unroll
-              for (int fe = 0; fe < FE; ++fe)
-                wa[d ^ 1][fe][q] = __builtin_amdgcn_raw_buffer_load_b128(
-                    wr, ok ? woff[fe][q] : kOobOffset, ok ? phys(st + 1) * SB : 0, 0);
-            }
-#endif
-#if FB_B_PIPELINE
+            const int slot = (kNStep * d + q) % kRing;             // compile-time after unrolling
+            load_slice(ring[(slot + kRing - 1) % kRing], st + (q + kRing - 1) / kNStep,
+                       (q + kRing - 1) % kNStep);
             const u32x4* bfr = bq[q & 1];
-#else
-            u32x4 bfr[FT];
-#pragma unroll
-            for (int ft = 0; ft < FT; ++ft)
-              bfr[ft] = *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + q * kStepBytes + boff);
-#endif
 #pragma unroll
             for (int ft = 0; ft < FT; ++ft) {
 #pragma unroll
               for (int fe = 0; fe < FE; ++fe) {
                 if constexpr (BF16) {
                   acc[fe][ft] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                      __builtin_bit_cast(bf16x8, wa[d][fe][q]), __builtin_bit_cast(bf16x8, bfr[ft]),
+                      __builtin_bit_cast(bf16x8, ring[slot][fe]), __builtin_bit_cast(bf16x8, bfr[ft]),
                       acc[fe][ft], 0, 0, 0);
                 } else {
                   // four k-pairs per fragment; A and B take the same k for every lane
-                  const f32x4 av = __builtin_bit_cast(f32x4, wa[d][fe][q]);
+                  const f32x4 av = __builtin_bit_cast(f32x4, ring[slot][fe]);
                   const f32x4 bv = __builtin_bit_cast(f32x4, bfr[ft]);
 #pragma unroll
                   for (int j = 0; j < 4; ++j)
@@ -417,9 +366,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
                 }
               }
             }
-#if FB_W_INTERLEAVE || FB_B_PIPELINE || FB_W_RING
             __builtin_amdgcn_sched_barrier(0);
-#endif
           }
         }
       }
@@ -728,7 +675,7 @@ int epad_of(int32_t E) {
 template <int EPAD>
 int launch_pack_cfg(const void* w, int32_t E, int32_t Hbytes, void* out, void* stream) {
   const int32_t nst = (Hbytes + kStageRowBytes - 1) / kStageRowBytes;
-  const int64_t units = (int64_t)nst * EPAD * 8;
+  const int64_t units = (int64_t)nst * EPAD * (kStageRowBytes / 16);
   const int64_t blocks64 = (units + 255) / 256;
   const int blocks = (int)(blocks64 < 4096 ? (blocks64 > 0 ? blocks64 : 1) : 4096);
   hipLaunchKernelGGL((pack_kernel<EPAD>), dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream),

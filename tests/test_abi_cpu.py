@@ -63,12 +63,12 @@ def test_version_and_status_strings():
                                        (256, 7168, L.FB_F32), (33, 48, L.FB_F32)])
 def test_packed_router_and_workspace_sizes(E, H, dtype):
     """The packed weight holds E rounded up to 32, 64, 128 or 256 rows of H elements rounded up
-    to whole 128-byte stages; the unpacked entry point's workspace adds 2 KB of accumulators."""
+    to whole 256-byte stages; the unpacked entry point's workspace adds 2 KB of accumulators."""
     lib = fb.lib()
     hb = H * (2 if dtype == L.FB_BF16 else 4)
     epad = next(p for p in (32, 64, 128, 256) if E <= p)
     packed = lib.fb_router_packed_bytes(E, H, dtype)
-    assert packed == epad * (-(-hb // 128)) * 128
+    assert packed == epad * (-(-hb // 256)) * 256
     assert lib.fb_predict_workspace_bytes(E, H, dtype) == packed + 2048
 
 
@@ -90,10 +90,10 @@ def test_packed_sizes_reject_invalid():
     (dict(H=48), L.FB_EUNSUPPORTED),
     (dict(w=0x2004), L.FB_EUNSUPPORTED),
     (dict(out=0x3008), L.FB_EUNSUPPORTED),
-    (dict(nbytes=4095), L.FB_ENOSPC),
+    (dict(nbytes=8191), L.FB_ENOSPC),
 ])
 def test_pack_validation_without_gpu(over, code):
-    a = dict(w=0x2000, E=16, H=64, dtype=L.FB_BF16, out=0x3000, nbytes=4096)
+    a = dict(w=0x2000, E=16, H=64, dtype=L.FB_BF16, out=0x3000, nbytes=8192)
     a.update(over)
     assert fb.lib().fb_pack_router_weight(a["w"], a["E"], a["H"], a["dtype"], a["out"], a["nbytes"],
                                           None) == code
@@ -262,7 +262,7 @@ def test_predict_validation_without_gpu(over, code):
 
 def _predict_packed_call(**over):
     """fb_predict_load_packed with fake (never dereferenced) pointers."""
-    a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, wp=0x2000, wpb=4096, E=16, lb=None,
+    a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, wp=0x2000, wpb=8192, E=16, lb=None,
              sb=None, sc=fb.Scoring("softmax", 2).to_c(), e2r=0x3000, R=4, counts=0x4000,
              rl=0x5000, mm=0x6000, ws=0x7000, wsb=2048, topk=None, logits=None, stream=None)
     a.update(over)
@@ -276,7 +276,7 @@ def _predict_packed_call(**over):
 @pytest.mark.parametrize("over,code", [
     (dict(wp=None), L.FB_EINVAL),
     (dict(wp=0x2008), L.FB_EUNSUPPORTED),
-    (dict(wpb=4095), L.FB_ENOSPC),                       # packed weight too small for E, H
+    (dict(wpb=8191), L.FB_ENOSPC),                       # packed weight too small for E, H
     (dict(E=33), L.FB_ENOSPC),                           # 33 experts pack into 64 rows
     (dict(wsb=2047), L.FB_ENOSPC),                       # accumulators need 2 KB
     (dict(sc=None), L.FB_EINVAL),
@@ -289,7 +289,7 @@ def test_predict_packed_validation_without_gpu(over, code):
 
 
 def test_unpacked_predict_needs_room_for_the_packed_weight():
-    assert _predict_call(wsb=2048 + 4096 - 1) == L.FB_ENOSPC
+    assert _predict_call(wsb=2048 + 8192 - 1) == L.FB_ENOSPC
 
 
 def test_diagnostics_validation_without_gpu():

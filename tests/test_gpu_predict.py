@@ -193,16 +193,16 @@ def _pack_reference(w_bytes: np.ndarray, E: int, row_bytes: int) -> np.ndarray:
     epad = next(p for p in (32, 64, 128, 256) if E <= p)
     W = 4 if epad >= 128 else (2 if epad == 64 else 1)
     F = epad // (32 * W)
-    nst = -(-row_bytes // 128)
-    src = np.zeros((epad, nst * 128), np.uint8)
+    nst = -(-row_bytes // 256)
+    src = np.zeros((epad, nst * 256), np.uint8)
     src[:E, :row_bytes] = w_bytes.reshape(E, row_bytes)
-    out = np.zeros((nst, epad // 8, 64, 16), np.uint8)
+    out = np.zeros((nst, epad // 4, 64, 16), np.uint8)
     for st in range(nst):
-        for c in range(epad // 8):
-            f, q, w = c % F, (c // F) % 4, c // (4 * F)
+        for c in range(epad // 4):
+            f, q, w = c % F, (c // F) % 8, c // (8 * F)
             for l in range(64):
                 row = w * (epad // W) + f * 32 + (l % 32)
-                b = st * 128 + q * 32 + (l // 32) * 16
+                b = st * 256 + q * 32 + (l // 32) * 16
                 out[st, c, l] = src[row, b:b + 16]
     return out.reshape(-1)
 
