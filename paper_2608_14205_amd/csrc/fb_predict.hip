@@ -6,24 +6,23 @@
 // last workgroup to finish folds the histogram into per-rank loads under the expert-to-rank
 // placement (Alg. 1, second step) and computes the max-to-mean ratio (Sec. "Metrics").
 //
-// Workgroup: 8 waves (512 threads), one workgroup per CU.  The contraction runs in k-stages of
-// 256 bytes of every row (128 bf16 / 64 f32 elements).
-//   * Waves 0-3 are producers.  They stream the tile's hidden rows from HBM with full 128-byte
-//     line requests (4 rows x 256 B per instruction), two stages ahead, and store them row-major
-//     into a double-buffered LDS stage (row pitch 272 B, so both the stores and the fragment reads
-//     below stay conflict-free).
-//   * Waves 4-7 are consumers, one per SIMD next to a producer.  Each owns a slice of the
-//     experts.  It loads its router-weight fragments from the pre-packed weight (one contiguous
-//     1 KB per load instruction, L2-resident) straight into registers through a ring of eight
-//     k-step slices that runs seven k-steps ahead of the MFMAs, reads the hidden fragments from
-//     LDS one k-step ahead, and runs v_mfma_f32_32x32x16_bf16 (or 32x32x2 f32).  The router weight
-//     is the A operand (M = experts) and the hidden tile is B (N = tokens), so each lane ends with
-//     groups of four consecutive experts of one token.  The 32x32 shape does the same contraction
-//     with half the instructions of the 16x16 one and, measured on MI355X, less time and energy per
-//     flop, which matters because this kernel runs at the board's power limit.
-//   * The two global streams (HBM hidden rows, L2 router weight) live in different waves, so a
-//     short-latency weight load never waits in the in-order vmcnt queue behind a hidden-row load.
-//   * One LDS barrier per stage couples producers and consumers.
+// Workgroup: 4 waves (256 threads), one per SIMD, one workgroup per CU.  A wave may then hold up to
+// 512 registers, which the contraction spends on deep prefetching rather than on extra waves:
+//   * Hidden rows go from HBM straight into LDS (buffer_load ... lds, 16 bytes per lane): no
+//     register round trip and no LDS store instructions.  The k dimension runs in stages of 256
+//     bytes of every row; a ring of NS stage buffers keeps up to NS - 1 stages in flight beyond the
+//     one being read.  Each
+//     workgroup-wide load instruction writes 4 rows x 256 bytes; inside a row the 16-byte chunks are
+//     XOR-swizzled by the row index so the fragment reads below are free of bank conflicts.
+//   * Each wave owns a slice of the experts (and, for small E, of the tokens).  Its router-weight
+//     fragments come from the pre-packed weight (one contiguous 1 KB per load instruction,
+//     L2-resident) straight into registers through a ring of 16 k-step slices, 15 k-steps ahead of
+//     the MFMAs; the hidden fragments are read from LDS one k-step ahead.  The router weight is the
+//     A operand (M = experts) and the hidden tile is B (N = tokens): v_mfma_f32_32x32x16_bf16 (or
+//     32x32x2 f32), so each lane ends with groups of four consecutive experts of one token.
+//   * One workgroup barrier per stage, placed before the stage's last k-step: it publishes the next
+//     stage (every wave waits for its own share of that stage's loads first) and frees the buffer
+//     just read, which the next load batch then refills.  Waits are counted, never drained.
 // The logits never leave the chip: scores go to an LDS tile, EPAD/32 lanes cooperate on one
 // token, and the histogram is privatised in LDS with one global atomic per expert per workgroup.
 //
@@ -43,42 +42,35 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr;
 
-constexpr int kThreads = 512;
+constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kProducers = 4;
-#ifndef FB_STAGE_BYTES
-#define FB_STAGE_BYTES 256
-#endif
 constexpr int kStepBytes = 32;                  // bytes of a row feeding one MFMA k-step
-constexpr int kNStep = FB_STAGE_BYTES / kStepBytes;  // k-steps per pipeline stage
-constexpr int kRing = 8;                        // router-weight k-step slices held per consumer
-constexpr int kStageRowBytes = kStepBytes * kNStep;
-constexpr int kPitch = kStageRowBytes + 16;     // LDS row pitch of a hidden stage
+constexpr int kNStep = 8;                       // k-steps per stage
+constexpr int kStageRowBytes = kStepBytes * kNStep;   // 256
+constexpr int kRingW = 16;                      // router-weight k-step slices held per wave
 constexpr int kMaxK = FB_MAX_TOPK;
 constexpr int kMaxGroups = 32;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;    // raw buffer, 32-bit dwords
 constexpr uint32_t kOobOffset = 0x80000000u;    // fails the buffer range check: load returns 0
-#ifndef FB_PRODUCER_DEPTH
-#define FB_PRODUCER_DEPTH 2
-#endif
-#ifndef FB_STAGE_ROTATE
-#define FB_STAGE_ROTATE 0
-#endif
 #ifndef FB_SEL_CACHE
 #define FB_SEL_CACHE 5
 #endif
 constexpr int kCache = FB_SEL_CACHE;            // per-lane cached keys in the top-k extraction
-constexpr int kDX = FB_PRODUCER_DEPTH;          // stages of hidden rows in flight per producer
-constexpr int kStageUnroll = kDX % 2 == 0 ? kDX : 2 * kDX;  // multiple of kDX and of 2
 
-// Consumer tile shapes: WE waves along experts x WT waves along tokens, BM tokens per workgroup;
-// every wave tile is a whole number of 32 x 32 MFMA blocks.
+// Tile shapes: WE waves along experts x WT waves along tokens, BM tokens per workgroup; every wave
+// tile is a whole number of 32 x 32 MFMA blocks.
 template <int EPAD> struct TileCfg;
 template <> struct TileCfg<256> { static constexpr int WE = 4, WT = 1, BM = 128; };
 template <> struct TileCfg<128> { static constexpr int WE = 4, WT = 1, BM = 64; };
 template <> struct TileCfg<64> { static constexpr int WE = 2, WT = 2, BM = 64; };
 template <> struct TileCfg<32> { static constexpr int WE = 1, WT = 4, BM = 128; };
+
+// Stages of the LDS ring for a tile height.  Each wave may have at most 63 vector-memory loads in
+// flight; NS is the deepest ring whose counted waits stay below that (checked in the kernel).
+constexpr int ring_stages(int BM) { return BM >= 128 ? 3 : 4; }
 
 struct Params {
   const char* x;
@@ -116,6 +108,47 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
 }
 
+// 32-bit LDS address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16-byte LDS read as an instruction of its own; its completion is awaited with lgkm_wait.
+__device__ __forceinline__ void ds_read_b128(u32x4& dst, uint32_t addr, int offset) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "i"(offset));
+}
+template <int N>
+__device__ __forceinline__ void lgkm_wait() {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N));
+}
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N));
+}
+// 16-byte buffer load into accumulation registers, as an instruction of its own; its completion is
+// awaited with vm_wait.  rsrc: buffer descriptor (base, num_records bytes, raw 32-bit words).
+__device__ __forceinline__ void buffer_load_b128_acc(u32x4& dst, const i32x4& rsrc, uint32_t voff,
+                                                     uint32_t soff) {
+  asm volatile("buffer_load_dwordx4 %0, %1, %2, %3 offen" : "=a"(dst) : "v"(voff), "s"(rsrc), "s"(soff));
+}
+// After an explicit wait: the values below are (re)defined here, so nothing reads them earlier.
+template <int N>
+__device__ __forceinline__ void pin(u32x4 (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
+template <int N>
+__device__ __forceinline__ void pin_acc(u32x4 (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+a"(v[i]));
+}
+
+// s_waitcnt immediate: at most `vm` vector-memory loads outstanding (6-bit count) and at most `lgkm`
+// LDS/scalar operations (expcnt left free).
+constexpr int waitcnt_imm(int vm, int lgkm) {
+  return (vm & 15) | (((vm >> 4) & 3) << 14) | (7 << 4) | ((lgkm & 15) << 8);
+}
+
 // Order-preserving map of float bits to unsigned (for finite values; -0 is canonicalised first).
 __device__ __forceinline__ uint32_t ord_bits(float s) {
   uint32_t u = __float_as_uint(s);
@@ -139,6 +172,7 @@ __device__ __forceinline__ float dpp_f32(float v) {
 // DPP patterns that stay inside aligned groups of 2, 4, 8 and 16 lanes.
 constexpr int kXor1 = 0xB1;       // quad_perm [1,0,3,2]
 constexpr int kXor2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kXor3 = 0x1B;       // quad_perm [3,2,1,0]
 constexpr int kHalfMirror = 0x141;
 constexpr int kMirror = 0x140;
 
@@ -167,12 +201,39 @@ __device__ __forceinline__ void top2_group(float& m1, float& m2, int g) {
   if (g >= 16) top2_merge_step<kMirror>(m1, m2);
 }
 
+// Rank of this lane's group among the groups of its token (score desc, lower group first), for
+// groups that each cover lpg whole lanes of the token's G lanes (lane jl covers experts 32 jl ..
+// 32 jl + 31; lanes at or past E hold no group).  Values of the other lanes of the aligned
+// G-lane group come in by lane exchange: lanes jl ^ 1..3 through quad permutations, lanes
+// jl ^ 4..7 through the half-row mirror (lane jl ^ 7) followed by the same permutations.
+template <int G>
+__device__ __forceinline__ int group_rank(float g, int jl, int lpg, int E) {
+  float v[8];
+  v[0] = g;
+  if constexpr (G >= 2) v[1] = dpp_f32<kXor1>(g);
+  if constexpr (G >= 4) { v[2] = dpp_f32<kXor2>(g); v[3] = dpp_f32<kXor3>(g); }
+  if constexpr (G >= 8) {
+    const float m = dpp_f32<kHalfMirror>(g);   // lane jl ^ 7
+    v[7] = m; v[6] = dpp_f32<kXor1>(m); v[5] = dpp_f32<kXor2>(m); v[4] = dpp_f32<kXor3>(m);
+  }
+  const int me = jl / lpg;
+  int rank = 0;
+#pragma unroll
+  for (int x = 1; x < G; ++x) {
+    const int j = jl ^ x;
+    const bool counts = (j % lpg) == 0 && j * 32 < E;
+    const float o = v[x];
+    rank += counts && (o > g || (o == g && j / lpg < me));
+  }
+  return rank;
+}
+
 // ---- packed router weight --------------------------------------------------------------------
 // Stage st (kStageRowBytes of every row) occupies EPAD * kStageRowBytes contiguous bytes.  Inside
 // it, the 1 KB chunk c = (we * kNStep + q) * FE + fe holds, for lane l, the 16 bytes of row
 // e = we * EW + fe * 32 + (l & 31) at byte st * kStageRowBytes + q * 32 + (l >> 5) * 16 of that row:
-// exactly the A-operand fragment consumer wave `we` loads for expert block fe of k-step q.  Rows >= E
-// and bytes past H are zero.
+// exactly the A-operand fragment wave `we` loads for expert block fe of k-step q.  Rows >= E and
+// bytes past H are zero.
 template <int EPAD>
 __global__ void pack_kernel(const char* __restrict__ w, int32_t E, int32_t Hbytes, int32_t nstages,
                             u32x4* __restrict__ out) {
@@ -194,6 +255,192 @@ __global__ void pack_kernel(const char* __restrict__ w, int32_t E, int32_t Hbyte
   }
 }
 
+// ---- the contraction ---------------------------------------------------------------------------
+// acc[fe][ft] += (router weight block fe) x (hidden block ft) over every stage of the tile; the NS
+// stage buffers start at ring_lds.
+template <bool BF16, int EPAD, int FE, int FT, int NS, int BM, int TW>
+__device__ __forceinline__ void contract(f32x16 (&acc)[FE][FT], const Params& p, int64_t row0,
+                                         int wave, int we, int wt, int lane, char* ring_lds) {
+  constexpr int LPW = BM / 4 / kWaves;               // stage load instructions per wave (4 rows each)
+  constexpr int UNROLL = kRingW / kNStep;            // one period of the weight ring per iteration
+  constexpr int STAGE = BM * kStageRowBytes;         // LDS bytes of one stage buffer
+  // counted waits (see the issue order below): loads issued after a stage's own batch by the time
+  // the stage must be resident, and the most a wave ever has in flight
+  constexpr int kWaitStage = 8 * FE * (NS - 1) + (NS - 2) * LPW;
+  // the batch of stage t goes out at the end of stage t - NS, right before the weight slice of
+  // k-step kLead + 8 t; the prologue keeps that order for stages 0 .. NS-1
+  constexpr int kLead = kNStep - 1 + kRingW - 1 - kNStep * NS;
+  static_assert(kLead < 0, "stage 0's batch precedes every weight slice");
+  // Batches the prologue issues before any weight slice have fewer loads behind them than the
+  // steady-state count assumes; the prologue waits for all of them (they went out together).
+  constexpr int kEarly = (-kLead + kNStep - 1) / kNStep;          // stages t with kLead + 8 t < 0
+  constexpr int kWaitFirst = (NS - kEarly) * LPW + (kRingW - 1) * FE;
+  static_assert(kWaitStage <= 63 && (kRingW - 1) * FE + NS * LPW <= 63,
+                "more loads in flight than a wave can count");
+  static_assert(LPW >= 1 && BM % (4 * kWaves) == 0, "stage loads split evenly over the waves");
+  static_assert(kRingW % kNStep == 0, "the weight ring holds whole stages");
+  const uint32_t lds0 = lds_addr(ring_lds);
+  const int nst = p.nstages;
+  const int Hb = p.Hbytes;
+  const int64_t rows = (p.T - row0) < BM ? (p.T - row0) : BM;
+
+  // hidden rows: rows past T are outside the buffer and read as zero
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.x + row0 * (int64_t)p.ldx_bytes), (short)0, (int)(rows * p.ldx_bytes), kRsrcWord3);
+  // Load instruction j of this wave fills rows 4 (wave LPW + j) + (lane >> 4); lane l writes the
+  // 16-byte slot (l & 15) of its row, which holds logical chunk (l & 15) ^ (row & 15).
+  uint32_t voff[LPW];
+  int cbyte[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int r = 4 * (wave * LPW + j) + (lane >> 4);
+    const int c = (lane & 15) ^ (r & 15);
+    voff[j] = (uint32_t)(r * p.ldx_bytes + c * 16);
+    cbyte[j] = c * 16;
+  }
+  // a stage's batch; bytes at or past H (tail of the last stage) and stages past the end are not
+  // fetched and land as zeros
+  // The counted waits below assume each batch goes out whole, in program order with the weight
+  // slices: the scheduling barriers keep other loads from moving into or across it.
+  auto load_stage = [&](int bi, int st) {        // bi: stage buffer (wave-uniform)
+    const bool live = st < nst;
+    const int sb = live ? st * kStageRowBytes : 0;
+    const int lim = live ? Hb - sb : 0;           // bytes of the stage inside the row (scalar)
+    char* const dst = ring_lds + bi * STAGE + wave * LPW * 1024;
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+      const uint32_t off = cbyte[j] < lim ? voff[j] : kOobOffset;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr)(dst + j * 1024), 16, off, sb, 0, 2);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // router weight: stage st of the packed layout is EPAD * 256 bytes; this wave's fragment of
+  // k-step q and expert block fe is the 1 KB chunk (we * kNStep + q) * FE + fe.  These loads are
+  // instructions of their own (into accumulation registers, which the MFMAs read directly) with
+  // counted waits: the issue order is fixed, so the count of loads issued after a k-step's slice is
+  // known exactly, where the compiler's own tracking turns conservative at the loop head.
+  constexpr int kPackStage = EPAD * kStageRowBytes;
+  const uint64_t wbase_addr = reinterpret_cast<uint64_t>(p.wpack);
+  const i32x4 wr = {(int32_t)(uint32_t)wbase_addr, (int32_t)(uint32_t)(wbase_addr >> 32),
+                    nst * kPackStage, (int32_t)kRsrcWord3};
+  const uint32_t wbase = (uint32_t)(we * kNStep * FE * 1024 + lane * 16);
+  auto load_w = [&](u32x4(&dst)[FE], int st, int q) {
+    const bool ok = st < nst;
+#pragma unroll
+    for (int fe = 0; fe < FE; ++fe)
+      buffer_load_b128_acc(dst[fe], wr, ok ? wbase + (uint32_t)((q * FE + fe) * 1024) : kOobOffset,
+                           ok ? st * kPackStage : 0);
+  };
+  // loads issued after the weight slice of k-step q (of any stage) by the time its MFMAs start: the
+  // slices of the next kRingW - 1 k-steps, and the stage batches issued at k-step 7 of the stages
+  // in between (two of them, except for q = 6, whose window holds one)
+  auto wait_w = [&](int q) {
+    if (q == kNStep - 2) vm_wait<(kRingW - 1) * FE + LPW>();
+    else vm_wait<(kRingW - 1) * FE + 2 * LPW>();
+  };
+  static_assert(kRingW - 1 > kNStep && kRingW - 1 < 2 * kNStep, "two stage batches per weight window");
+
+  // hidden fragment of k-step q: token wt TW + ft 32 + (lane & 31), logical chunk 2q + (lane >> 5).
+  // These LDS reads are written as instructions of their own, with their waits counted below: the
+  // compiler cannot tell a read of one ring buffer from the stage loads still filling another and
+  // would otherwise wait for every load in flight before each read.
+  uint32_t baddr[kNStep];
+#pragma unroll
+  for (int q = 0; q < kNStep; ++q)
+    baddr[q] = lds0 + (uint32_t)((wt * TW + (lane & 31)) * kStageRowBytes +
+                                 (((2 * q + (lane >> 5)) ^ (lane & 15)) * 16));
+  auto load_b = [&](u32x4(&dst)[FT], int bi, int q) {
+    const uint32_t a = baddr[q] + (uint32_t)(bi * STAGE);
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) ds_read_b128(dst[ft], a, ft * 32 * kStageRowBytes);
+  };
+
+  auto mma = [&](const u32x4(&a)[FE], const u32x4(&b)[FT]) {
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) {
+#pragma unroll
+      for (int fe = 0; fe < FE; ++fe) {
+        if constexpr (BF16) {
+          acc[fe][ft] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, a[fe]), __builtin_bit_cast(bf16x8, b[ft]), acc[fe][ft], 0, 0, 0);
+        } else {
+          // four k-pairs per fragment; A and B take the same k for every lane
+          const f32x4 av = __builtin_bit_cast(f32x4, a[fe]);
+          const f32x4 bv = __builtin_bit_cast(f32x4, b[ft]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[fe][ft] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[j], bv[j], acc[fe][ft], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  // ---- prologue: stages 0 .. NS-1 and k-steps 0 .. kRingW-2 in flight, then stage 0 published.
+  // Loads go out in the steady state's order, so every wait at the loop head counts the same loads
+  // on both paths into it.
+  u32x4 ring[kRingW][FE];
+  u32x4 bq[2][FT];
+#pragma unroll
+  for (int t = 0; t < NS; ++t)
+    if (kLead + kNStep * t < 0) load_stage(t, t);
+#pragma unroll
+  for (int g = 0; g < kRingW - 1; ++g) {
+#pragma unroll
+    for (int t = 0; t < NS; ++t)
+      if (kLead + kNStep * t == g) load_stage(t, t);
+    load_w(ring[g], g / kNStep, g % kNStep);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int t = 0; t < NS; ++t)
+    if (kLead + kNStep * t >= kRingW - 1) load_stage(t, t);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(kWaitFirst, 0));
+  asm volatile("s_barrier" ::: "memory");
+  load_b(bq[0], 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- steady state.  Issue order per stage: k-steps 0..6 each read the next hidden fragments
+  // and one weight slice; k-step 7 waits for this wave's share of stage s+1, meets the other waves
+  // (after which stage s is no longer read and stage s+1 is complete), refills stage s's buffer
+  // with stage s+NS, reads stage s+1's first fragments, then its weight slice.
+  int bi = 0;                                   // stage buffer of stage s (= s mod NS)
+  for (int s0 = 0; s0 < nst; s0 += UNROLL) {
+#pragma unroll
+    for (int d = 0; d < UNROLL; ++d) {
+      const int s = s0 + d;
+      if (s >= nst) break;
+      const int bn = bi + 1 == NS ? 0 : bi + 1;   // stage buffer of stage s + 1
+#pragma unroll
+      for (int q = 0; q < kNStep; ++q) {
+        const int slot = (d * kNStep + q) % kRingW;
+        if (q + 1 < kNStep) {
+          load_b(bq[(q + 1) & 1], bi, q + 1);
+        } else {
+          // this wave's share of stage s + 1 has landed and its reads of stage s are done; after
+          // the barrier every wave's are, so stage s + 1 is complete and stage s's buffer is free
+          __builtin_amdgcn_s_waitcnt(waitcnt_imm(kWaitStage, 0));
+          asm volatile("s_barrier" ::: "memory");
+          load_stage(bi, s + NS);
+          load_b(bq[0], bn, 0);
+        }
+        load_w(ring[(slot + kRingW - 1) % kRingW], s + (q + kRingW - 1) / kNStep, (q + kRingW - 1) % kNStep);
+        lgkm_wait<FT>();                        // this k-step's fragments (the next k-step's may be in flight)
+        wait_w(q);                              // this k-step's weight slice
+        pin(bq[q & 1]);
+        pin_acc(ring[slot]);
+        mma(ring[slot], bq[q & 1]);
+        // keep every load in the k-step it was written in: the prefetch distances are the design
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      bi = bn;
+    }
+  }
+  // no stage load may still be writing LDS when the tile is reused below
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+}
+
 // BM_: tokens per workgroup (the configuration's own, or half of it when that fills the chip better)
 template <bool BF16, int EPAD, int BM_>
 __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
@@ -201,23 +448,19 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   constexpr int WE = Cfg::WE, WT = Cfg::WT, BM = BM_;
   constexpr int EW = EPAD / WE, TW = BM / WT;
   constexpr int FE = EW / 32, FT = TW / 32;
-  constexpr int RPW = BM / kProducers;           // hidden rows per producer wave
-  constexpr int LPR = kStageRowBytes / 16;       // lanes per row of a stage (16 bytes each)
-  constexpr int RPI = 64 / LPR;                  // rows per load instruction
-  constexpr int LPW = RPW / RPI;                 // loads per producer per stage
-  constexpr int XSTAGE = BM * kPitch;
-  constexpr int SB = EPAD * kStageRowBytes;      // packed weight bytes per stage
+  constexpr int NS = ring_stages(BM);
+  constexpr int STAGE = BM * kStageRowBytes;     // LDS bytes of one hidden stage
   constexpr int SROW = EPAD + 4;                 // score-tile row stride in floats
   constexpr int SCORE_BYTES = BM * SROW * 4;
-  constexpr int SMEM = (2 * XSTAGE > SCORE_BYTES) ? 2 * XSTAGE : SCORE_BYTES;
+  constexpr int SMEM = (NS * STAGE > SCORE_BYTES) ? NS * STAGE : SCORE_BYTES;
   constexpr int LPT = EPAD / 32;                 // lanes per token in the selection phase
   constexpr int TPP = kThreads / LPT;            // tokens per selection pass
   constexpr int NPASS = (BM + TPP - 1) / TPP;
   constexpr int GSC_TOK = TPP < BM ? TPP : BM;
-  static_assert(LPW >= 1 && RPW % RPI == 0, "producers split the tile in whole load instructions");
-  static_assert(WE * WT == kWaves - kProducers, "one consumer per SIMD");
+  static_assert(WE * WT == kWaves, "every wave owns one tile slice");
   static_assert(EW % 32 == 0 && TW % 32 == 0, "wave tiles are whole 32 x 32 MFMA blocks");
-  static_assert(TPP % 64 == 0, "selection passes cover whole waves");
+  static_assert(BM % TPP == 0 || (TPP > BM && BM % (64 / LPT) == 0),
+                "every selection pass covers whole waves");
 
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   __shared__ int32_t hist[EPAD];
@@ -233,10 +476,8 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   // wave-uniform by construction; readfirstlane keeps it (and every buffer-load offset derived
   // from it) in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool consumer = wave >= kProducers;
-  const int cw = consumer ? wave - kProducers : 0;
-  const int we = cw % WE;
-  const int wt = cw / WE;
+  const int we = wave % WE;
+  const int wt = wave / WE;
   const int64_t row0 = (int64_t)blockIdx.x * BM;
   const int E = p.E;
 
@@ -255,130 +496,14 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  // Both roles run exactly NP stages with one barrier each (NP: nstages rounded up to a multiple
-  // of both loops' unroll factors).  Stages past the end load out of range, i.e. zeros.
-  const int nst = p.nstages;
-  const int NP = (nst + kStageUnroll - 1) / kStageUnroll * kStageUnroll;
-#if FB_STAGE_ROTATE
-  // Workgroups on one XCD (blockIdx = x mod 8) start the k-loop at different stages, so the
-  // router-weight stages they read at any moment are spread over the L2 channels.
-  const int rot = nst > 0 ? (int)(((blockIdx.x >> 3) * 5u) % (unsigned)nst) : 0;
-#else
-  const int rot = 0;
-#endif
-  auto phys = [&](int st) { const int v = st + rot; return v >= nst ? v - nst : v; };
-  if (row0 < p.T) {
-    if (!consumer) {
-      // ---- producers: hidden rows, HBM -> registers -> LDS ----------------------------------
-      const int64_t rows = (p.T - row0) < BM ? (p.T - row0) : BM;
-      const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-          (void*)(p.x + row0 * (int64_t)p.ldx_bytes), (short)0, (int)(rows * p.ldx_bytes), kRsrcWord3);
-      const int col = (lane % LPR) * 16;         // byte within the stage segment of a row
-      uint32_t xoff[LPW], loff[LPW];
-#pragma unroll
-      for (int i = 0; i < LPW; ++i) {
-        const int r = wave * RPW + i * RPI + lane / LPR;
-        xoff[i] = (uint32_t)(r * p.ldx_bytes + col);
-        loff[i] = (uint32_t)(r * kPitch + col);
-      }
-      u32x4 xa[kDX][LPW];
-      // bytes at or past H (tail of a half-width last stage, padded stages) are not fetched
-      auto load_x = [&](u32x4(&dst)[LPW], int st) {
-        const bool stage_ok = st < nst;
-        const int ps = phys(st);
-        const bool ok = stage_ok && ps * kStageRowBytes + col < p.Hbytes;
-#pragma unroll
-        for (int i = 0; i < LPW; ++i)
-          dst[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, ok ? xoff[i] : kOobOffset,
-                                                         stage_ok ? ps * kStageRowBytes : 0, 2);
-      };
-#pragma unroll
-      for (int d = 0; d < kDX; ++d) load_x(xa[d], d);
-      for (int st0 = 0; st0 < NP; st0 += kDX) {
-#pragma unroll
-        for (int d = 0; d < kDX; ++d) {
-          const int st = st0 + d;
-          char* buf = smem + (st & 1) * XSTAGE;
-#pragma unroll
-          for (int i = 0; i < LPW; ++i) *reinterpret_cast<u32x4*>(buf + loff[i]) = xa[d][i];
-          load_x(xa[d], st + kDX);
-          __builtin_amdgcn_sched_barrier(0);
-          lds_barrier();                         // stage st is in LDS
-        }
-      }
-    } else {
-      // ---- consumers: packed router weight L2 -> registers, hidden fragments from LDS --------
-      // Weight fragments live in a ring of kRing k-step slices (global k-step g in slot g % kRing);
-      // each k-step refills the slot the previous one consumed with the slice kRing - 1 k-steps
-      // ahead, so weight loads lead the MFMAs by kRing - 1 k-steps.
-      const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
-          (void*)p.wpack, (short)0, nst * SB, kRsrcWord3);
-      const uint32_t wbase = (uint32_t)(we * kNStep * FE * 1024 + lane * 16);
-      const uint32_t boff = (uint32_t)((wt * TW + (lane & 31)) * kPitch + (lane >> 5) * 16);
-      u32x4 ring[kRing][FE];
-      auto load_slice = [&](u32x4(&dst)[FE], int st, int q) {
-        const bool ok = st < nst;
-#pragma unroll
-        for (int fe = 0; fe < FE; ++fe)
-          dst[fe] = __builtin_amdgcn_raw_buffer_load_b128(
-              wr, ok ? wbase + (uint32_t)((q * FE + fe) * 1024) : kOobOffset, ok ? phys(st) * SB : 0, 0);
-      };
-#pragma unroll
-      for (int g = 0; g < kRing - 1; ++g) load_slice(ring[g], g / kNStep, g % kNStep);
-      for (int st0 = 0; st0 < NP; st0 += 2) {
-#pragma unroll
-        for (int d = 0; d < 2; ++d) {
-          const int st = st0 + d;
-          lds_barrier();                         // stage st is in LDS
-          const char* buf = smem + (st & 1) * XSTAGE;
-          // hidden fragments one k-step ahead, so only the first read of a stage waits on LDS
-          u32x4 bq[2][FT];
-#pragma unroll
-          for (int ft = 0; ft < FT; ++ft)
-            bq[0][ft] = *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + boff);
-#pragma unroll
-          for (int q = 0; q < kNStep; ++q) {
-            if (q + 1 < kNStep) {
-#pragma unroll
-              for (int ft = 0; ft < FT; ++ft)
-                bq[(q + 1) & 1][ft] =
-                    *reinterpret_cast<const u32x4*>(buf + ft * 32 * kPitch + (q + 1) * kStepBytes + boff);
-            }
-            const int slot = (kNStep * d + q) % kRing;             // compile-time after unrolling
-            load_slice(ring[(slot + kRing - 1) % kRing], st + (q + kRing - 1) / kNStep,
-                       (q + kRing - 1) % kNStep);
-            const u32x4* bfr = bq[q & 1];
-#pragma unroll
-            for (int ft = 0; ft < FT; ++ft) {
-#pragma unroll
-              for (int fe = 0; fe < FE; ++fe) {
-                if constexpr (BF16) {
-                  acc[fe][ft] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                      __builtin_bit_cast(bf16x8, ring[slot][fe]), __builtin_bit_cast(bf16x8, bfr[ft]),
-                      acc[fe][ft], 0, 0, 0);
-                } else {
-                  // four k-pairs per fragment; A and B take the same k for every lane
-                  const f32x4 av = __builtin_bit_cast(f32x4, ring[slot][fe]);
-                  const f32x4 bv = __builtin_bit_cast(f32x4, bfr[ft]);
-#pragma unroll
-                  for (int j = 0; j < 4; ++j)
-                    acc[fe][ft] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[j], bv[j], acc[fe][ft], 0, 0, 0);
-                }
-              }
-            }
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        }
-      }
-    }
-  }
+  if (row0 < p.T) contract<BF16, EPAD, FE, FT, NS, BM, TW>(acc, p, row0, wave, we, wt, lane, smem);
   lds_barrier();
 
-  // ---- consumers: logits and scores into an LDS tile S[token][expert] ------------------------
+  // ---- logits and scores into an LDS tile S[token][expert] ------------------------
   // Lane l of a 32 x 32 block holds token (l & 31) and experts g * 8 + (l >> 5) * 4 + r in
   // register g * 4 + r.
   float* S = reinterpret_cast<float*>(smem);
-  if (consumer && row0 < p.T) {
+  if (row0 < p.T) {
     if (p.logits) {                              // debug output of the early logits
 #pragma unroll
       for (int fe = 0; fe < FE; ++fe)
@@ -433,25 +558,36 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   const int gshift = __builtin_ctz((unsigned)gsz);   // group sizes below 32 are powers of two
   auto local_of = [&](int i) { return ((((i >> 2) + jl) & 7) << 2) | (i & 3); };  // expert - 32 jl
   const int idx_base = 255 - jl * 32;        // key index bits of element i: idx_base - local_of(i)
+  auto read_scores = [&](float(&dst)[32], int tlr) {
+    const float* row = S + tlr * SROW + jl * 32;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(row + ((q + jl) & 7) * 4);
+      dst[q * 4 + 0] = v[0]; dst[q * 4 + 1] = v[1]; dst[q * 4 + 2] = v[2]; dst[q * 4 + 3] = v[3];
+    }
+  };
+  // each pass's scores are read while the previous pass is processed (one wave per SIMD: nothing
+  // else hides the LDS latency)
+  float snext[32];
+  if (gslot < BM) read_scores(snext, gslot);
 #pragma unroll 1
   for (int pass = 0; pass < NPASS; ++pass) {
     const int tl = pass * TPP + gslot;
-    if (tl >= BM) continue;                    // whole waves (TPP is a multiple of 64)
+    if (tl >= BM) continue;                    // whole waves (checked above)
     const int64_t t = row0 + tl;
     const bool tvalid = t < p.T;
 
     float s[32];
-    const float* srow = S + tl * SROW + jl * 32;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(srow + ((q + jl) & 7) * 4);
-      s[q * 4 + 0] = v[0]; s[q * 4 + 1] = v[1]; s[q * 4 + 2] = v[2]; s[q * 4 + 3] = v[3];
-    }
+    for (int i = 0; i < 32; ++i) s[i] = snext[i];
+    if (tl + TPP < BM) read_scores(snext, tl + TPP);
     uint32_t keep = 0xFFFFFFFFu;               // bit i: element i survives the group limit
     if (ng > 1) {
       float* gs = gsc[gslot];
       // group scores: sum of the group's group_topn best scores, largest first
       if (gsz >= 32) {
+        // whole lanes per group: group scores and ranks stay in registers (lane exchanges inside
+        // the token's LPT lanes); see the else branch for groups smaller than a lane's slice
         const int lpg = gsz >> 5;
         float m1 = -__builtin_inff(), m2 = -__builtin_inff();
 #pragma unroll
@@ -460,7 +596,10 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
           m1 = fmaxf(m1, s[i]);
         }
         top2_group(m1, m2, lpg);
-        if ((jl & (lpg - 1)) == 0 && jl * 32 < E) gs[(jl * 32) >> gshift] = p.group_topn == 2 ? m1 + m2 : m1;
+        const bool real = jl * 32 < E;
+        const float g = p.group_topn == 2 ? m1 + m2 : m1;
+        const int rank = group_rank<LPT>(g, jl, lpg, E);
+        keep = (real && rank < p.topk_group) ? 0xFFFFFFFFu : 0u;
       } else {
         const int gpl = 32 >> gshift;
         for (int u = 0; u < gpl; ++u) {
@@ -474,26 +613,24 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
           if (jl * 32 + u * gsz < E) gs[jl * gpl + u] = p.group_topn == 2 ? m1 + m2 : m1;
         }
       }
-      wave_lds_sync();
-      // rank of a group among all groups (score desc, lower index first), four scores per read
-      // (rows hold kMaxGroups entries, so the reads stay in bounds)
-      auto kept = [&](int g) -> bool {
-        const float mine = gs[g];
-        int rank = 0;
+      if (gsz < 32) {
+        wave_lds_sync();
+        // rank of a group among all groups (score desc, lower index first), four scores per read
+        // (rows hold kMaxGroups entries, so the reads stay in bounds)
+        auto kept = [&](int g) -> bool {
+          const float mine = gs[g];
+          int rank = 0;
 #pragma unroll 1
-        for (int h4 = 0; h4 < ng; h4 += 4) {
-          const f32x4 o = *reinterpret_cast<const f32x4*>(gs + h4);
+          for (int h4 = 0; h4 < ng; h4 += 4) {
+            const f32x4 o = *reinterpret_cast<const f32x4*>(gs + h4);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int h = h4 + j;
-            rank += (h < ng) & ((o[j] > mine) | ((o[j] == mine) & (h < g)));
+            for (int j = 0; j < 4; ++j) {
+              const int h = h4 + j;
+              rank += (h < ng) & ((o[j] > mine) | ((o[j] == mine) & (h < g)));
+            }
           }
-        }
-        return rank < p.topk_group;
-      };
-      if (gsz >= 32) {
-        keep = (jl * 32 < E && kept((jl * 32) >> gshift)) ? 0xFFFFFFFFu : 0u;
-      } else {
+          return rank < p.topk_group;
+        };
         keep = 0;
         const int gpl = 32 >> gshift;
         for (int u = 0; u < gpl; ++u) {
@@ -504,7 +641,6 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
         }
       }
     }
-
     // 32-bit keys: the top 24 bits of the order-preserving score encoding, then 255 - expert.
     // Experts outside the kept groups (and every expert of a token past T) keep only their index
     // bits, which ranks them below every selectable expert; padding experts score -inf.
@@ -555,18 +691,26 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
         for (int i = 0; i < 32; ++i) insert(key[i] < last ? key[i] : 0u);
       }
     }
-    const bool tie = tvalid && (next >> 8) != 0 && (next >> 8) == (kth >> 8);
+    const uint32_t tb = kth >> 8;              // score bits of the k-th key
+    const bool tie = tvalid && (next >> 8) != 0 && (next >> 8) == tb;
     if (tie) {
-      // exact path: 64-bit keys (full order-preserving score bits, then the inverted index)
+      // Exact path for the boundary only.  Every key whose score bits exceed tb is selected and
+      // already in place (the keys were popped in descending order); the remaining slots go to the
+      // experts whose score bits equal tb, ranked by the full 64-bit key (all score bits, then the
+      // inverted index), which is the exact order.
+      int above = 0;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) above += (key[i] >> 8) > tb;
+#pragma unroll
+      for (int off = 1; off < LPT; off <<= 1) above += __shfl_xor(above, off, LPT);
       uint64_t lastk = ~0ull;
-      for (int r = 0; r < k; ++r) {
+      for (int r = above; r < k; ++r) {
         uint64_t best = 0;
 #pragma unroll
         for (int i = 0; i < 32; ++i) {
-          const int e = jl * 32 + local_of(i);
-          const float se = srow[local_of(i)];     // re-read: the scores are not kept in registers
-          const uint64_t kk = ((uint64_t)ord_bits(se + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)e);
-          const bool ok = (key[i] >> 8) != 0 && kk < lastk && kk > best;   // selectable only
+          const uint32_t e = (uint32_t)(jl * 32 + local_of(i));
+          const uint64_t kk = ((uint64_t)ord_bits(s[i] + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - e);
+          const bool ok = (key[i] >> 8) == tb && kk < lastk && kk > best;
           best = ok ? kk : best;
         }
 #pragma unroll
@@ -574,7 +718,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
           const uint64_t o = __shfl_xor(best, off, LPT);
           best = o > best ? o : best;
         }
-        if (best == 0) break;                  // cannot happen with >= k selectable experts
+        if (best == 0) break;                  // cannot happen: at least two keys share tb
         lastk = best;
         if (jl == 0) sel[tl][r] = (int)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFu));
       }
