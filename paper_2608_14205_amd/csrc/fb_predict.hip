@@ -151,8 +151,13 @@ constexpr int waitcnt_imm(int vm, int lgkm) {
 
 // Order-preserving map of float bits to unsigned (for finite values; -0 is canonicalised first).
 __device__ __forceinline__ uint32_t ord_bits(float s) {
-  uint32_t u = __float_as_uint(s);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  const uint32_t u = __float_as_uint(s);
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+}
+
+// Inverse of ord_bits.
+__device__ __forceinline__ float from_ord_bits(uint32_t o) {
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
 }
 
 // Median of three (v_med3_u32): the middle value, used to maintain a sorted top-3.
@@ -454,19 +459,23 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   constexpr int SCORE_BYTES = BM * SROW * 4;
   constexpr int SMEM = (NS * STAGE > SCORE_BYTES) ? NS * STAGE : SCORE_BYTES;
   constexpr int LPT = EPAD / 32;                 // lanes per token in the selection phase
-  constexpr int TPP = kThreads / LPT;            // tokens per selection pass
-  constexpr int NPASS = (BM + TPP - 1) / TPP;
-  constexpr int GSC_TOK = TPP < BM ? TPP : BM;
+  constexpr int TPP = kThreads / LPT;            // token slots (lane groups) of the workgroup
+  // tokens a lane group works on at once: 1 (interleaving two ran slower on MI355X)
+  constexpr int NT = 1;
+  constexpr int TPASS = TPP * NT;                // tokens per selection pass
+  constexpr int NPASS = (BM + TPASS - 1) / TPASS;
+  constexpr int GSC_TOK = TPASS < BM ? TPASS : BM;
   static_assert(WE * WT == kWaves, "every wave owns one tile slice");
   static_assert(EW % 32 == 0 && TW % 32 == 0, "wave tiles are whole 32 x 32 MFMA blocks");
-  static_assert(BM % TPP == 0 || (TPP > BM && BM % (64 / LPT) == 0),
+  static_assert(BM % TPASS == 0 || (TPASS > BM && NT == 1 && BM % (64 / LPT) == 0),
                 "every selection pass covers whole waves");
 
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   __shared__ int32_t hist[EPAD];
   __shared__ __attribute__((aligned(16))) float s_lbias[EPAD];   // router bias (-inf past E)
   __shared__ __attribute__((aligned(16))) float s_sbias[EPAD];   // selection bias (-inf past E)
-  __shared__ int32_t sel[BM][kMaxK + 1];
+  // selected experts per token (ids < 256), with spare slots kMaxK .. kMaxK + LPT - 1
+  __shared__ int16_t sel[BM][kMaxK + LPT];
   __shared__ __attribute__((aligned(16))) float gsc[GSC_TOK][kMaxGroups];
   __shared__ int32_t s_flag;
   __shared__ int64_t s_red[kWaves][2];
@@ -549,7 +558,9 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   // ---- selection: LPT lanes per token, 32 contiguous experts per lane ------------------------
   // Lane jl reads its eight 4-expert chunks starting at chunk jl, which keeps the 16 lanes of a
   // DPP row (two tokens) on distinct LDS banks; element 4q + j of the lane is expert
-  // 32 jl + 4 ((q + jl) mod 8) + j.  Tokens past T take part with no selectable expert.
+  // 32 jl + 4 ((q + jl) mod 8) + j.  Tokens past T take part with no selectable expert.  With one
+  // wave per SIMD nothing hides latency between waves, so each lane group works on NT tokens at
+  // once as independent instruction chains.
   const int k = p.k;
   const int jl = tid % LPT;      // lane within the token group
   const int gslot = tid / LPT;   // token slot within a pass
@@ -566,77 +577,103 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       dst[q * 4 + 0] = v[0]; dst[q * 4 + 1] = v[1]; dst[q * 4 + 2] = v[2]; dst[q * 4 + 3] = v[3];
     }
   };
-  // each pass's scores are read while the previous pass is processed (one wave per SIMD: nothing
-  // else hides the LDS latency)
-  float snext[32];
-  if (gslot < BM) read_scores(snext, gslot);
+  uint32_t idxb[32];                         // key index bits of each element
+#pragma unroll
+  for (int i = 0; i < 32; ++i) idxb[i] = (uint32_t)(idx_base - local_of(i));
+  // each pass's scores are read while the previous pass is processed
+  float snext[NT][32];
+#pragma unroll
+  for (int u = 0; u < NT; ++u)
+    if (u * TPP + gslot < BM) read_scores(snext[u], u * TPP + gslot);
 #pragma unroll 1
   for (int pass = 0; pass < NPASS; ++pass) {
-    const int tl = pass * TPP + gslot;
-    if (tl >= BM) continue;                    // whole waves (checked above)
-    const int64_t t = row0 + tl;
-    const bool tvalid = t < p.T;
-
-    float s[32];
+    if (pass * TPASS + gslot >= BM) continue;  // whole waves (checked above)
+    int tl[NT];
+    int64_t tt[NT];
+    bool tvalid[NT];
+    float s[NT][32];
 #pragma unroll
-    for (int i = 0; i < 32; ++i) s[i] = snext[i];
-    if (tl + TPP < BM) read_scores(snext, tl + TPP);
-    uint32_t keep = 0xFFFFFFFFu;               // bit i: element i survives the group limit
+    for (int u = 0; u < NT; ++u) {
+      tl[u] = pass * TPASS + u * TPP + gslot;
+      tt[u] = row0 + tl[u];
+      tvalid[u] = tt[u] < p.T;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) s[u][i] = snext[u][i];
+      if (tl[u] + TPASS < BM) read_scores(snext[u], tl[u] + TPASS);
+    }
+    uint32_t ob[NT][32];                       // order-preserving bits of the scores
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+      for (int i = 0; i < 32; ++i) ob[u][i] = ord_bits(s[u][i]);
+    uint32_t keep[NT];                         // bit i: element i survives the group limit
+#pragma unroll
+    for (int u = 0; u < NT; ++u) keep[u] = 0xFFFFFFFFu;
     if (ng > 1) {
-      float* gs = gsc[gslot];
       // group scores: sum of the group's group_topn best scores, largest first
       if (gsz >= 32) {
         // whole lanes per group: group scores and ranks stay in registers (lane exchanges inside
-        // the token's LPT lanes); see the else branch for groups smaller than a lane's slice
+        // the token's LPT lanes); the else branch handles groups smaller than a lane's slice
         const int lpg = gsz >> 5;
-        float m1 = -__builtin_inff(), m2 = -__builtin_inff();
-#pragma unroll
-        for (int i = 0; i < 32; ++i) {
-          m2 = __builtin_amdgcn_fmed3f(m1, m2, s[i]);
-          m1 = fmaxf(m1, s[i]);
-        }
-        top2_group(m1, m2, lpg);
         const bool real = jl * 32 < E;
-        const float g = p.group_topn == 2 ? m1 + m2 : m1;
-        const int rank = group_rank<LPT>(g, jl, lpg, E);
-        keep = (real && rank < p.topk_group) ? 0xFFFFFFFFu : 0u;
-      } else {
-        const int gpl = 32 >> gshift;
-        for (int u = 0; u < gpl; ++u) {
-          float m1 = -__builtin_inff(), m2 = -__builtin_inff();
+#pragma unroll
+        for (int u = 0; u < NT; ++u) {
+          // top two of the lane's scores, compared as order-preserving integers (no NaN handling
+          // needed: scores are finite or -inf), then merged over the group's lanes
+          uint32_t k1 = 0, k2 = 0;
 #pragma unroll
           for (int i = 0; i < 32; ++i) {
-            const bool in = (local_of(i) >> gshift) == u;
-            m2 = in ? __builtin_amdgcn_fmed3f(m1, m2, s[i]) : m2;
-            m1 = in ? fmaxf(m1, s[i]) : m1;
+            k2 = umed3(k1, k2, ob[u][i]);
+            k1 = max(k1, ob[u][i]);
           }
-          if (jl * 32 + u * gsz < E) gs[jl * gpl + u] = p.group_topn == 2 ? m1 + m2 : m1;
+          float m1 = from_ord_bits(k1), m2 = from_ord_bits(k2);
+          if (lpg > 1) top2_group(m1, m2, lpg);
+          const float g = p.group_topn == 2 ? m1 + m2 : m1;
+          const int rank = group_rank<LPT>(g, jl, lpg, E);
+          keep[u] = (real && rank < p.topk_group) ? 0xFFFFFFFFu : 0u;
         }
-      }
-      if (gsz < 32) {
-        wave_lds_sync();
-        // rank of a group among all groups (score desc, lower index first), four scores per read
-        // (rows hold kMaxGroups entries, so the reads stay in bounds)
-        auto kept = [&](int g) -> bool {
-          const float mine = gs[g];
-          int rank = 0;
-#pragma unroll 1
-          for (int h4 = 0; h4 < ng; h4 += 4) {
-            const f32x4 o = *reinterpret_cast<const f32x4*>(gs + h4);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int h = h4 + j;
-              rank += (h < ng) & ((o[j] > mine) | ((o[j] == mine) & (h < g)));
-            }
-          }
-          return rank < p.topk_group;
-        };
-        keep = 0;
+      } else {
         const int gpl = 32 >> gshift;
-        for (int u = 0; u < gpl; ++u) {
-          if (jl * 32 + u * gsz < E && kept(jl * gpl + u)) {
 #pragma unroll
-            for (int i = 0; i < 32; ++i) keep |= (uint32_t)((local_of(i) >> gshift) == u) << i;
+        for (int u = 0; u < NT; ++u) {
+          float* gs = gsc[u * TPP + gslot];
+          for (int v = 0; v < gpl; ++v) {
+            float m1 = -__builtin_inff(), m2 = -__builtin_inff();
+#pragma unroll
+            for (int i = 0; i < 32; ++i) {
+              const bool in = (local_of(i) >> gshift) == v;
+              m2 = in ? __builtin_amdgcn_fmed3f(m1, m2, s[u][i]) : m2;
+              m1 = in ? fmaxf(m1, s[u][i]) : m1;
+            }
+            if (jl * 32 + v * gsz < E) gs[jl * gpl + v] = p.group_topn == 2 ? m1 + m2 : m1;
+          }
+        }
+        wave_lds_sync();
+#pragma unroll
+        for (int u = 0; u < NT; ++u) {
+          const float* gs = gsc[u * TPP + gslot];
+          // rank of a group among all groups (score desc, lower index first), four scores per read
+          // (rows hold kMaxGroups entries, so the reads stay in bounds)
+          auto kept = [&](int g) -> bool {
+            const float mine = gs[g];
+            int rank = 0;
+#pragma unroll 1
+            for (int h4 = 0; h4 < ng; h4 += 4) {
+              const f32x4 o = *reinterpret_cast<const f32x4*>(gs + h4);
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const int h = h4 + j;
+                rank += (h < ng) & ((o[j] > mine) | ((o[j] == mine) & (h < g)));
+              }
+            }
+            return rank < p.topk_group;
+          };
+          keep[u] = 0;
+          for (int v = 0; v < gpl; ++v) {
+            if (jl * 32 + v * gsz < E && kept(jl * gpl + v)) {
+#pragma unroll
+              for (int i = 0; i < 32; ++i) keep[u] |= (uint32_t)((local_of(i) >> gshift) == v) << i;
+            }
           }
         }
       }
@@ -644,109 +681,132 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     // 32-bit keys: the top 24 bits of the order-preserving score encoding, then 255 - expert.
     // Experts outside the kept groups (and every expert of a token past T) keep only their index
     // bits, which ranks them below every selectable expert; padding experts score -inf.
-    uint32_t key[32];
-    if (ng == 1 || gsz >= 32) {                // the lane's experts are kept or dropped together
-      const uint32_t m = tvalid && keep ? 0xFFFFFF00u : 0u;
+    uint32_t key[NT][32];
 #pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        const uint32_t u = __float_as_uint(s[i]);
-        key[i] = ((u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u)) & m) | (uint32_t)(idx_base - local_of(i));
-      }
-    } else {
+    for (int u = 0; u < NT; ++u) {
+      if (ng == 1 || gsz >= 32) {              // the lane's experts are kept or dropped together
+        const uint32_t m = tvalid[u] && keep[u] ? 0xFFFFFF00u : 0u;
 #pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        const uint32_t u = __float_as_uint(s[i]);
-        const uint32_t m = tvalid && ((keep >> i) & 1u) ? 0xFFFFFF00u : 0u;
-        key[i] = ((u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u)) & m) | (uint32_t)(idx_base - local_of(i));
+        for (int i = 0; i < 32; ++i) key[u][i] = (ob[u][i] & m) | idxb[i];
+      } else {
+#pragma unroll
+        for (int i = 0; i < 32; ++i) {
+          const uint32_t m = tvalid[u] && ((keep[u] >> i) & 1u) ? 0xFFFFFF00u : 0u;
+          key[u][i] = (ob[u][i] & m) | idxb[i];
+        }
       }
     }
     // per-lane cache of the kCache largest keys (descending), refilled by a rescan below the last
     // popped key when it runs dry
-    uint32_t c[kCache];
+    uint32_t c[NT][kCache];
 #pragma unroll
-    for (int d = 0; d < kCache; ++d) c[d] = 0;
-    auto insert = [&](uint32_t v) {
+    for (int u = 0; u < NT; ++u)
 #pragma unroll
-      for (int d = kCache - 1; d >= 1; --d) c[d] = umed3(c[d - 1], c[d], v);
-      c[0] = max(c[0], v);
+      for (int d = 0; d < kCache; ++d) c[u][d] = 0;
+    auto insert = [&](int u, uint32_t v) {
+#pragma unroll
+      for (int d = kCache - 1; d >= 1; --d) c[u][d] = umed3(c[u][d - 1], c[u][d], v);
+      c[u][0] = max(c[u][0], v);
     };
 #pragma unroll
-    for (int i = 0; i < 32; ++i) insert(key[i]);
-    int npop = 0;
-    uint32_t last = 0xFFFFFFFFu, kth = 0, next = 0;
+    for (int i = 0; i < 32; ++i)
+#pragma unroll
+      for (int u = 0; u < NT; ++u) insert(u, key[u][i]);
+    uint32_t last[NT], kth[NT], next[NT];
+#pragma unroll
+    for (int u = 0; u < NT; ++u) { last[u] = 0xFFFFFFFFu; kth[u] = 0; next[u] = 0; }
+    // Rounds are branch-free per lane: the popping lane records the expert in slot r, every other
+    // lane writes its own spare slot past kMaxK; a refill runs only when some lane of the wave ran
+    // dry, and lanes that did not insert zeros (which leave a sorted cache unchanged).
     for (int r = 0; r <= k; ++r) {
-      const uint32_t h = c[0];
-      const uint32_t m = group_max_u32<LPT>(h);
-      if (r == k - 1) kth = m;
-      if (r == k) next = m;
-      const bool mine = m != 0 && h == m;
-      if (mine && r < k) sel[tl][r] = 255 - (int)(m & 0xFFu);
+      bool dry[NT];
 #pragma unroll
-      for (int d = 0; d < kCache - 1; ++d) c[d] = mine ? c[d + 1] : c[d];
-      c[kCache - 1] = mine ? 0u : c[kCache - 1];
-      npop += mine;
-      last = mine ? m : last;
-      if (mine && c[0] == 0 && npop < 32) {    // this lane's cache ran dry: rescan below `last`
+      for (int u = 0; u < NT; ++u) {
+        const uint32_t h = c[u][0];
+        const uint32_t m = group_max_u32<LPT>(h);
+        if (r >= k - 1) {                      // uniform
+          kth[u] = r == k - 1 ? m : kth[u];
+          next[u] = m;
+        }
+        const bool mine = m != 0 && h == m;
+        sel[tl[u]][mine && r < k ? r : kMaxK + jl] = (int16_t)(255 - (int)(m & 0xFFu));
 #pragma unroll
-        for (int i = 0; i < 32; ++i) insert(key[i] < last ? key[i] : 0u);
+        for (int d = 0; d < kCache - 1; ++d) c[u][d] = mine ? c[u][d + 1] : c[u][d];
+        c[u][kCache - 1] = mine ? 0u : c[u][kCache - 1];
+        last[u] = mine ? m : last[u];
+        // refill below last[u]; a lane with nothing left below it inserts only zeros
+        dry[u] = mine && c[u][0] == 0;
+      }
+#pragma unroll
+      for (int u = 0; u < NT; ++u) {           // each token refills on its own (rare)
+        if (__builtin_amdgcn_ballot_w64(dry[u]) != 0) {
+#pragma unroll
+          for (int i = 0; i < 32; ++i) insert(u, dry[u] && key[u][i] < last[u] ? key[u][i] : 0u);
+        }
       }
     }
-    const uint32_t tb = kth >> 8;              // score bits of the k-th key
-    const bool tie = tvalid && (next >> 8) != 0 && (next >> 8) == tb;
-    if (tie) {
-      // Exact path for the boundary only.  Every key whose score bits exceed tb is selected and
-      // already in place (the keys were popped in descending order); the remaining slots go to the
-      // experts whose score bits equal tb, ranked by the full 64-bit key (all score bits, then the
-      // inverted index), which is the exact order.
-      int above = 0;
 #pragma unroll
-      for (int i = 0; i < 32; ++i) above += (key[i] >> 8) > tb;
+    for (int u = 0; u < NT; ++u) {
+      const uint32_t tb = kth[u] >> 8;         // score bits of the k-th key
+      const bool tie = tvalid[u] && (next[u] >> 8) != 0 && (next[u] >> 8) == tb;
+      if (tie) {
+        // Exact path for the boundary only.  Every key whose score bits exceed tb is selected and
+        // already in place (the keys were popped in descending order); the remaining slots go to
+        // the experts whose score bits equal tb, ranked by the full 64-bit key (all score bits,
+        // then the inverted index), which is the exact order.
+        int above = 0;
 #pragma unroll
-      for (int off = 1; off < LPT; off <<= 1) above += __shfl_xor(above, off, LPT);
-      uint64_t lastk = ~0ull;
-      for (int r = above; r < k; ++r) {
-        uint64_t best = 0;
+        for (int i = 0; i < 32; ++i) above += (key[u][i] >> 8) > tb;
 #pragma unroll
-        for (int i = 0; i < 32; ++i) {
-          const uint32_t e = (uint32_t)(jl * 32 + local_of(i));
-          const uint64_t kk = ((uint64_t)ord_bits(s[i] + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - e);
-          const bool ok = (key[i] >> 8) == tb && kk < lastk && kk > best;
-          best = ok ? kk : best;
+        for (int off = 1; off < LPT; off <<= 1) above += __shfl_xor(above, off, LPT);
+        uint64_t lastk = ~0ull;
+        for (int r = above; r < k; ++r) {
+          uint64_t best = 0;
+#pragma unroll
+          for (int i = 0; i < 32; ++i) {
+            const uint32_t e = (uint32_t)(jl * 32 + local_of(i));
+            const uint64_t kk = ((uint64_t)ord_bits(s[u][i] + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - e);
+            const bool ok = (key[u][i] >> 8) == tb && kk < lastk && kk > best;
+            best = ok ? kk : best;
+          }
+#pragma unroll
+          for (int off = 1; off < LPT; off <<= 1) {
+            const uint64_t o = __shfl_xor(best, off, LPT);
+            best = o > best ? o : best;
+          }
+          if (best == 0) break;                // cannot happen: at least two keys share tb
+          lastk = best;
+          if (jl == 0) sel[tl[u]][r] = (int16_t)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFu));
         }
-#pragma unroll
-        for (int off = 1; off < LPT; off <<= 1) {
-          const uint64_t o = __shfl_xor(best, off, LPT);
-          best = o > best ? o : best;
-        }
-        if (best == 0) break;                  // cannot happen: at least two keys share tb
-        lastk = best;
-        if (jl == 0) sel[tl][r] = (int)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFu));
       }
     }
     wave_lds_sync();
-    if (tvalid) {
-      for (int r = jl; r < k; r += LPT) {
-        const int e = sel[tl][r];
-        if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
-      }
-    }
-    if (p.topk_idx && jl == 0 && tvalid) {
-      // debug output in exact descending score order: insertion sort of the k selected in place
-      int* list = sel[tl];
-      for (int r = 1; r < k; ++r) {
-        const int e = list[r];
-        const float se = (unsigned)e < (unsigned)E ? S[tl * SROW + e] : -__builtin_inff();
-        int q = r;
-        while (q > 0) {
-          const int eo = list[q - 1];
-          const float so = (unsigned)eo < (unsigned)E ? S[tl * SROW + eo] : -__builtin_inff();
-          if (so > se || (so == se && eo < e)) break;
-          list[q] = eo;
-          --q;
+#pragma unroll
+    for (int u = 0; u < NT; ++u) {
+      if (tvalid[u]) {
+        for (int r = jl; r < k; r += LPT) {
+          const int e = sel[tl[u]][r];
+          if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
         }
-        list[q] = e;
       }
-      for (int r = 0; r < k; ++r) p.topk_idx[t * k + r] = list[r];
+      if (p.topk_idx && jl == 0 && tvalid[u]) {
+        // debug output in exact descending score order: insertion sort of the k selected in place
+        int16_t* list = sel[tl[u]];
+        for (int r = 1; r < k; ++r) {
+          const int e = list[r];
+          const float se = (unsigned)e < (unsigned)E ? S[tl[u] * SROW + e] : -__builtin_inff();
+          int q = r;
+          while (q > 0) {
+            const int eo = list[q - 1];
+            const float so = (unsigned)eo < (unsigned)E ? S[tl[u] * SROW + eo] : -__builtin_inff();
+            if (so > se || (so == se && eo < e)) break;
+            list[q] = (int16_t)eo;
+            --q;
+          }
+          list[q] = (int16_t)e;
+        }
+        for (int r = 0; r < k; ++r) p.topk_idx[tt[u] * k + r] = list[r];
+      }
     }
   }
   lds_barrier();
