@@ -90,8 +90,10 @@ def cpu_baseline(wl, li, e2r, slots, target_s: float):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=200)
+    # The chip needs roughly 20-40 ms of sustained load before its clocks settle (measured: the first
+    # launches take up to 1.5x the steady-state time), so the default warm-up is long.
+    ap.add_argument("--warmup", type=int, default=400)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -148,7 +150,9 @@ def main():
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
 
-    # the predictor kernel alone: K launches back to back, bracketed by events on its stream
+    # the predictor kernel alone: K launches back to back, bracketed by events on its stream.  With
+    # no idle gap between launches the chip sustains a slightly lower clock than inside the step,
+    # so this duration is the conservative one.
     k_start = torch.cuda.Event(enable_timing=True)
     k_end = torch.cuda.Event(enable_timing=True)
     k_start.record(stream)
@@ -167,6 +171,20 @@ def main():
     p_end.record(stream)
     torch.cuda.synchronize()
     plan_ms = p_start.elapsed_time(p_end) / K
+
+    # context: the vendor library's plain router GEMM (hipBLASLt through torch.matmul, bf16 in and
+    # out, no scoring or selection) on the same hidden buffers, timed the same way
+    g_start = torch.cuda.Event(enable_timing=True)
+    g_end = torch.cuda.Event(enable_timing=True)
+    wt = w.t()
+    for i in range(min(args.warmup, 50)):
+        torch.matmul(xs[i % nbuf], wt)
+    g_start.record(stream)
+    for i in range(K):
+        torch.matmul(xs[i % nbuf], wt)
+    g_end.record(stream)
+    torch.cuda.synchronize()
+    gemm_ms = g_start.elapsed_time(g_end) / K
 
     counts = out.counts.cpu().numpy()
     host_plan = plan.to_host()
@@ -213,6 +231,10 @@ def main():
                      "bytes_per_launch": nbytes, "kernel_ms": avg_kernel_s * 1e3,
                      "mfma": {"achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                               "frac": tflops / PEAK_BF16_TFLOPS}},
+        "context": {"hipblaslt_router_gemm_ms": gemm_ms,
+                    "what": "torch.matmul(hidden, router_w.T), bf16 in and out, same buffers and "
+                            "stream, K back-to-back launches: the plain GEMM alone, without scores, "
+                            "selection or histogram; compare with roofline.kernel_ms"},
         "plan": {"swaps": len(host_plan.swaps), "kernel_ms": plan_ms,
                  "max_mean_before": float(out.max_mean.item()),
                  "max_mean_after": float(host_plan.rank_loads.max() * wl.R / host_plan.rank_loads.sum())},
