@@ -32,6 +32,16 @@ Readings of points the paper leaves open:
 * The per-rank budget (the paper enforces budgets per participant, not only globally) is a cap on the
   number of accepted swaps a rank takes part in; 0 means no per-rank cap.
 * The benefit reported for a swap is gamma_den * Delta, an exact integer.
+
+Time-budgeted planning (the cost form of the same section, Eq. 9-10, with the budget enforced per
+rank and per link), used when a cost model is given:
+
+* every candidate costs C = alpha + ceil((S(e_a) + S(e_b)) / beta) whole nanoseconds on its link
+  (oracle.cost.swap_cost_ns; an empty slot transfers nothing);
+* a candidate is admissible only if C fits the remaining budget of both ranks and of their link;
+* candidates are ordered by decreasing Delta / C, then by the same lexicographic tie-break;
+* after an accepted swap both ranks' and the link's remaining budgets drop by C.
+The swap cap and the per-rank cap still apply on top of the time budget.
 """
 from __future__ import annotations
 
@@ -39,6 +49,8 @@ from fractions import Fraction
 from typing import List, NamedTuple, Optional, Tuple
 
 import numpy as np
+
+from .cost import CostModel, swap_cost_ns
 
 FRONTIER, FULL = "frontier", "full"
 
@@ -59,6 +71,7 @@ class Plan(NamedTuple):
     expert_to_rank: np.ndarray
     rank_loads: np.ndarray     # loads after the plan
     loads_before: np.ndarray
+    costs: List[int]           # cost of every swap in ns (time-budgeted planning), else empty
 
 
 def phi(L, gamma: Fraction) -> Fraction:
@@ -70,7 +83,7 @@ def phi(L, gamma: Fraction) -> Fraction:
 
 def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]] = None,
                tau: int = 0, mode: str = FRONTIER, per_rank_cap: int = 0,
-               layer_id: int = 0) -> Plan:
+               layer_id: int = 0, cost: Optional[CostModel] = None) -> Plan:
     counts = [int(c) for c in np.asarray(counts).reshape(-1)]
     E = len(counts)
     table = np.asarray(slots, dtype=np.int64)
@@ -107,6 +120,19 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
     moved = set()
     part = [0] * R
     swaps: List[Swap] = []
+    costs: List[int] = []
+    if cost is not None:
+        if len(cost.rank_node) != R or len(cost.expert_bytes) != E:
+            raise ValueError("cost model does not match the placement")
+        if any(int(v) < 0 for v in cost.expert_bytes) or cost.rank_budget_ns < 0 or \
+                (cost.link_budget_ns is not None and cost.link_budget_ns < 0):
+            raise ValueError("negative size or budget")
+        rank_left = [int(cost.rank_budget_ns)] * R
+        link_cap = int(cost.rank_budget_ns if cost.link_budget_ns is None else cost.link_budget_ns)
+        link_used = {}
+
+    def bytes_of(i: int) -> int:
+        return int(cost.expert_bytes[i]) if i < E else 0
 
     def lowest_argmax(vals):
         return max(range(len(vals)), key=lambda r: (vals[r], -r))
@@ -141,12 +167,21 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
                     delta = phi_now - phi(L2, gamma)
                     if delta <= 0:
                         continue
-                    rank_key = (-delta, layer_id, a, b, i, j)
+                    if cost is None:
+                        c, order = 0, -delta
+                    else:
+                        c = swap_cost_ns(cost, a, b, bytes_of(i), bytes_of(j))
+                        link = (min(a, b), max(a, b))
+                        if c > rank_left[a] or c > rank_left[b] or \
+                                c > link_cap - link_used.get(link, 0):
+                            continue
+                        order = -(delta / c)
+                    rank_key = (order, layer_id, a, b, i, j)
                     if best is None or rank_key < best[0]:
-                        best = (rank_key, a, b, p, q, L2, delta)
+                        best = (rank_key, a, b, p, q, L2, delta, c)
         if best is None:
             break
-        _, a, b, p, q, L2, delta = best
+        _, a, b, p, q, L2, delta, c = best
         i, j = item[a][p], item[b][q]
         item[a][p], item[b][q] = j, i
         L = L2
@@ -156,6 +191,12 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
         g = delta * g_den
         assert g.denominator == 1
         swaps.append(Swap(a, b, p, q, i if i < E else -1, j if j < E else -1, int(g)))
+        if cost is not None:
+            rank_left[a] -= c
+            rank_left[b] -= c
+            link = (min(a, b), max(a, b))
+            link_used[link] = link_used.get(link, 0) + c
+            costs.append(c)
 
     new_slots = np.array([[i if i < E else -1 for i in row] for row in item], dtype=np.int32)
     e2r = np.empty(E, dtype=np.int32)
@@ -163,4 +204,4 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
         for i in item[r]:
             if i < E:
                 e2r[i] = r
-    return Plan(swaps, new_slots, e2r, np.array(L, dtype=np.int64), before)
+    return Plan(swaps, new_slots, e2r, np.array(L, dtype=np.int64), before, costs)
