@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define FB_ABI_VERSION 2
+#define FB_ABI_VERSION 3
 
 /* Status codes. */
 #define FB_OK 0
@@ -98,6 +98,28 @@ typedef struct fb_budget {
   int32_t mode;
   int32_t layer_id;
 } fb_budget;
+
+/* Migration cost model and time budget of the planner (Sec. "Budgeted Expert-Swap Planning",
+ * Eq. 9-10, with the budget enforced per rank and per link).  A swap of the item on rank a with the
+ * item on rank b costs, in whole nanoseconds,
+ *     C = alpha_ns[t] + ceil((S(e_a) + S(e_b)) * 1000 / beta_bytes_per_us[t]),
+ * where t = 0 if the two ranks share a node and 1 otherwise (the paper's intra- and inter-node
+ * links) and S(e) is the size of expert e (an empty slot transfers nothing).  A candidate is
+ * admissible only if C fits the remaining budget of both ranks and of their link; admissible
+ * candidates are ranked by benefit / C (compared exactly, by cross-multiplication), then by the
+ * tie-break of fb_budget.layer_id; an accepted swap charges C to both ranks and to the link.
+ *   rank_budget_ns     B_l of Eq. 10 for every rank, >= 0 (the profiled attention time of the
+ *                      layer's attention type minus the safety margin delta).
+ *   link_budget_ns     budget of every rank pair, >= 0; -1 = rank_budget_ns (then the rank budgets
+ *                      already bound every link).
+ *   alpha_ns           per-swap overhead for link types 0 and 1, 1 .. 2^40.
+ *   beta_bytes_per_us  point-to-point bandwidth for link types 0 and 1, 1 .. 2^40. */
+typedef struct fb_cost_model {
+  int64_t rank_budget_ns;
+  int64_t link_budget_ns;
+  int64_t alpha_ns[2];
+  int64_t beta_bytes_per_us[2];
+} fb_cost_model;
 
 /* One accepted swap, in acceptance order.  The expert in src_slot of src_rank (the more loaded
  * rank) trades places with the expert in dst_slot of dst_rank.  expert_* is -1 for an empty slot
@@ -276,6 +298,42 @@ int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_e
                          int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
                          int32_t* new_slot_expert, int32_t* new_expert_to_rank,
                          int64_t* new_rank_loads, int32_t* status, void* stream);
+
+/* The planner under a time budget (fb_cost_model) on the host: fb_plan_swaps with every candidate
+ * costed by Eq. 9 and admitted against the per-rank and per-link budgets, ranked by benefit-to-cost
+ * ratio.  budget->max_swaps and budget->per_rank_cap still apply on top of the time budget.  Pure
+ * and deterministic.
+ *   cost            host, see fb_cost_model.
+ *   rank_node       host int32[R]: node id of every rank (link type 0 between equal ids).
+ *   expert_bytes    host int64[E]: S(e), 0 .. 2^40.
+ *   swap_cost_ns    host int64[swaps_cap] out, may be NULL: C of every accepted swap.
+ * Every other argument as in fb_plan_swaps.  FB_EINVAL also for a null cost, rank_node or
+ * expert_bytes, or a cost-model value out of range. */
+int fb_plan_swaps_timed(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
+                        int32_t S, const fb_budget* budget, const fb_cost_model* cost,
+                        const int32_t* rank_node, const int64_t* expert_bytes, fb_swap* swaps,
+                        int64_t* swap_cost_ns, int32_t swaps_cap, int32_t* n_swaps,
+                        int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                        int64_t* new_rank_loads);
+
+/* The time-budgeted planner as one stream-ordered single-workgroup kernel: exactly the plan of
+ * fb_plan_swaps_timed.  Limits as fb_plan_swaps_device, and budget->max_swaps <= 1024.
+ *   counts, slot_expert   device inputs as in fb_plan_swaps.
+ *   budget, cost          host structs, read during the call.
+ *   rank_node             device int32[R].
+ *   expert_bytes          device int64[E].
+ *   swaps                 device fb_swap[budget->max_swaps] out.
+ *   swap_cost_ns          device int64[budget->max_swaps] out, may be NULL.
+ *   n_swaps, new_slot_expert, new_expert_to_rank, new_rank_loads, status  as fb_plan_swaps_device;
+ *                         status is FB_EINVAL also for an expert size outside 0 .. 2^40.
+ * FB_EUNSUPPORTED for max_swaps > 1024; FB_EINVAL for a cost-model value out of range. */
+int fb_plan_swaps_timed_device(const int32_t* counts, int32_t E, const int32_t* slot_expert,
+                               int32_t R, int32_t S, const fb_budget* budget,
+                               const fb_cost_model* cost, const int32_t* rank_node,
+                               const int64_t* expert_bytes, fb_swap* swaps, int64_t* swap_cost_ns,
+                               int32_t* n_swaps, int32_t* new_slot_expert,
+                               int32_t* new_expert_to_rank, int64_t* new_rank_loads,
+                               int32_t* status, void* stream);
 
 /* Swap cap from the cost model: with a uniform expert size S_e and one link type every swap costs
  * C = alpha + 2 * S_e / beta (Eq. 9) and the window is B_l = max(0, t_attn - delta) (Eq. 10); the

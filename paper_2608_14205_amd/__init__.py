@@ -6,6 +6,7 @@ absence raises an error: nothing here computes on the CPU in its place.
 """
 from .api import (  # noqa: F401
     Budget,
+    CostModel,
     DevicePlan,
     PackedRouter,
     Quality,
@@ -20,6 +21,8 @@ from .api import (  # noqa: F401
     topk_hits,
     plan_swaps,
     plan_swaps_device,
+    plan_swaps_timed,
+    plan_swaps_timed_device,
     predict_load,
     swap_budget_from_cost,
 )

@@ -16,7 +16,7 @@ FB_OK, FB_EINVAL, FB_EUNSUPPORTED, FB_EDEVICE, FB_ENOSPC = 0, -1, -2, -3, -4
 FB_BF16, FB_F32 = 0, 1
 FB_SOFTMAX, FB_SIGMOID = 0, 1
 FB_FRONTIER, FB_FULL = 0, 1
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 
 class fb_scoring(ctypes.Structure):
@@ -29,6 +29,11 @@ class fb_budget(ctypes.Structure):
                 ("tau", ctypes.c_int64), ("gamma_num", ctypes.c_int64),
                 ("gamma_den", ctypes.c_int64), ("mode", ctypes.c_int32),
                 ("layer_id", ctypes.c_int32)]
+
+
+class fb_cost_model(ctypes.Structure):
+    _fields_ = [("rank_budget_ns", ctypes.c_int64), ("link_budget_ns", ctypes.c_int64),
+                ("alpha_ns", ctypes.c_int64 * 2), ("beta_bytes_per_us", ctypes.c_int64 * 2)]
 
 
 class fb_swap(ctypes.Structure):
@@ -63,6 +68,13 @@ SIGNATURES = {
                                      _I32, _VP, _VP, _VP, _VP]),
     "fb_plan_swaps_device": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32, ctypes.POINTER(fb_budget),
                                             _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "fb_plan_swaps_timed": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32, ctypes.POINTER(fb_budget),
+                                           ctypes.POINTER(fb_cost_model), _VP, _VP, _VP, _VP, _I32,
+                                           _VP, _VP, _VP, _VP]),
+    "fb_plan_swaps_timed_device": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32,
+                                                  ctypes.POINTER(fb_budget),
+                                                  ctypes.POINTER(fb_cost_model), _VP, _VP, _VP,
+                                                  _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "fb_swap_budget_from_cost": (_I64, [_D, _D, _D, _D, _I64]),
     "fb_topk_hits": (ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
     "fb_cosine_workspace_bytes": (_SZ, []),

@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import ctypes
 import dataclasses
-from typing import List, NamedTuple, Optional, Tuple
+from typing import List, NamedTuple, Optional, Sequence, Tuple
 
 import numpy as np
 import torch
@@ -58,6 +58,27 @@ class Budget:
                            self.layer_id)
 
 
+@dataclasses.dataclass(frozen=True)
+class CostModel:
+    """Migration cost model and time budget (fb_cost_model plus the per-rank node ids and the
+    per-expert sizes).  link_budget_ns=None means the rank budget."""
+
+    rank_node: Sequence[int]
+    expert_bytes: Sequence[int]
+    alpha_ns: Tuple[int, int]
+    beta_bytes_per_us: Tuple[int, int]
+    rank_budget_ns: int
+    link_budget_ns: Optional[int] = None
+
+    def to_c(self) -> L.fb_cost_model:
+        m = L.fb_cost_model()
+        m.rank_budget_ns = self.rank_budget_ns
+        m.link_budget_ns = -1 if self.link_budget_ns is None else self.link_budget_ns
+        m.alpha_ns[0], m.alpha_ns[1] = self.alpha_ns
+        m.beta_bytes_per_us[0], m.beta_bytes_per_us[1] = self.beta_bytes_per_us
+        return m
+
+
 @dataclasses.dataclass
 class Prediction:
     counts: torch.Tensor                 # int32 [E]
@@ -72,6 +93,7 @@ class Plan(NamedTuple):
     slots: np.ndarray          # int32 R x S
     expert_to_rank: np.ndarray  # int32 E
     rank_loads: np.ndarray     # int64 R
+    costs: Optional[List[int]] = None  # ns per swap, time-budgeted planning only
 
 
 @dataclasses.dataclass
@@ -82,14 +104,16 @@ class DevicePlan:
     expert_to_rank: torch.Tensor  # int32 [E]
     rank_loads: torch.Tensor   # int64 [R]
     status: torch.Tensor       # int32 [1]
+    costs: Optional[torch.Tensor] = None  # int64 [max_swaps]: ns per swap (time budget only)
 
     def to_host(self) -> Plan:
         st = int(self.status.item())
         L.check(st, "fb_plan_swaps_device (device status)")
         n = int(self.n_swaps.item())
         rec = np.frombuffer(self.swaps.cpu().numpy().tobytes(), dtype=SWAP_DTYPE)[:n]
+        costs = None if self.costs is None else [int(v) for v in self.costs.cpu().numpy()[:n]]
         return Plan([tuple(int(v) for v in r) for r in rec], self.slots.cpu().numpy(),
-                    self.expert_to_rank.cpu().numpy(), self.rank_loads.cpu().numpy())
+                    self.expert_to_rank.cpu().numpy(), self.rank_loads.cpu().numpy(), costs)
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -271,6 +295,38 @@ def plan_swaps(counts, slots, budget: Budget) -> Plan:
     return Plan(out, new_slots, new_e2r, new_L)
 
 
+def plan_swaps_timed(counts, slots, budget: Budget, cost: CostModel) -> Plan:
+    """fb_plan_swaps_timed (host planner under a time budget) on host arrays."""
+    c = np.ascontiguousarray(np.asarray(counts), dtype=np.int32)
+    sl = np.ascontiguousarray(np.asarray(slots), dtype=np.int32)
+    if sl.ndim != 2:
+        raise ValueError("slots must be R x S")
+    R, S = sl.shape
+    E = c.size
+    nodes = np.ascontiguousarray(np.asarray(cost.rank_node), dtype=np.int32)
+    nbytes = np.ascontiguousarray(np.asarray(cost.expert_bytes), dtype=np.int64)
+    if nodes.size != R or nbytes.size != E:
+        raise ValueError("cost model does not match the placement")
+    bg = budget.to_c()
+    cm = cost.to_c()
+    cap = max(budget.max_swaps, 1)
+    swaps = (L.fb_swap * cap)()
+    costs = np.zeros(cap, np.int64)
+    n = ctypes.c_int32(0)
+    new_slots = np.empty((R, S), np.int32)
+    new_e2r = np.empty(E, np.int32)
+    new_L = np.empty(R, np.int64)
+    st = L.lib().fb_plan_swaps_timed(c.ctypes.data, E, sl.ctypes.data, R, S, ctypes.byref(bg),
+                                     ctypes.byref(cm), nodes.ctypes.data, nbytes.ctypes.data,
+                                     ctypes.addressof(swaps), costs.ctypes.data, cap,
+                                     ctypes.addressof(n), new_slots.ctypes.data, new_e2r.ctypes.data,
+                                     new_L.ctypes.data)
+    L.check(st, "fb_plan_swaps_timed")
+    out = [(s.src_rank, s.dst_rank, s.src_slot, s.dst_slot, s.expert_src, s.expert_dst, s.gain)
+           for s in swaps[:n.value]]
+    return Plan(out, new_slots, new_e2r, new_L, [int(v) for v in costs[:n.value]])
+
+
 def plan_swaps_device(counts: torch.Tensor, slots: torch.Tensor, budget: Budget,
                       out: Optional[DevicePlan] = None,
                       stream: Optional[torch.cuda.Stream] = None) -> DevicePlan:
@@ -296,6 +352,44 @@ def plan_swaps_device(counts: torch.Tensor, slots: torch.Tensor, budget: Budget,
             out.n_swaps.data_ptr(), out.slots.data_ptr(), out.expert_to_rank.data_ptr(),
             out.rank_loads.data_ptr(), out.status.data_ptr(), _stream_handle(dev, stream))
     L.check(st, "fb_plan_swaps_device")
+    return out
+
+
+def plan_swaps_timed_device(counts: torch.Tensor, slots: torch.Tensor, budget: Budget,
+                            cost: CostModel, out: Optional[DevicePlan] = None,
+                            stream: Optional[torch.cuda.Stream] = None) -> DevicePlan:
+    """fb_plan_swaps_timed_device: the time-budgeted planner as a stream-ordered kernel.  The
+    cost model's node ids and expert sizes may be sequences (copied to the device) or device
+    tensors (int32[R] and int64[E])."""
+    if counts.dtype != torch.int32 or slots.dtype != torch.int32 or slots.dim() != 2:
+        raise ValueError("counts must be int32[E] and slots int32[R, S]")
+    if not (counts.is_contiguous() and slots.is_contiguous()):
+        raise ValueError("counts and slots must be contiguous")
+    dev = counts.device
+    R, S = slots.shape
+    E = counts.numel()
+    nodes = torch.as_tensor(cost.rank_node, dtype=torch.int32, device=dev).contiguous()
+    nbytes = torch.as_tensor(cost.expert_bytes, dtype=torch.int64, device=dev).contiguous()
+    if nodes.numel() != R or nbytes.numel() != E:
+        raise ValueError("cost model does not match the placement")
+    cap = max(budget.max_swaps, 1)
+    if out is None:
+        out = DevicePlan(torch.empty(cap * SWAP_BYTES, dtype=torch.uint8, device=dev),
+                         torch.empty(1, dtype=torch.int32, device=dev),
+                         torch.empty((R, S), dtype=torch.int32, device=dev),
+                         torch.empty(E, dtype=torch.int32, device=dev),
+                         torch.empty(R, dtype=torch.int64, device=dev),
+                         torch.empty(1, dtype=torch.int32, device=dev),
+                         torch.zeros(cap, dtype=torch.int64, device=dev))
+    bg = budget.to_c()
+    cm = cost.to_c()
+    with torch.cuda.device(dev):
+        st = L.lib().fb_plan_swaps_timed_device(
+            counts.data_ptr(), E, slots.data_ptr(), R, S, ctypes.byref(bg), ctypes.byref(cm),
+            nodes.data_ptr(), nbytes.data_ptr(), out.swaps.data_ptr(), _ptr(out.costs),
+            out.n_swaps.data_ptr(), out.slots.data_ptr(), out.expert_to_rank.data_ptr(),
+            out.rank_loads.data_ptr(), out.status.data_ptr(), _stream_handle(dev, stream))
+    L.check(st, "fb_plan_swaps_timed_device")
     return out
 
 

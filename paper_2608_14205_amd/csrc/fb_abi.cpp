@@ -267,6 +267,60 @@ int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_e
   a.new_rank_loads = new_rank_loads;
   a.status = status;
   a.stream = stream;
+  a.timed = 0;
+  a.rank_node = nullptr;
+  a.expert_bytes = nullptr;
+  a.swap_cost_ns = nullptr;
+  return fb::launch_plan_device(a);
+}
+
+int fb_plan_swaps_timed_device(const int32_t* counts, int32_t E, const int32_t* slot_expert,
+                               int32_t R, int32_t S, const fb_budget* budget,
+                               const fb_cost_model* cost, const int32_t* rank_node,
+                               const int64_t* expert_bytes, fb_swap* swaps, int64_t* swap_cost_ns,
+                               int32_t* n_swaps, int32_t* new_slot_expert,
+                               int32_t* new_expert_to_rank, int64_t* new_rank_loads,
+                               int32_t* status, void* stream) {
+  if (!counts || !slot_expert || !budget || !cost || !rank_node || !expert_bytes || !n_swaps ||
+      !new_slot_expert || !new_expert_to_rank || !new_rank_loads || !status)
+    return FB_EINVAL;
+  if (E < 1 || R < 1 || S < 1) return FB_EINVAL;
+  if (R > FB_MAX_RANKS || (int64_t)R * S > FB_MAX_SLOTS_TOTAL) return FB_EUNSUPPORTED;
+  if (E > R * S) return FB_EINVAL;
+  const fb_budget bg = *budget;
+  if (bg.max_swaps < 0 || bg.per_rank_cap < 0 || bg.tau < 0 || bg.gamma_num < 0 || bg.gamma_den < 0)
+    return FB_EINVAL;
+  if (bg.mode != FB_FRONTIER && bg.mode != FB_FULL) return FB_EINVAL;
+  if (bg.max_swaps > 0 && !swaps) return FB_EINVAL;
+  if (bg.max_swaps > fb::kMaxTimedSwaps) return FB_EUNSUPPORTED;
+  fb_cost_model m = *cost;
+  if (m.rank_budget_ns < 0 || m.link_budget_ns < -1) return FB_EINVAL;
+  for (int t = 0; t < 2; ++t)
+    if (m.alpha_ns[t] < 1 || m.alpha_ns[t] > fb::kCostLimit || m.beta_bytes_per_us[t] < 1 ||
+        m.beta_bytes_per_us[t] > fb::kCostLimit)
+      return FB_EINVAL;
+  if (m.link_budget_ns < 0) m.link_budget_ns = m.rank_budget_ns;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  fb::PlanDeviceLaunch a;
+  a.counts = counts;
+  a.E = E;
+  a.slot_expert = slot_expert;
+  a.R = R;
+  a.S = S;
+  a.budget = bg;
+  a.swaps = swaps;
+  a.n_swaps = n_swaps;
+  a.new_slot_expert = new_slot_expert;
+  a.new_expert_to_rank = new_expert_to_rank;
+  a.new_rank_loads = new_rank_loads;
+  a.status = status;
+  a.stream = stream;
+  a.timed = 1;
+  a.cost = m;
+  a.rank_node = rank_node;
+  a.expert_bytes = expert_bytes;
+  a.swap_cost_ns = swap_cost_ns;
   return fb::launch_plan_device(a);
 }
 

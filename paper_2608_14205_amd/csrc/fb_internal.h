@@ -60,7 +60,15 @@ struct PlanDeviceLaunch {
   int64_t* new_rank_loads;
   int32_t* status;
   void* stream;
+  // time budget (fb_plan_swaps_timed_device); timed == 0 for a swap-count budget
+  int32_t timed;
+  fb_cost_model cost;            // link_budget_ns already resolved (>= 0)
+  const int32_t* rank_node;      // device int32[R]
+  const int64_t* expert_bytes;   // device int64[E]
+  int64_t* swap_cost_ns;         // device int64[max_swaps] or NULL
 };
+constexpr int kMaxTimedSwaps = 1024;           // swap cap of the device planner under a time budget
+constexpr int64_t kCostLimit = (int64_t)1 << 40;  // alpha, beta and expert sizes
 int launch_plan_device(const PlanDeviceLaunch& a);
 
 // Prediction-quality diagnostics (fb_quality.hip).

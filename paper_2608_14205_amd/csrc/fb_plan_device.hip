@@ -16,8 +16,13 @@
 //     loads live in registers (ranks lane + 64 m), each lane owns one candidate (p, q), slot entries
 //     carry the item, its moved flag and its count so that a candidate costs one LDS round trip,
 //     and a round is a handful of wave reductions with no workgroup barrier.
-//   * plan_general<NT> for everything else (full mode, larger S): state in LDS, threads split the
-//     candidates by rank pair, per-wave reductions combined through LDS.
+//   * plan_general<NT> for everything else (full mode, larger S, a time budget): state in LDS,
+//     threads split the candidates by rank pair, per-wave reductions combined through LDS.
+//
+// Under a time budget (the cost form of the same section, Eq. 9-10 enforced per rank and per link)
+// every candidate also costs C = alpha + ceil(bytes * 1000 / beta) ns on its link, must fit what is
+// left of both ranks' and the link's budgets, and the best candidate is the largest benefit / C,
+// compared exactly as gain_1 * C_2 vs gain_2 * C_1 (gains < 2^63, costs < 2^42), then the tie key.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -83,11 +88,49 @@ struct Shared {
   int64_t L[kMaxR];
   int32_t part[kMaxR];
   uint8_t moved[2 * kMaxRS];
-  uint64_t wgain[16], wtie[16];
+  uint64_t wgain[16], wtie[16], wcost[16];
   int64_t N;
   int32_t bad, stop, amax, amin, top[3], ns;
   int64_t other;
+  // time budget: what is left of every rank's budget, rank nodes, and the accepted swaps' links
+  // and costs (the link budgets are charged by scanning them)
+  int64_t rank_left[kMaxR];
+  int32_t node[kMaxR];
+  int32_t acc_pair[kMaxTimedSwaps];   // a * kMaxR + b, a < b
+  int64_t acc_cost[kMaxTimedSwaps];
 };
+
+// Eq. 9 in whole nanoseconds for a swap of items i (rank a) and j (rank b).
+__device__ __forceinline__ int64_t swap_cost(const PlanDeviceLaunch& a, const Shared& sh, int ra,
+                                             int rb, int i, int j) {
+  const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
+  const int64_t bytes = (i < a.E ? a.expert_bytes[i] : 0) + (j < a.E ? a.expert_bytes[j] : 0);
+  const int64_t beta = a.cost.beta_bytes_per_us[t];
+  return a.cost.alpha_ns[t] + (bytes * 1000 + beta - 1) / beta;
+}
+
+// Does a swap of cost c between ranks ra and rb fit the remaining rank and link budgets?
+__device__ __forceinline__ bool swap_fits(const PlanDeviceLaunch& a, const Shared& sh, int ra,
+                                          int rb, int64_t c) {
+  if (c > sh.rank_left[ra] || c > sh.rank_left[rb]) return false;
+  // every swap on a link also charges both of its ranks, so a link budget at least the rank
+  // budget never binds
+  if (a.cost.link_budget_ns >= a.cost.rank_budget_ns) return true;
+  const int key = ra < rb ? ra * kMaxR + rb : rb * kMaxR + ra;
+  int64_t used = 0;
+  for (int s = 0; s < sh.ns; ++s) used += sh.acc_pair[s] == key ? sh.acc_cost[s] : 0;
+  return c <= a.cost.link_budget_ns - used;
+}
+
+// (gain, cost, tie) ordering of the time-budgeted planner; gain 0 means "no candidate".
+__device__ __forceinline__ bool ratio_better(uint64_t g1, uint64_t c1, uint64_t t1, uint64_t g2,
+                                             uint64_t c2, uint64_t t2) {
+  if (g1 == 0) return false;
+  if (g2 == 0) return true;
+  const unsigned __int128 l = (unsigned __int128)g1 * c2, r = (unsigned __int128)g2 * c1;
+  if (l != r) return l > r;
+  return t1 < t2;
+}
 
 template <int NT>
 __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
@@ -102,7 +145,12 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   for (int e = tid; e < E; e += NT) { sh.seen[e] = 0; sh.cnt[e] = a.counts[e]; }
   for (int c = tid; c < E + RS; c += NT) sh.moved[c] = 0;
   for (int r = tid; r < R; r += NT) sh.part[r] = 0;
+  if (a.timed)
+    for (int r = tid; r < R; r += NT) { sh.node[r] = a.rank_node[r]; sh.rank_left[r] = a.cost.rank_budget_ns; }
   __syncthreads();
+  if (a.timed)
+    for (int e = tid; e < E; e += NT)
+      if (a.expert_bytes[e] < 0 || a.expert_bytes[e] > kCostLimit) sh.bad = 1;
   for (int c = tid; c < RS; c += NT) {
     const int e = a.slot_expert[c];
     if (e == -1) { sh.item[c] = E + c; sh.pos[E + c] = c; }
@@ -181,6 +229,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
     const int amax = sh.amax, amin = sh.amin;
     const int64_t M = sh.L[amax];
     uint64_t bgain = 0, btie = 0;     // gain 0: nothing found (every accepted gain is > 0)
+    uint64_t bcost = 1;
     auto consider = [&](int ra, int rb, int p, int q, int64_t other) {
       const int i = sh.item[ra * S + p], j = sh.item[rb * S + q];
       if (sh.moved[i] || sh.moved[j] || (i >= E && j >= E)) return;
@@ -193,6 +242,14 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       const int64_t gain = g_den * (M - m2) + spread;
       if (gain <= 0) return;
       const uint64_t tk = tie_key(ra, rb, i, j);
+      if (a.timed) {
+        const int64_t c = swap_cost(a, sh, ra, rb, i, j);
+        if (!swap_fits(a, sh, ra, rb, c)) return;
+        if (ratio_better((uint64_t)gain, (uint64_t)c, tk, bgain, bcost, btie)) {
+          bgain = (uint64_t)gain; bcost = (uint64_t)c; btie = tk;
+        }
+        return;
+      }
       if ((uint64_t)gain > bgain || ((uint64_t)gain == bgain && tk < btie)) { bgain = (uint64_t)gain; btie = tk; }
     };
     const bool capped = bg.per_rank_cap != 0;
@@ -218,17 +275,34 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
           for (int q = 0; q < S; ++q) consider(ra, rb, p, q, other);
       }
     }
-    // best of the wave: largest gain, then smallest tie key
-    const uint64_t wg = wave_max_u64(bgain);
-    const uint64_t wt = ~wave_max_u64((wg != 0 && bgain == wg) ? ~btie : 0ull);
-    uint64_t g = wg, t = wt;
-    if (NT > 64) {
-      if (lane == 0) { sh.wgain[wave] = wg; sh.wtie[wave] = wt; }
+    uint64_t g, t, cst = 1;
+    if (a.timed) {
+      // best of the wave by benefit / cost, then tie key: butterfly over the lanes
+      uint64_t wg = bgain, wc = bcost, wt = btie;
+      for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t og = __shfl_xor(wg, off), oc = __shfl_xor(wc, off), ot = __shfl_xor(wt, off);
+        if (ratio_better(og, oc, ot, wg, wc, wt)) { wg = og; wc = oc; wt = ot; }
+      }
+      if (lane == 0) { sh.wgain[wave] = wg; sh.wtie[wave] = wt; sh.wcost[wave] = wc; }
       __syncthreads();
-      g = sh.wgain[0]; t = sh.wtie[0];
-      for (int w = 1; w < NT / 64; ++w) {
-        const uint64_t og = sh.wgain[w], ot = sh.wtie[w];
-        if (og > g || (og == g && og != 0 && ot < t)) { g = og; t = ot; }
+      g = sh.wgain[0]; t = sh.wtie[0]; cst = sh.wcost[0];
+      for (int w = 1; w < NT / 64; ++w)
+        if (ratio_better(sh.wgain[w], sh.wcost[w], sh.wtie[w], g, cst, t)) {
+          g = sh.wgain[w]; t = sh.wtie[w]; cst = sh.wcost[w];
+        }
+    } else {
+      // best of the wave: largest gain, then smallest tie key
+      const uint64_t wg = wave_max_u64(bgain);
+      const uint64_t wt = ~wave_max_u64((wg != 0 && bgain == wg) ? ~btie : 0ull);
+      g = wg; t = wt;
+      if (NT > 64) {
+        if (lane == 0) { sh.wgain[wave] = wg; sh.wtie[wave] = wt; }
+        __syncthreads();
+        g = sh.wgain[0]; t = sh.wtie[0];
+        for (int w = 1; w < NT / 64; ++w) {
+          const uint64_t og = sh.wgain[w], ot = sh.wtie[w];
+          if (og > g || (og == g && og != 0 && ot < t)) { g = og; t = ot; }
+        }
       }
     }
     if (g == 0) break;                          // no admissible candidate with positive benefit
@@ -251,6 +325,13 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       sw.expert_dst = cj < E ? cj : -1;
       sw.gain = (int64_t)g;
       a.swaps[sh.ns] = sw;
+      if (a.timed) {
+        sh.rank_left[ca] -= (int64_t)cst;
+        sh.rank_left[cb] -= (int64_t)cst;
+        sh.acc_pair[sh.ns] = ca < cb ? ca * kMaxR + cb : cb * kMaxR + ca;
+        sh.acc_cost[sh.ns] = (int64_t)cst;
+        if (a.swap_cost_ns) a.swap_cost_ns[sh.ns] = (int64_t)cst;
+      }
       sh.ns = sh.ns + 1;
     }
     __syncthreads();
@@ -528,7 +609,7 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
 int launch_plan_device(const PlanDeviceLaunch& a) {
   (void)hipGetLastError();
   hipStream_t st = static_cast<hipStream_t>(a.stream);
-  if (a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 64) {
+  if (!a.timed && a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 64) {
     if (a.R <= 64) hipLaunchKernelGGL(plan_frontier_wave<1>, dim3(1), dim3(64), 0, st, a);
     else if (a.R <= 128) hipLaunchKernelGGL(plan_frontier_wave<2>, dim3(1), dim3(64), 0, st, a);
     else if (a.R <= 256) hipLaunchKernelGGL(plan_frontier_wave<4>, dim3(1), dim3(64), 0, st, a);

@@ -14,10 +14,16 @@
 // accepts the candidate with the largest benefit, ties broken by (layer, src rank, dst rank, item
 // ids).  Empty slots are zero-load items with id E + r * S + s.  The loop ends when the swap cap is
 // reached, L_max - L_min <= tau, or no candidate remains.
+//
+// Under a time budget (fb_plan_swaps_timed) every candidate also costs C = alpha + ceil(bytes *
+// 1000 / beta) ns on its link (Eq. 9), must fit what is left of both ranks' and the link's budgets
+// (Eq. 10, enforced per participant), and candidates are ranked by benefit / C, compared exactly as
+// gain_1 * C_2 vs gain_2 * C_1.
 #include <stdint.h>
 #include <math.h>
 #include <string.h>
 
+#include <unordered_map>
 #include <vector>
 
 #include "fb_internal.h"
@@ -26,29 +32,63 @@ namespace {
 
 typedef __int128 i128;
 
+
 struct Best {
   bool found = false;
   i128 gain = 0;
+  int64_t cost = 1;     // 1 for every candidate under a swap-count budget
   int32_t a = 0, b = 0, p = 0, q = 0;
   int64_t i = 0, j = 0;
 };
 
-// Candidate ordering: larger gain first, then lexicographically smaller (a, b, i, j).
-bool better(i128 gain, int32_t a, int32_t b, int64_t i, int64_t j, const Best& cur) {
+// Candidate ordering: larger gain / cost first (exact cross-multiplication; gains < 2^63 and costs
+// < 2^42, so the products fit 128 bits), then lexicographically smaller (a, b, i, j).
+bool better(i128 gain, int64_t cost, int32_t a, int32_t b, int64_t i, int64_t j, const Best& cur) {
   if (!cur.found) return true;
-  if (gain != cur.gain) return gain > cur.gain;
+  const i128 lhs = gain * cur.cost, rhs = cur.gain * cost;
+  if (lhs != rhs) return lhs > rhs;
   if (a != cur.a) return a < cur.a;
   if (b != cur.b) return b < cur.b;
   if (i != cur.i) return i < cur.i;
   return j < cur.j;
 }
 
-}  // namespace
+// The time budget, when there is one: link types from the rank nodes, expert sizes, and what is
+// left of every rank's and every used link's budget.
+struct TimeBudget {
+  fb_cost_model m;
+  const int32_t* rank_node;
+  const int64_t* expert_bytes;
+  int32_t E, R;
+  int64_t link_cap;
+  std::vector<int64_t> rank_left;
+  std::unordered_map<int64_t, int64_t> link_used;   // key a * R + b with a < b
 
-extern "C" int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
-                             int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t swaps_cap,
-                             int32_t* n_swaps, int32_t* new_slot_expert,
-                             int32_t* new_expert_to_rank, int64_t* new_rank_loads) {
+  int64_t cost(int32_t a, int32_t b, int64_t i, int64_t j) const {   // Eq. 9, whole ns
+    const int t = rank_node[a] == rank_node[b] ? 0 : 1;
+    const int64_t bytes = (i < E ? expert_bytes[i] : 0) + (j < E ? expert_bytes[j] : 0);
+    const int64_t beta = m.beta_bytes_per_us[t];
+    return m.alpha_ns[t] + (bytes * 1000 + beta - 1) / beta;
+  }
+  int64_t link_key(int32_t a, int32_t b) const {
+    return a < b ? (int64_t)a * R + b : (int64_t)b * R + a;
+  }
+  bool fits(int32_t a, int32_t b, int64_t c) const {
+    if (c > rank_left[a] || c > rank_left[b]) return false;
+    const auto it = link_used.find(link_key(a, b));
+    return c <= link_cap - (it == link_used.end() ? 0 : it->second);
+  }
+  void charge(int32_t a, int32_t b, int64_t c) {
+    rank_left[a] -= c;
+    rank_left[b] -= c;
+    link_used[link_key(a, b)] += c;
+  }
+};
+
+int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R, int32_t S,
+              const fb_budget* budget, TimeBudget* tb, fb_swap* swaps, int64_t* swap_cost_ns,
+              int32_t swaps_cap, int32_t* n_swaps, int32_t* new_slot_expert,
+              int32_t* new_expert_to_rank, int64_t* new_rank_loads) {
   if (!counts || !slot_expert || !budget || !n_swaps || (swaps_cap > 0 && !swaps)) return FB_EINVAL;
   if (E < 1 || R < 1 || S < 1) return FB_EINVAL;
   if ((int64_t)R * S > (int64_t)1 << 30) return FB_EUNSUPPORTED;
@@ -131,8 +171,13 @@ extern "C" int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* sl
           if (other > m2) m2 = other;
           const i128 gain = g_den * (i128)(M - m2) + g_num * 2 * (i128)d * (i128)(L[b] - L[a] - d);
           if (gain <= 0) continue;
-          if (better(gain, a, b, i, j, best)) {
-            best.found = true; best.gain = gain;
+          int64_t c = 1;
+          if (tb) {
+            c = tb->cost(a, b, i, j);
+            if (!tb->fits(a, b, c)) continue;
+          }
+          if (better(gain, c, a, b, i, j, best)) {
+            best.found = true; best.gain = gain; best.cost = c;
             best.a = a; best.b = b; best.p = p; best.q = q; best.i = i; best.j = j;
           }
         }
@@ -163,6 +208,10 @@ extern "C" int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* sl
     sw.expert_src = best.i < E ? (int32_t)best.i : -1;
     sw.expert_dst = best.j < E ? (int32_t)best.j : -1;
     sw.gain = (int64_t)best.gain;
+    if (tb) {
+      tb->charge(best.a, best.b, best.cost);
+      if (swap_cost_ns) swap_cost_ns[ns - 1] = best.cost;
+    }
   }
 
   *n_swaps = ns;
@@ -174,6 +223,44 @@ extern "C" int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* sl
   if (new_rank_loads)
     for (int32_t r = 0; r < R; ++r) new_rank_loads[r] = L[r];
   return FB_OK;
+}
+
+}  // namespace
+
+extern "C" int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
+                             int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t swaps_cap,
+                             int32_t* n_swaps, int32_t* new_slot_expert,
+                             int32_t* new_expert_to_rank, int64_t* new_rank_loads) {
+  return plan_impl(counts, E, slot_expert, R, S, budget, nullptr, swaps, nullptr, swaps_cap, n_swaps,
+                   new_slot_expert, new_expert_to_rank, new_rank_loads);
+}
+
+extern "C" int fb_plan_swaps_timed(const int32_t* counts, int32_t E, const int32_t* slot_expert,
+                                   int32_t R, int32_t S, const fb_budget* budget,
+                                   const fb_cost_model* cost, const int32_t* rank_node,
+                                   const int64_t* expert_bytes, fb_swap* swaps,
+                                   int64_t* swap_cost_ns, int32_t swaps_cap, int32_t* n_swaps,
+                                   int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                                   int64_t* new_rank_loads) {
+  if (!cost || !rank_node || !expert_bytes || E < 1 || R < 1) return FB_EINVAL;
+  const fb_cost_model m = *cost;
+  if (m.rank_budget_ns < 0 || m.link_budget_ns < -1) return FB_EINVAL;
+  for (int t = 0; t < 2; ++t)
+    if (m.alpha_ns[t] < 1 || m.alpha_ns[t] > fb::kCostLimit || m.beta_bytes_per_us[t] < 1 ||
+        m.beta_bytes_per_us[t] > fb::kCostLimit)
+      return FB_EINVAL;
+  for (int32_t e = 0; e < E; ++e)
+    if (expert_bytes[e] < 0 || expert_bytes[e] > fb::kCostLimit) return FB_EINVAL;
+  TimeBudget tb;
+  tb.m = m;
+  tb.rank_node = rank_node;
+  tb.expert_bytes = expert_bytes;
+  tb.E = E;
+  tb.R = R;
+  tb.link_cap = m.link_budget_ns < 0 ? m.rank_budget_ns : m.link_budget_ns;
+  tb.rank_left.assign(R, m.rank_budget_ns);
+  return plan_impl(counts, E, slot_expert, R, S, budget, &tb, swaps, swap_cost_ns, swaps_cap,
+                   n_swaps, new_slot_expert, new_expert_to_rank, new_rank_loads);
 }
 
 extern "C" int64_t fb_swap_budget_from_cost(double t_attn_us, double delta_us, double alpha_us,

@@ -33,7 +33,8 @@ def test_header_declares_the_boundary():
                             "fb_pack_router_weight", "fb_predict_load", "fb_predict_load_packed",
                             "fb_plan_swaps", "fb_plan_swaps_device", "fb_swap_budget_from_cost",
                             "fb_topk_hits", "fb_cosine_workspace_bytes", "fb_row_cosine_mean",
-                            "fb_fold_rank_loads"])
+                            "fb_fold_rank_loads", "fb_plan_swaps_timed",
+                            "fb_plan_swaps_timed_device"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -47,11 +48,12 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(L.fb_scoring) == 20
     assert ctypes.sizeof(L.fb_budget) == 40
     assert ctypes.sizeof(L.fb_swap) == 32 == fb.api.SWAP_BYTES
+    assert ctypes.sizeof(L.fb_cost_model) == 48
 
 
 def test_version_and_status_strings():
     lib = fb.lib()
-    assert lib.fb_abi_version() == 2
+    assert lib.fb_abi_version() == 3
     for code in (0, -1, -2, -3, -4):
         assert L.status_string(code).startswith("FB_")
     assert "unknown" in L.status_string(7)
@@ -346,3 +348,101 @@ def test_oracle_is_not_reachable_from_the_product_package():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in re.findall(r"(?:import|from)\s+(\w+)", text), f
     assert "paper_2608_14205_amd" in sys.modules
+
+
+# ---- time-budgeted planner (Eq. 9-10, budgets per rank and link) --------------------------------
+
+def _cost_model(d):
+    return fb.CostModel(d["rank_node"], d["expert_bytes"], tuple(d["alpha_ns"]),
+                        tuple(d["beta_bytes_per_us"]), d["rank_budget_ns"], d.get("link_budget_ns"))
+
+
+def test_timed_host_planner_hand_worked_plans(golden_dir):
+    with open(os.path.join(golden_dir, "planner_costed_hand.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        h = fb.plan_swaps_timed(c["counts"], c["slots"], fb.Budget(c["max_swaps"], mode=c["mode"]),
+                                _cost_model(c["cost"]))
+        assert [list(s) for s in h.swaps] == c["swaps"], c["name"]
+        assert h.costs == c["costs"], c["name"]
+        assert h.slots.tolist() == c["new_slots"], c["name"]
+        assert h.rank_loads.tolist() == c["rank_loads"], c["name"]
+
+
+def _random_timed_instance(g, R, S):
+    E = int(g.integers(1, R * S + 1))
+    cells = g.permutation(R * S)[:E]
+    slots = np.full(R * S, -1, np.int32)
+    slots[cells] = np.arange(E)
+    slots = slots.reshape(R, S)
+    counts = (g.integers(0, 40, size=E) * (g.random(E) < 0.85)).astype(np.int32)
+    cm = OC.CostModel(g.integers(0, 2, size=R).tolist(), g.integers(0, 400, size=E).tolist(),
+                      (int(g.integers(1, 50)), int(g.integers(1, 200))),
+                      (int(g.integers(100, 2000)), int(g.integers(20, 400))),
+                      int(g.integers(0, 12000)),
+                      None if g.random() < 0.5 else int(g.integers(0, 12000)))
+    return counts, slots, cm
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.integers(1, 6), st.integers(1, 5), st.integers(0, 10 ** 9), st.integers(0, 6),
+       st.sampled_from(["frontier", "full"]), st.integers(0, 3), st.integers(0, 6),
+       st.sampled_from([None, (0, 1), (1, 7), (3, 2)]), st.integers(0, 5))
+def test_timed_host_planner_matches_oracle(R, S, seed, B, mode, cap, tau, gamma, layer):
+    g = np.random.default_rng(seed)
+    counts, slots, cm = _random_timed_instance(g, R, S)
+    ref = OP.plan_swaps(counts, slots, B, gamma=gamma, tau=tau, mode=mode, per_rank_cap=cap,
+                        layer_id=layer, cost=cm)
+    host = fb.plan_swaps_timed(counts, slots, fb.Budget(B, per_rank_cap=cap, tau=tau, gamma=gamma,
+                                                        mode=mode, layer_id=layer),
+                               fb.CostModel(*cm))
+    _same(host, ref)
+    assert host.costs == ref.costs
+
+
+def test_timed_host_planner_argument_checks():
+    lib = fb.lib()
+    c = np.ones(4, np.int32)
+    sl = np.arange(4, dtype=np.int32)
+    nodes = np.zeros(2, np.int32)
+    nb = np.full(4, 10, np.int64)
+    n = ctypes.c_int32(-7)
+    sw = (L.fb_swap * 4)()
+    bg = fb.Budget(4).to_c()
+    good = fb.CostModel([0, 0], [10] * 4, (5, 5), (100, 100), 1000)
+
+    def call(cm=None, nodes_p=nodes.ctypes.data, nb_p=nb.ctypes.data):
+        m = (cm or good).to_c()
+        return lib.fb_plan_swaps_timed(c.ctypes.data, 4, sl.ctypes.data, 2, 2, ctypes.byref(bg),
+                                       ctypes.byref(m), nodes_p, nb_p, ctypes.addressof(sw), None, 4,
+                                       ctypes.addressof(n), None, None, None)
+    assert call() == L.FB_OK
+    assert call(nodes_p=None) == L.FB_EINVAL
+    assert call(nb_p=None) == L.FB_EINVAL
+    assert call(fb.CostModel([0, 0], [10] * 4, (0, 5), (100, 100), 1000)) == L.FB_EINVAL   # alpha 0
+    assert call(fb.CostModel([0, 0], [10] * 4, (5, 5), (100, 0), 1000)) == L.FB_EINVAL     # beta 0
+    assert call(fb.CostModel([0, 0], [10] * 4, (5, 5), (100, 100), -1)) == L.FB_EINVAL     # budget
+    assert call(fb.CostModel([0, 0], [10] * 4, (5, 5), (100, 100), 10, -2)) == L.FB_EINVAL
+    big = np.full(4, 2 ** 41, np.int64)
+    assert call(nb_p=big.ctypes.data) == L.FB_EINVAL
+    assert lib.fb_plan_swaps_timed(c.ctypes.data, 4, sl.ctypes.data, 2, 2, ctypes.byref(bg), None,
+                                   nodes.ctypes.data, nb.ctypes.data, ctypes.addressof(sw), None, 4,
+                                   ctypes.addressof(n), None, None, None) == L.FB_EINVAL
+
+
+def test_timed_device_planner_validation_without_gpu():
+    lib = fb.lib()
+    bg = fb.Budget(2).to_c()
+    cm = fb.CostModel([0, 0], [1] * 4, (5, 5), (100, 100), 1000).to_c()
+    args = [0x1000, 4, 0x2000, 2, 2, ctypes.byref(bg), ctypes.byref(cm), 0x9000, 0xa000, 0x3000,
+            None, 0x4000, 0x5000, 0x6000, 0x7000, 0x8000, None]
+    a = list(args); a[6] = None
+    assert lib.fb_plan_swaps_timed_device(*a) == L.FB_EINVAL
+    a = list(args); a[7] = None
+    assert lib.fb_plan_swaps_timed_device(*a) == L.FB_EINVAL
+    big = fb.Budget(1025).to_c()
+    a = list(args); a[5] = ctypes.byref(big)
+    assert lib.fb_plan_swaps_timed_device(*a) == L.FB_EUNSUPPORTED
+    bad = fb.CostModel([0, 0], [1] * 4, (5, 5), (0, 100), 1000).to_c()
+    a = list(args); a[6] = ctypes.byref(bad)
+    assert lib.fb_plan_swaps_timed_device(*a) == L.FB_EINVAL

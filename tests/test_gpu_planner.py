@@ -136,3 +136,86 @@ def test_predict_then_plan_on_stream():
     s.synchronize()
     host = fb.plan_swaps(out.counts.cpu().numpy(), slots, fb.Budget(wl.budget))
     _same(plan.to_host(), host)
+
+
+# ---- time-budgeted planner (Eq. 9-10, budgets per rank and link) --------------------------------
+
+def _dev_timed(counts, slots, budget, cost):
+    c = torch.from_numpy(np.ascontiguousarray(counts, np.int32)).cuda()
+    s = torch.from_numpy(np.ascontiguousarray(slots, np.int32)).cuda()
+    return fb.plan_swaps_timed_device(c, s, budget, cost).to_host()
+
+
+def test_timed_device_planner_random_instances():
+    print("[plan] timed random instances", flush=True)
+    from oracle.cost import CostModel as OCost
+    g = np.random.default_rng(1)
+    for it in range(120):
+        R = int(g.integers(1, 9))
+        S = int(g.integers(1, 6))
+        E = int(g.integers(1, R * S + 1))
+        cells = g.permutation(R * S)[:E]
+        slots = np.full(R * S, -1, np.int32)
+        slots[cells] = np.arange(E)
+        slots = slots.reshape(R, S)
+        counts = (g.integers(0, 60, size=E) * (g.random(E) < 0.85)).astype(np.int32)
+        cm = OCost(g.integers(0, 2, size=R).tolist(), g.integers(0, 400, size=E).tolist(),
+                   (int(g.integers(1, 50)), int(g.integers(1, 200))),
+                   (int(g.integers(100, 2000)), int(g.integers(20, 400))),
+                   int(g.integers(0, 12000)), None if it % 2 else int(g.integers(0, 12000)))
+        bg = fb.Budget(int(g.integers(0, 7)), per_rank_cap=int(g.integers(0, 3)),
+                       tau=int(g.integers(0, 5)),
+                       gamma=[None, (0, 1), (2, 5)][it % 3], mode=["frontier", "full"][(it // 2) % 2])
+        host = fb.plan_swaps_timed(counts, slots, bg, fb.CostModel(*cm))
+        dev = _dev_timed(counts, slots, bg, fb.CostModel(*cm))
+        _same(dev, host)
+        assert dev.costs == host.costs
+        ref = OP.plan_swaps(counts, slots, bg.max_swaps, gamma=bg.gamma, tau=bg.tau, mode=bg.mode,
+                            per_rank_cap=bg.per_rank_cap, cost=cm)
+        _same(dev, ref)
+        assert dev.costs == ref.costs
+
+
+@pytest.mark.parametrize("mode", ["frontier", "full"])
+def test_timed_device_planner_on_predicted_counts(mode):
+    """DeepSeek-V3-shaped predicted counts, 32 ranks on 4 nodes of 8, 88 MB experts (three
+    7168 x 2048 bf16 matrices), 20 us / 100 GB/s inside a node and 50 us / 25 GB/s across nodes
+    (one intra-node swap costs 1.78 ms, an inter-node one 7.1 ms), per-rank budgets of 2-16 ms.
+    Device = host on every case; the oracle joins in frontier mode (in full mode its exact-rational
+    enumeration of ~30k candidates per round takes minutes; host = oracle there is covered on
+    smaller instances)."""
+    print(f"[plan] timed dsv3 counts {mode}", flush=True)
+    from oracle.cost import CostModel as OCost
+    wl = CONFIGS["dsv3"].with_T(4096)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    li = make_layer(wl, 0)
+    gpu = run_gpu(li, wl, e2r, debug=False)
+    nodes = [r // 8 for r in range(wl.R)]
+    nbytes = [3 * 7168 * 2048 * 2] * wl.E
+    budgets = (2_000_000, 8_000_000, 16_000_000) if mode == "frontier" else (2_000_000, 4_000_000, 8_000_000)
+    for budget_ns in budgets:
+        args = (nodes, nbytes, (20_000, 50_000), (100_000, 25_000), budget_ns)
+        bg = fb.Budget(64, mode=mode, layer_id=5)
+        host = fb.plan_swaps_timed(gpu["counts"], slots, bg, fb.CostModel(*args))
+        dev = _dev_timed(gpu["counts"], slots, bg, fb.CostModel(*args))
+        _same(dev, host)
+        assert dev.costs == host.costs
+        if mode == "frontier":
+            ref = OP.plan_swaps(gpu["counts"], slots, 64, mode=mode, layer_id=5, cost=OCost(*args))
+            _same(host, ref)
+            assert host.costs == ref.costs
+        else:
+            assert len(host.swaps) > 0
+        if host.swaps:
+            assert host.rank_loads.max() < gpu["rank_loads"].max()
+        print(f"[plan]   budget {budget_ns / 1e6:.0f} ms: {len(host.swaps)} swaps", flush=True)
+
+
+def test_timed_device_planner_reports_bad_sizes():
+    print("[plan] timed: expert size out of range", flush=True)
+    slots = torch.tensor([[0, 1], [2, 3]], dtype=torch.int32, device="cuda")
+    c = torch.tensor([9, 1, 1, 1], dtype=torch.int32, device="cuda")
+    cm = fb.CostModel([0, 0], [1, 1, 2 ** 41, 1], (5, 5), (100, 100), 10 ** 6)
+    out = fb.plan_swaps_timed_device(c, slots, fb.Budget(2), cm)
+    torch.cuda.synchronize()
+    assert int(out.status.item()) == -1 and int(out.n_swaps.item()) == 0
