@@ -715,21 +715,19 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     uint32_t last[NT], kth[NT], next[NT];
 #pragma unroll
     for (int u = 0; u < NT; ++u) { last[u] = 0xFFFFFFFFu; kth[u] = 0; next[u] = 0; }
-    // Rounds are branch-free per lane: the popping lane records the expert in slot r, every other
-    // lane writes its own spare slot past kMaxK; a refill runs only when some lane of the wave ran
-    // dry, and lanes that did not insert zeros (which leave a sorted cache unchanged).
-    for (int r = 0; r <= k; ++r) {
+    // k rounds, each popping the token's largest remaining key.  Rounds are branch-free per lane:
+    // the popping lane records the expert in slot r, every other lane writes its own spare slot
+    // past kMaxK; a refill runs only when some lane of the wave ran dry, and lanes that did not
+    // insert zeros (which leave a sorted cache unchanged).
+    for (int r = 0; r < k; ++r) {
       bool dry[NT];
 #pragma unroll
       for (int u = 0; u < NT; ++u) {
         const uint32_t h = c[u][0];
         const uint32_t m = group_max_u32<LPT>(h);
-        if (r >= k - 1) {                      // uniform
-          kth[u] = r == k - 1 ? m : kth[u];
-          next[u] = m;
-        }
+        kth[u] = m;
         const bool mine = m != 0 && h == m;
-        sel[tl[u]][mine && r < k ? r : kMaxK + jl] = (int16_t)(255 - (int)(m & 0xFFu));
+        sel[tl[u]][mine ? r : kMaxK + jl] = (int16_t)(255 - (int)(m & 0xFFu));
 #pragma unroll
         for (int d = 0; d < kCache - 1; ++d) c[u][d] = mine ? c[u][d + 1] : c[u][d];
         c[u][kCache - 1] = mine ? 0u : c[u][kCache - 1];
@@ -745,6 +743,9 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
         }
       }
     }
+    // the (k+1)-th key, for the boundary test below: nothing is popped
+#pragma unroll
+    for (int u = 0; u < NT; ++u) next[u] = group_max_u32<LPT>(c[u][0]);
 #pragma unroll
     for (int u = 0; u < NT; ++u) {
       const uint32_t tb = kth[u] >> 8;         // score bits of the k-th key
