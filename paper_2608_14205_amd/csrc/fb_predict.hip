@@ -56,7 +56,7 @@ constexpr int kMaxGroups = 32;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;    // raw buffer, 32-bit dwords
 constexpr uint32_t kOobOffset = 0x80000000u;    // fails the buffer range check: load returns 0
 #ifndef FB_SEL_CACHE
-#define FB_SEL_CACHE 5
+#define FB_SEL_CACHE 7
 #endif
 constexpr int kCache = FB_SEL_CACHE;            // per-lane cached keys in the top-k extraction
 
@@ -211,8 +211,26 @@ __device__ __forceinline__ void top2_group(float& m1, float& m2, int g) {
 // 32 jl + 31; lanes at or past E hold no group).  Values of the other lanes of the aligned
 // G-lane group come in by lane exchange: lanes jl ^ 1..3 through quad permutations, lanes
 // jl ^ 4..7 through the half-row mirror (lane jl ^ 7) followed by the same permutations.
+// Which lanes jl ^ x lead a group (lead[x]) and whose group comes before this lane's (lower[x]) does
+// not depend on the token: computed once, as 0/1 integers kept in vector registers, so the rank is
+// plain compare-and-select arithmetic with no branches.
 template <int G>
-__device__ __forceinline__ int group_rank(float g, int jl, int lpg, int E) {
+struct RankLanes { int lead[G], lower[G]; };
+template <int G>
+__device__ __forceinline__ RankLanes<G> rank_lanes(int jl, int lpg, int E) {
+  RankLanes<G> r;
+  const int me = jl / lpg;
+#pragma unroll
+  for (int x = 0; x < G; ++x) {
+    const int j = jl ^ x;
+    r.lead[x] = (x != 0 && (j % lpg) == 0 && j * 32 < E) ? 1 : 0;
+    r.lower[x] = (j / lpg < me) ? 1 : 0;
+    asm volatile("" : "+v"(r.lead[x]), "+v"(r.lower[x]));
+  }
+  return r;
+}
+template <int G>
+__device__ __forceinline__ int group_rank(float g, const RankLanes<G>& rl) {
   float v[8];
   v[0] = g;
   if constexpr (G >= 2) v[1] = dpp_f32<kXor1>(g);
@@ -221,14 +239,12 @@ __device__ __forceinline__ int group_rank(float g, int jl, int lpg, int E) {
     const float m = dpp_f32<kHalfMirror>(g);   // lane jl ^ 7
     v[7] = m; v[6] = dpp_f32<kXor1>(m); v[5] = dpp_f32<kXor2>(m); v[4] = dpp_f32<kXor3>(m);
   }
-  const int me = jl / lpg;
   int rank = 0;
 #pragma unroll
   for (int x = 1; x < G; ++x) {
-    const int j = jl ^ x;
-    const bool counts = (j % lpg) == 0 && j * 32 < E;
     const float o = v[x];
-    rank += counts && (o > g || (o == g && j / lpg < me));
+    const int gt = o > g ? 1 : 0, eq = o == g ? 1 : 0;
+    rank += rl.lead[x] & (gt | (eq & rl.lower[x]));
   }
   return rank;
 }
@@ -580,6 +596,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   uint32_t idxb[32];                         // key index bits of each element
 #pragma unroll
   for (int i = 0; i < 32; ++i) idxb[i] = (uint32_t)(idx_base - local_of(i));
+  const RankLanes<LPT> rlanes = rank_lanes<LPT>(jl, gsz >= 32 ? gsz >> 5 : 1, E);
   // each pass's scores are read while the previous pass is processed
   float snext[NT][32];
 #pragma unroll
@@ -629,7 +646,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
           float m1 = from_ord_bits(k1), m2 = from_ord_bits(k2);
           if (lpg > 1) top2_group(m1, m2, lpg);
           const float g = p.group_topn == 2 ? m1 + m2 : m1;
-          const int rank = group_rank<LPT>(g, jl, lpg, E);
+          const int rank = group_rank<LPT>(g, rlanes);
           keep[u] = (real && rank < p.topk_group) ? 0xFFFFFFFFu : 0u;
         }
       } else {
@@ -726,7 +743,9 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
         const uint32_t h = c[u][0];
         const uint32_t m = group_max_u32<LPT>(h);
         kth[u] = m;
-        const bool mine = m != 0 && h == m;
+        // m is never 0 here: every lane holds 32 keys and only experts >= 255 can have key 0, so
+        // each of the first k <= 32 maxima is a real key with exactly one owner
+        const bool mine = h == m;
         sel[tl[u]][mine ? r : kMaxK + jl] = (int16_t)(255 - (int)(m & 0xFFu));
 #pragma unroll
         for (int d = 0; d < kCache - 1; ++d) c[u][d] = mine ? c[u][d + 1] : c[u][d];
