@@ -33,6 +33,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "fb_internal.h"
 
 namespace fb {
@@ -546,27 +548,42 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
           }
         }
     }
-    const bool sig = p.kind == FB_SIGMOID;
+    // The common case (sigmoid, no logit bias) is its own instantiation: the exponential and
+    // the reciprocal dominate this phase, and it then needs only three other operations per
+    // score.  A sigmoid score is never -0 (the reciprocal is positive, and +0 + -0 = +0), so only
+    // the logits need the -0 -> +0 canonicalisation of the order-preserving key.
+    auto emit = [&](auto sig_c, auto lbias_c) {
+      constexpr bool SIG = decltype(sig_c)::value, LBIAS = decltype(lbias_c)::value;
 #pragma unroll
-    for (int fe = 0; fe < FE; ++fe) {
+      for (int fe = 0; fe < FE; ++fe) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int e0 = we * EW + fe * 32 + g * 8 + (lane >> 5) * 4;
-        const f32x4 lb = *reinterpret_cast<const f32x4*>(s_lbias + e0);
-        const f32x4 sb = *reinterpret_cast<const f32x4*>(s_sbias + e0);
+        for (int g = 0; g < 4; ++g) {
+          const int e0 = we * EW + fe * 32 + g * 8 + (lane >> 5) * 4;
+          const f32x4 lb = *reinterpret_cast<const f32x4*>(s_lbias + e0);
+          const f32x4 sb = *reinterpret_cast<const f32x4*>(s_sbias + e0);
 #pragma unroll
-        for (int ft = 0; ft < FT; ++ft) {
-          const int tl = wt * TW + ft * 32 + (lane & 31);
-          f32x4 sv;
+          for (int ft = 0; ft < FT; ++ft) {
+            const int tl = wt * TW + ft * 32 + (lane & 31);
+            f32x4 sv;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float z = acc[fe][ft][g * 4 + r] + lb[r];
-            const float sc = sig ? __builtin_amdgcn_rcpf(1.0f + __expf(-z)) + sb[r] : z;
-            sv[r] = sc + 0.0f;                   // -0 -> +0; padding experts stay -inf
+            for (int r = 0; r < 4; ++r) {
+              const float z = LBIAS ? acc[fe][ft][g * 4 + r] + lb[r] : acc[fe][ft][g * 4 + r];
+              if constexpr (SIG)
+                sv[r] = __builtin_amdgcn_rcpf(1.0f + __expf(-z)) + sb[r];
+              else
+                sv[r] = z + 0.0f;                // -0 -> +0; padding experts stay -inf
+            }
+            *reinterpret_cast<f32x4*>(S + tl * SROW + e0) = sv;
           }
-          *reinterpret_cast<f32x4*>(S + tl * SROW + e0) = sv;
         }
       }
+    };
+    using T1 = std::integral_constant<bool, true>;
+    using F0 = std::integral_constant<bool, false>;
+    if (p.kind == FB_SIGMOID) {
+      if (p.logit_bias) emit(T1{}, T1{}); else emit(T1{}, F0{});
+    } else {
+      emit(F0{}, T1{});
     }
   }
   lds_barrier();
