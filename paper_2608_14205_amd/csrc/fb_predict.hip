@@ -494,6 +494,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   __shared__ __attribute__((aligned(16))) float s_sbias[EPAD];   // selection bias (-inf past E)
   // selected experts per token (ids < 256), with spare slots kMaxK .. kMaxK + LPT - 1
   __shared__ int16_t sel[BM][kMaxK + LPT];
+  __shared__ uint8_t kmask[BM];                 // kept lanes of each token (second phase)
   __shared__ __attribute__((aligned(16))) float gsc[GSC_TOK][kMaxGroups];
   __shared__ int32_t s_flag;
   __shared__ int64_t s_red[kWaves][2];
@@ -614,6 +615,112 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
   for (int i = 0; i < 32; ++i) idxb[i] = (uint32_t)(idx_base - local_of(i));
   const RankLanes<LPT> rlanes = rank_lanes<LPT>(jl, gsz >= 32 ? gsz >> 5 : 1, E);
+  // Second phase for group-limited routing where the kept groups fill exactly half of a token's
+  // lanes (as with 8 groups of 32 keeping 4): the extraction then runs on half the lanes.
+  const bool compact = NPASS % 2 == 0 && BM % TPASS == 0 && LPT >= 2 && ng > 1 && gsz >= 32 &&
+                       p.topk_group * (gsz >> 5) * 2 == LPT;
+  // ---- finishing a token: per-lane key caches, k extraction rounds, boundary ties, histogram --
+  // G lanes per token; lane jg holds 32 keys; element i of the lane is expert
+  // 32 L + 4 ((i / 4 + L) mod 8) + i mod 4 (L = the lane's 32-expert slice).
+  auto finish = [&](auto g_c, int jg, int tlu, bool tv, int64_t ttu, const uint32_t(&key)[32],
+                    const float(&sv)[32], int L) {
+    constexpr int G = decltype(g_c)::value;
+    // per-lane cache of the kCache largest keys (descending), refilled by a rescan below the last
+    // popped key when it runs dry
+    uint32_t c[kCache];
+#pragma unroll
+    for (int d = 0; d < kCache; ++d) c[d] = 0;
+    auto insert = [&](uint32_t v) {
+#pragma unroll
+      for (int d = kCache - 1; d >= 1; --d) c[d] = umed3(c[d - 1], c[d], v);
+      c[0] = max(c[0], v);
+    };
+#pragma unroll
+    for (int i = 0; i < 32; ++i) insert(key[i]);
+    uint32_t last = 0xFFFFFFFFu, kth = 0, next = 0;
+    // k rounds, each popping the token's largest remaining key.  Rounds are branch-free per lane:
+    // the popping lane records the expert in slot r, every other lane writes its own spare slot
+    // past kMaxK; a refill runs only when some lane of the wave ran dry, and lanes that did not
+    // insert zeros (which leave a sorted cache unchanged).
+    for (int r = 0; r < k; ++r) {
+      const uint32_t h = c[0];
+      const uint32_t m = group_max_u32<G>(h);
+      kth = m;
+      // m is never 0 here: every lane holds 32 keys and only experts >= 255 can have key 0, so
+      // each of the first k <= 32 maxima is a real key with exactly one owner
+      const bool mine = h == m;
+      sel[tlu][mine ? r : kMaxK + jg] = (int16_t)(255 - (int)(m & 0xFFu));
+#pragma unroll
+      for (int d = 0; d < kCache - 1; ++d) c[d] = mine ? c[d + 1] : c[d];
+      c[kCache - 1] = mine ? 0u : c[kCache - 1];
+      last = mine ? m : last;
+      // refill below last; a lane with nothing left below it inserts only zeros
+      const bool dry = mine && c[0] == 0;
+      if (__builtin_amdgcn_ballot_w64(dry) != 0) {   // rare
+#pragma unroll
+        for (int i = 0; i < 32; ++i) insert(dry && key[i] < last ? key[i] : 0u);
+      }
+    }
+    // the (k+1)-th key, for the boundary test below: nothing is popped
+    next = group_max_u32<G>(c[0]);
+    const uint32_t tb = kth >> 8;              // score bits of the k-th key
+    const bool tie = tv && (next >> 8) != 0 && (next >> 8) == tb;
+    if (tie) {
+      // Exact path for the boundary only.  Every key whose score bits exceed tb is selected and
+      // already in place (the keys were popped in descending order); the remaining slots go to
+      // the experts whose score bits equal tb, ranked by the full 64-bit key (all score bits,
+      // then the inverted index), which is the exact order.
+      int above = 0;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) above += (key[i] >> 8) > tb;
+#pragma unroll
+      for (int off = 1; off < G; off <<= 1) above += __shfl_xor(above, off, G);
+      uint64_t lastk = ~0ull;
+      for (int r = above; r < k; ++r) {
+        uint64_t best = 0;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) {
+          const uint32_t e = (uint32_t)(L * 32 + (((((i >> 2) + L) & 7) << 2) | (i & 3)));
+          const uint64_t kk = ((uint64_t)ord_bits(sv[i] + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - e);
+          const bool ok = (key[i] >> 8) == tb && kk < lastk && kk > best;
+          best = ok ? kk : best;
+        }
+#pragma unroll
+        for (int off = 1; off < G; off <<= 1) {
+          const uint64_t o = __shfl_xor(best, off, G);
+          best = o > best ? o : best;
+        }
+        if (best == 0) break;                  // cannot happen: at least two keys share tb
+        lastk = best;
+        if (jg == 0) sel[tlu][r] = (int16_t)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFu));
+      }
+    }
+    wave_lds_sync();
+    if (tv) {
+      for (int r = jg; r < k; r += G) {
+        const int e = sel[tlu][r];
+        if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
+      }
+    }
+    if (p.topk_idx && jg == 0 && tv) {
+      // debug output in exact descending score order: insertion sort of the k selected in place
+      int16_t* list = sel[tlu];
+      for (int r = 1; r < k; ++r) {
+        const int e = list[r];
+        const float se = (unsigned)e < (unsigned)E ? S[tlu * SROW + e] : -__builtin_inff();
+        int q = r;
+        while (q > 0) {
+          const int eo = list[q - 1];
+          const float so = (unsigned)eo < (unsigned)E ? S[tlu * SROW + eo] : -__builtin_inff();
+          if (so > se || (so == se && eo < e)) break;
+          list[q] = (int16_t)eo;
+          --q;
+        }
+        list[q] = (int16_t)e;
+      }
+      for (int r = 0; r < k; ++r) p.topk_idx[ttu * k + r] = list[r];
+    }
+  };
   // each pass's scores are read while the previous pass is processed
   float snext[NT][32];
 #pragma unroll
@@ -715,135 +822,63 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     // 32-bit keys: the top 24 bits of the order-preserving score encoding, then 255 - expert.
     // Experts outside the kept groups (and every expert of a token past T) keep only their index
     // bits, which ranks them below every selectable expert; padding experts score -inf.
-    uint32_t key[NT][32];
+    if (compact) {
+      // Only the kept groups matter from here on, and they fill exactly half of the token's lanes:
+      // record which lanes they are and finish the token in the second phase below, two tokens
+      // per lane group.
+      const uint64_t b = __builtin_amdgcn_ballot_w64(keep[0] != 0);
+      if (jl == 0) kmask[tl[0]] = (uint8_t)((b >> (lane & (64 - LPT))) & ((1u << LPT) - 1u));
+      continue;
+    }
+    uint32_t key[32];
+    if (ng == 1 || gsz >= 32) {                // the lane's experts are kept or dropped together
+      const uint32_t m = tvalid[0] && keep[0] ? 0xFFFFFF00u : 0u;
 #pragma unroll
-    for (int u = 0; u < NT; ++u) {
-      if (ng == 1 || gsz >= 32) {              // the lane's experts are kept or dropped together
-        const uint32_t m = tvalid[u] && keep[u] ? 0xFFFFFF00u : 0u;
+      for (int i = 0; i < 32; ++i) key[i] = (ob[0][i] & m) | idxb[i];
+    } else {
 #pragma unroll
-        for (int i = 0; i < 32; ++i) key[u][i] = (ob[u][i] & m) | idxb[i];
-      } else {
-#pragma unroll
-        for (int i = 0; i < 32; ++i) {
-          const uint32_t m = tvalid[u] && ((keep[u] >> i) & 1u) ? 0xFFFFFF00u : 0u;
-          key[u][i] = (ob[u][i] & m) | idxb[i];
-        }
+      for (int i = 0; i < 32; ++i) {
+        const uint32_t m = tvalid[0] && ((keep[0] >> i) & 1u) ? 0xFFFFFF00u : 0u;
+        key[i] = (ob[0][i] & m) | idxb[i];
       }
     }
-    // per-lane cache of the kCache largest keys (descending), refilled by a rescan below the last
-    // popped key when it runs dry
-    uint32_t c[NT][kCache];
-#pragma unroll
-    for (int u = 0; u < NT; ++u)
-#pragma unroll
-      for (int d = 0; d < kCache; ++d) c[u][d] = 0;
-    auto insert = [&](int u, uint32_t v) {
-#pragma unroll
-      for (int d = kCache - 1; d >= 1; --d) c[u][d] = umed3(c[u][d - 1], c[u][d], v);
-      c[u][0] = max(c[u][0], v);
-    };
-#pragma unroll
-    for (int i = 0; i < 32; ++i)
-#pragma unroll
-      for (int u = 0; u < NT; ++u) insert(u, key[u][i]);
-    uint32_t last[NT], kth[NT], next[NT];
-#pragma unroll
-    for (int u = 0; u < NT; ++u) { last[u] = 0xFFFFFFFFu; kth[u] = 0; next[u] = 0; }
-    // k rounds, each popping the token's largest remaining key.  Rounds are branch-free per lane:
-    // the popping lane records the expert in slot r, every other lane writes its own spare slot
-    // past kMaxK; a refill runs only when some lane of the wave ran dry, and lanes that did not
-    // insert zeros (which leave a sorted cache unchanged).
-    for (int r = 0; r < k; ++r) {
-      bool dry[NT];
-#pragma unroll
-      for (int u = 0; u < NT; ++u) {
-        const uint32_t h = c[u][0];
-        const uint32_t m = group_max_u32<LPT>(h);
-        kth[u] = m;
-        // m is never 0 here: every lane holds 32 keys and only experts >= 255 can have key 0, so
-        // each of the first k <= 32 maxima is a real key with exactly one owner
-        const bool mine = h == m;
-        sel[tl[u]][mine ? r : kMaxK + jl] = (int16_t)(255 - (int)(m & 0xFFu));
-#pragma unroll
-        for (int d = 0; d < kCache - 1; ++d) c[u][d] = mine ? c[u][d + 1] : c[u][d];
-        c[u][kCache - 1] = mine ? 0u : c[u][kCache - 1];
-        last[u] = mine ? m : last[u];
-        // refill below last[u]; a lane with nothing left below it inserts only zeros
-        dry[u] = mine && c[u][0] == 0;
-      }
-#pragma unroll
-      for (int u = 0; u < NT; ++u) {           // each token refills on its own (rare)
-        if (__builtin_amdgcn_ballot_w64(dry[u]) != 0) {
-#pragma unroll
-          for (int i = 0; i < 32; ++i) insert(u, dry[u] && key[u][i] < last[u] ? key[u][i] : 0u);
-        }
-      }
-    }
-    // the (k+1)-th key, for the boundary test below: nothing is popped
-#pragma unroll
-    for (int u = 0; u < NT; ++u) next[u] = group_max_u32<LPT>(c[u][0]);
-#pragma unroll
-    for (int u = 0; u < NT; ++u) {
-      const uint32_t tb = kth[u] >> 8;         // score bits of the k-th key
-      const bool tie = tvalid[u] && (next[u] >> 8) != 0 && (next[u] >> 8) == tb;
-      if (tie) {
-        // Exact path for the boundary only.  Every key whose score bits exceed tb is selected and
-        // already in place (the keys were popped in descending order); the remaining slots go to
-        // the experts whose score bits equal tb, ranked by the full 64-bit key (all score bits,
-        // then the inverted index), which is the exact order.
-        int above = 0;
-#pragma unroll
-        for (int i = 0; i < 32; ++i) above += (key[u][i] >> 8) > tb;
-#pragma unroll
-        for (int off = 1; off < LPT; off <<= 1) above += __shfl_xor(above, off, LPT);
-        uint64_t lastk = ~0ull;
-        for (int r = above; r < k; ++r) {
-          uint64_t best = 0;
-#pragma unroll
-          for (int i = 0; i < 32; ++i) {
-            const uint32_t e = (uint32_t)(jl * 32 + local_of(i));
-            const uint64_t kk = ((uint64_t)ord_bits(s[u][i] + 0.0f) << 32) | (uint64_t)(0xFFFFFFFFu - e);
-            const bool ok = (key[u][i] >> 8) == tb && kk < lastk && kk > best;
-            best = ok ? kk : best;
-          }
-#pragma unroll
-          for (int off = 1; off < LPT; off <<= 1) {
-            const uint64_t o = __shfl_xor(best, off, LPT);
-            best = o > best ? o : best;
-          }
-          if (best == 0) break;                // cannot happen: at least two keys share tb
-          lastk = best;
-          if (jl == 0) sel[tl[u]][r] = (int16_t)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFu));
-        }
-      }
-    }
+    finish(std::integral_constant<int, LPT>{}, jl, tl[0], tvalid[0], tt[0], key, s[0], jl);
+  }
+  if (compact) {
+    // Second phase: the lane group of a token slot takes two tokens of this wave, half of its
+    // lanes each; lane jb of a half reads the jb-th kept group's 32 scores back from the tile.
+    constexpr int G2 = LPT / 2;
     wave_lds_sync();
+    const int half = jl / G2, jb = jl % G2;
+#pragma unroll 1
+    for (int pb = 0; pb < NPASS / 2; ++pb) {
+      const int tlc = (2 * pb + half) * TPASS + gslot;
+      const int64_t ttc = row0 + tlc;
+      const bool tvc = ttc < p.T;
+      // the jb-th set bit of the token's kept-lane mask
+      const uint32_t km = kmask[tlc];
+      int L = 0, seen = 0;
 #pragma unroll
-    for (int u = 0; u < NT; ++u) {
-      if (tvalid[u]) {
-        for (int r = jl; r < k; r += LPT) {
-          const int e = sel[tl[u]][r];
-          if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
-        }
+      for (int b = 0; b < LPT; ++b) {
+        const int on = (km >> b) & 1;
+        L = (on && seen == jb) ? b : L;
+        seen += on;
       }
-      if (p.topk_idx && jl == 0 && tvalid[u]) {
-        // debug output in exact descending score order: insertion sort of the k selected in place
-        int16_t* list = sel[tl[u]];
-        for (int r = 1; r < k; ++r) {
-          const int e = list[r];
-          const float se = (unsigned)e < (unsigned)E ? S[tl[u] * SROW + e] : -__builtin_inff();
-          int q = r;
-          while (q > 0) {
-            const int eo = list[q - 1];
-            const float so = (unsigned)eo < (unsigned)E ? S[tl[u] * SROW + eo] : -__builtin_inff();
-            if (so > se || (so == se && eo < e)) break;
-            list[q] = (int16_t)eo;
-            --q;
-          }
-          list[q] = (int16_t)e;
-        }
-        for (int r = 0; r < k; ++r) p.topk_idx[tt[u] * k + r] = list[r];
+      float sc[32];
+      const float* row = S + tlc * SROW + L * 32;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(row + ((q + L) & 7) * 4);
+        sc[q * 4 + 0] = v[0]; sc[q * 4 + 1] = v[1]; sc[q * 4 + 2] = v[2]; sc[q * 4 + 3] = v[3];
       }
+      const uint32_t m = tvc ? 0xFFFFFF00u : 0u;
+      uint32_t key[32];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const int loc = ((((i >> 2) + L) & 7) << 2) | (i & 3);
+        key[i] = (ord_bits(sc[i]) & m) | (uint32_t)(255 - (L * 32 + loc));
+      }
+      finish(std::integral_constant<int, G2>{}, jb, tlc, tvc, ttc, key, sc, L);
     }
   }
   lds_barrier();
