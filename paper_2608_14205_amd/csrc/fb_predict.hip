@@ -495,6 +495,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   // selected experts per token (ids < 256), with spare slots kMaxK .. kMaxK + LPT - 1
   __shared__ int16_t sel[BM][kMaxK + LPT];
   __shared__ uint8_t kmask[BM];                 // kept lanes of each token (second phase)
+  __shared__ __attribute__((aligned(16))) float grp[BM][8];   // group scores (8 groups of 32)
   __shared__ __attribute__((aligned(16))) float gsc[GSC_TOK][kMaxGroups];
   __shared__ int32_t s_flag;
   __shared__ int64_t s_red[kWaves][2];
@@ -527,6 +528,17 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   if (row0 < p.T) contract<BF16, EPAD, FE, FT, NS, BM, TW>(acc, p, row0, wave, we, wt, lane, smem);
   lds_barrier();
 
+  // Group-limited routing where the kept groups fill exactly half of a token's lanes (as with 8
+  // groups of 32 keeping 4) finishes in a second selection phase on half the lanes (compact).
+  // With exactly 8 groups of 32 the group scores come straight from the score computation
+  // (early): each 32-expert block of a wave is one group, split over lanes l and l + 32.
+  const int ng = p.n_group;
+  const int gsz = E / ng;
+  const bool compact = NPASS % 2 == 0 && BM % TPASS == 0 && LPT >= 2 && ng > 1 && gsz >= 32 &&
+                       p.topk_group * (gsz >> 5) * 2 == LPT;
+  const bool early = compact && LPT == 8 && gsz == 32 && ng == 8 && p.kind == FB_SIGMOID &&
+                     p.logit_bias == nullptr;
+
   // ---- logits and scores into an LDS tile S[token][expert] ------------------------
   // Lane l of a 32 x 32 block holds token (l & 31) and experts g * 8 + (l >> 5) * 4 + r in
   // register g * 4 + r.
@@ -553,8 +565,15 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     // the reciprocal dominate this phase, and it then needs only three other operations per
     // score.  A sigmoid score is never -0 (the reciprocal is positive, and +0 + -0 = +0), so only
     // the logits need the -0 -> +0 canonicalisation of the order-preserving key.
-    auto emit = [&](auto sig_c, auto lbias_c) {
+    auto emit = [&](auto sig_c, auto lbias_c, auto groups_c) {
       constexpr bool SIG = decltype(sig_c)::value, LBIAS = decltype(lbias_c)::value;
+      constexpr bool GROUPS = decltype(groups_c)::value;
+      // top two scores of each (expert block, token block) over this lane's 16 of its 32 experts
+      float t1[FE][FT], t2[FE][FT];
+#pragma unroll
+      for (int fe = 0; fe < FE; ++fe)
+#pragma unroll
+        for (int ft = 0; ft < FT; ++ft) { t1[fe][ft] = -__builtin_inff(); t2[fe][ft] = -__builtin_inff(); }
 #pragma unroll
       for (int fe = 0; fe < FE; ++fe) {
 #pragma unroll
@@ -573,18 +592,37 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
                 sv[r] = __builtin_amdgcn_rcpf(1.0f + __expf(-z)) + sb[r];
               else
                 sv[r] = z + 0.0f;                // -0 -> +0; padding experts stay -inf
+              if constexpr (GROUPS) {
+                t2[fe][ft] = __builtin_amdgcn_fmed3f(t1[fe][ft], t2[fe][ft], sv[r]);
+                t1[fe][ft] = fmaxf(t1[fe][ft], sv[r]);
+              }
             }
             *reinterpret_cast<f32x4*>(S + tl * SROW + e0) = sv;
           }
         }
       }
+      if constexpr (GROUPS) {
+        // merge with the lane holding the block's other 16 experts of the same token
+#pragma unroll
+        for (int fe = 0; fe < FE; ++fe)
+#pragma unroll
+          for (int ft = 0; ft < FT; ++ft) {
+            const float o1 = __shfl_xor(t1[fe][ft], 32), o2 = __shfl_xor(t2[fe][ft], 32);
+            const float m1 = fmaxf(t1[fe][ft], o1);
+            const float m2 = fmaxf(fminf(t1[fe][ft], o1), fmaxf(t2[fe][ft], o2));
+            if (lane < 32)
+              grp[wt * TW + ft * 32 + lane][we * FE + fe] = p.group_topn == 2 ? m1 + m2 : m1;
+          }
+      }
     };
     using T1 = std::integral_constant<bool, true>;
     using F0 = std::integral_constant<bool, false>;
     if (p.kind == FB_SIGMOID) {
-      if (p.logit_bias) emit(T1{}, T1{}); else emit(T1{}, F0{});
+      if (p.logit_bias) emit(T1{}, T1{}, F0{});
+      else if (early) emit(T1{}, F0{}, T1{});
+      else emit(T1{}, F0{}, F0{});
     } else {
-      emit(F0{}, T1{});
+      emit(F0{}, T1{}, F0{});
     }
   }
   lds_barrier();
@@ -598,8 +636,6 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   const int k = p.k;
   const int jl = tid % LPT;      // lane within the token group
   const int gslot = tid / LPT;   // token slot within a pass
-  const int ng = p.n_group;
-  const int gsz = E / ng;
   const int gshift = __builtin_ctz((unsigned)gsz);   // group sizes below 32 are powers of two
   auto local_of = [&](int i) { return ((((i >> 2) + jl) & 7) << 2) | (i & 3); };  // expert - 32 jl
   const int idx_base = 255 - jl * 32;        // key index bits of element i: idx_base - local_of(i)
@@ -615,10 +651,6 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
   for (int i = 0; i < 32; ++i) idxb[i] = (uint32_t)(idx_base - local_of(i));
   const RankLanes<LPT> rlanes = rank_lanes<LPT>(jl, gsz >= 32 ? gsz >> 5 : 1, E);
-  // Second phase for group-limited routing where the kept groups fill exactly half of a token's
-  // lanes (as with 8 groups of 32 keeping 4): the extraction then runs on half the lanes.
-  const bool compact = NPASS % 2 == 0 && BM % TPASS == 0 && LPT >= 2 && ng > 1 && gsz >= 32 &&
-                       p.topk_group * (gsz >> 5) * 2 == LPT;
   // ---- finishing a token: per-lane key caches, k extraction rounds, boundary ties, histogram --
   // G lanes per token; lane jg holds 32 keys; element i of the lane is expert
   // 32 L + 4 ((i / 4 + L) mod 8) + i mod 4 (L = the lane's 32-expert slice).
@@ -723,6 +755,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   };
   // each pass's scores are read while the previous pass is processed
   float snext[NT][32];
+  if (!early) {
 #pragma unroll
   for (int u = 0; u < NT; ++u)
     if (u * TPP + gslot < BM) read_scores(snext[u], u * TPP + gslot);
@@ -844,6 +877,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     }
     finish(std::integral_constant<int, LPT>{}, jl, tl[0], tvalid[0], tt[0], key, s[0], jl);
   }
+  }
   if (compact) {
     // Second phase: the lane group of a token slot takes two tokens of this wave, half of its
     // lanes each; lane jb of a half reads the jb-th kept group's 32 scores back from the tile.
@@ -856,7 +890,30 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       const int64_t ttc = row0 + tlc;
       const bool tvc = ttc < p.T;
       // the jb-th set bit of the token's kept-lane mask
-      const uint32_t km = kmask[tlc];
+      uint32_t km;
+      if (early) {
+        // rank groups jb and jb + 4 of the token's 8 (score desc, lower group first), then
+        // gather the kept set over the half's four lanes
+        const f32x4 ga = *reinterpret_cast<const f32x4*>(&grp[tlc][0]);
+        const f32x4 gb = *reinterpret_cast<const f32x4*>(&grp[tlc][4]);
+        const float gv[8] = {ga[0], ga[1], ga[2], ga[3], gb[0], gb[1], gb[2], gb[3]};
+        uint32_t kb = 0;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int gi = jb + 4 * h;
+          const float mine = h ? gv[jb + 4] : gv[jb];
+          int rank = 0;
+#pragma unroll
+          for (int x = 0; x < 8; ++x)
+            rank += (int)(gv[x] > mine) | ((int)(gv[x] == mine) & (int)(x < gi));
+          kb |= (uint32_t)(rank < p.topk_group) << gi;
+        }
+        kb |= (uint32_t)__shfl_xor((int)kb, 1, G2);
+        kb |= (uint32_t)__shfl_xor((int)kb, 2, G2);
+        km = kb;
+      } else {
+        km = kmask[tlc];
+      }
       int L = 0, seen = 0;
 #pragma unroll
       for (int b = 0; b < LPT; ++b) {
