@@ -602,12 +602,16 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
         }
       }
       if constexpr (GROUPS) {
-        // merge with the lane holding the block's other 16 experts of the same token
+        // merge with lane l + 32, which holds the block's other 16 experts of the same token: the
+        // lane-half swap hands lanes 0..31 the values of lanes 32..63 (the upper half's result is
+        // not used)
 #pragma unroll
         for (int fe = 0; fe < FE; ++fe)
 #pragma unroll
           for (int ft = 0; ft < FT; ++ft) {
-            const float o1 = __shfl_xor(t1[fe][ft], 32), o2 = __shfl_xor(t2[fe][ft], 32);
+            const uint32_t u1 = __float_as_uint(t1[fe][ft]), u2 = __float_as_uint(t2[fe][ft]);
+            const float o1 = __uint_as_float(__builtin_amdgcn_permlane32_swap(u1, u1, false, false)[1]);
+            const float o2 = __uint_as_float(__builtin_amdgcn_permlane32_swap(u2, u2, false, false)[1]);
             const float m1 = fmaxf(t1[fe][ft], o1);
             const float m2 = fmaxf(fminf(t1[fe][ft], o1), fmaxf(t2[fe][ft], o2));
             if (lane < 32)
