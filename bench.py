@@ -87,6 +87,71 @@ def cpu_baseline(wl, li, e2r, slots, target_s: float):
                       f"the frontier planner (B={wl.budget}); {dt:.1f} s"}
 
 
+def _time_ms(torch, stream, fn, K):
+    """Average duration of K back-to-back calls of fn, bracketed by events on the stream."""
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    fn(0)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for i in range(K):
+        fn(i)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / K
+
+
+def measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t, slots_t, sb, pred,
+                   out, stream):
+    """The rest of the hot path's entry points on the same workload, each timed back to back:
+    the predict -> plan step replayed from a HIP graph, the prediction-quality diagnostics (row
+    cosine of two hidden-state batches, top-k hits, rank fold) and the time-budgeted planner."""
+    K = max(10, args.steps // 4)
+    res = {}
+    # predict -> plan captured once per hidden-state buffer, replayed in rotation
+    try:
+        side = torch.cuda.Stream()
+        plan_g = fb.plan_swaps_device(out.counts, slots_t, budget)
+        graphs = []
+        with torch.cuda.stream(side):
+            for i in range(nbuf):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=side):
+                    pred.predict_load(xs[i], wp, scoring, e2r_t, wl.R, select_bias=sb, out=out)
+                    fb.plan_swaps_device(out.counts, slots_t, budget, out=plan_g)
+                graphs.append(g)
+        torch.cuda.synchronize()
+        res["graph_ms_per_step"] = _time_ms(torch, stream, lambda i: graphs[i % nbuf].replay(), K)
+    except Exception as ex:  # graph capture is context, never a reason to lose the bench line
+        res["graph_ms_per_step"] = None
+        res["graph_error"] = str(ex)[:200]
+    # mean row cosine of two T x H bf16 batches: reads both once (the hidden-state cosine of the
+    # prediction-quality study), HBM-bound
+    a_, b_ = xs[0], xs[1 % nbuf]
+    cos_ms = _time_ms(torch, stream, lambda i: fb.row_cosine_mean(a_, b_), K)
+    nbytes = 2 * a_.numel() * a_.element_size()
+    res["row_cosine_mean"] = {"ms": cos_ms, "bytes": nbytes, "achieved_gbs": nbytes / cos_ms / 1e6,
+                              "frac_of_hbm_peak": nbytes / cos_ms / 1e6 / PEAK_HBM_GBS}
+    # top-k hits between two T x k selections, and the rank fold of a count vector
+    dbg = pred.predict_load(xs[0], wp, scoring, e2r_t, wl.R, select_bias=sb, return_topk=True)
+    dbg2 = pred.predict_load(xs[1 % nbuf], wp, scoring, e2r_t, wl.R, select_bias=sb, return_topk=True)
+    res["topk_hits_ms"] = _time_ms(torch, stream, lambda i: fb.topk_hits(dbg.topk, dbg2.topk), K)
+    res["fold_rank_loads_ms"] = _time_ms(torch, stream,
+                                         lambda i: fb.fold_rank_loads(out.counts, e2r_t, wl.R), K)
+    # time-budgeted planner: 32 ranks on 4 nodes of 8, 88 MB experts (three 7168 x 2048 bf16
+    # matrices), 20 us / 100 GB/s inside a node, 50 us / 25 GB/s across, 8 ms per rank
+    nodes_t = torch.tensor([r // 8 for r in range(wl.R)], dtype=torch.int32, device=out.counts.device)
+    sizes_t = torch.full((wl.E,), 3 * 7168 * 2048 * 2, dtype=torch.int64, device=out.counts.device)
+    cm = fb.CostModel(nodes_t, sizes_t, (20_000, 50_000), (100_000, 25_000), 8_000_000)
+    for mode in ("frontier", "full"):
+        bg_t = fb.Budget(64, mode=mode)
+        tplan = fb.plan_swaps_timed_device(out.counts, slots_t, bg_t, cm)
+        res[f"plan_timed_{mode}_ms"] = _time_ms(
+            torch, stream, lambda i: fb.plan_swaps_timed_device(out.counts, slots_t, bg_t, cm, out=tplan), K)
+        res[f"plan_timed_{mode}_swaps"] = len(tplan.to_host().swaps)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -188,6 +253,8 @@ def main():
 
     counts = out.counts.cpu().numpy()
     host_plan = plan.to_host()
+    extras = measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t, slots_t, sb,
+                            pred, out, stream)
 
     # the same step with fb_predict_load, which repacks the router weight on every call
     u_start = torch.cuda.Event(enable_timing=True)
@@ -235,6 +302,7 @@ def main():
                     "what": "torch.matmul(hidden, router_w.T), bf16 in and out, same buffers and "
                             "stream, K back-to-back launches: the plain GEMM alone, without scores, "
                             "selection or histogram; compare with roofline.kernel_ms"},
+        "extras": extras,
         "plan": {"swaps": len(host_plan.swaps), "kernel_ms": plan_ms,
                  "max_mean_before": float(out.max_mean.item()),
                  "max_mean_after": float(host_plan.rank_loads.max() * wl.R / host_plan.rank_loads.sum())},

@@ -359,8 +359,8 @@ def plan_swaps_timed_device(counts: torch.Tensor, slots: torch.Tensor, budget: B
                             cost: CostModel, out: Optional[DevicePlan] = None,
                             stream: Optional[torch.cuda.Stream] = None) -> DevicePlan:
     """fb_plan_swaps_timed_device: the time-budgeted planner as a stream-ordered kernel.  The
-    cost model's node ids and expert sizes may be sequences (copied to the device) or device
-    tensors (int32[R] and int64[E])."""
+    cost model's node ids and expert sizes may be sequences (copied to the device on every call)
+    or device tensors (int32[R] and int64[E], used as they are: the form for repeated calls)."""
     if counts.dtype != torch.int32 or slots.dtype != torch.int32 or slots.dim() != 2:
         raise ValueError("counts must be int32[E] and slots int32[R, S]")
     if not (counts.is_contiguous() and slots.is_contiguous()):

@@ -98,15 +98,27 @@ struct Shared {
   int32_t node[kMaxR];
   int32_t acc_pair[kMaxTimedSwaps];   // a * kMaxR + b, a < b
   int64_t acc_cost[kMaxTimedSwaps];
+  int64_t ebytes[kMaxRS];             // expert sizes
 };
+
+// ceil(num / beta) for 0 <= num < 2^52 and 1 <= beta <= 2^40, exactly: a double-precision
+// quotient is within one of the truncated one (its relative error is below 2^-51), and one
+// integer correction step settles it.
+__device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t beta, double inv_beta) {
+  int64_t q = (int64_t)((double)num * inv_beta);
+  int64_t r = num - q * beta;
+  if (r < 0) { q -= 1; r += beta; }
+  if (r >= beta) { q += 1; r -= beta; }
+  return q + (r > 0 ? 1 : 0);
+}
 
 // Eq. 9 in whole nanoseconds for a swap of items i (rank a) and j (rank b).
 __device__ __forceinline__ int64_t swap_cost(const PlanDeviceLaunch& a, const Shared& sh, int ra,
                                              int rb, int i, int j) {
   const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
-  const int64_t bytes = (i < a.E ? a.expert_bytes[i] : 0) + (j < a.E ? a.expert_bytes[j] : 0);
+  const int64_t bytes = (i < a.E ? sh.ebytes[i] : 0) + (j < a.E ? sh.ebytes[j] : 0);
   const int64_t beta = a.cost.beta_bytes_per_us[t];
-  return a.cost.alpha_ns[t] + (bytes * 1000 + beta - 1) / beta;
+  return a.cost.alpha_ns[t] + ceil_div(bytes * 1000, beta, 1.0 / (double)beta);
 }
 
 // Does a swap of cost c between ranks ra and rb fit the remaining rank and link budgets?
@@ -127,6 +139,12 @@ __device__ __forceinline__ bool ratio_better(uint64_t g1, uint64_t c1, uint64_t 
                                              uint64_t c2, uint64_t t2) {
   if (g1 == 0) return false;
   if (g2 == 0) return true;
+  // the products in double precision decide unless they are within 2^-30 of each other (their
+  // relative rounding error is below 2^-51); only then the exact 128-bit products are formed
+  const double ld = (double)g1 * (double)c2, rd = (double)g2 * (double)c1;
+  const double tol = 0x1p-30 * (ld > rd ? ld : rd);
+  if (ld - rd > tol) return true;
+  if (rd - ld > tol) return false;
   const unsigned __int128 l = (unsigned __int128)g1 * c2, r = (unsigned __int128)g2 * c1;
   if (l != r) return l > r;
   return t1 < t2;
@@ -149,8 +167,11 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
     for (int r = tid; r < R; r += NT) { sh.node[r] = a.rank_node[r]; sh.rank_left[r] = a.cost.rank_budget_ns; }
   __syncthreads();
   if (a.timed)
-    for (int e = tid; e < E; e += NT)
-      if (a.expert_bytes[e] < 0 || a.expert_bytes[e] > kCostLimit) sh.bad = 1;
+    for (int e = tid; e < E; e += NT) {
+      const int64_t b = a.expert_bytes[e];
+      sh.ebytes[e] = b;
+      if (b < 0 || b > kCostLimit) sh.bad = 1;
+    }
   for (int c = tid; c < RS; c += NT) {
     const int e = a.slot_expert[c];
     if (e == -1) { sh.item[c] = E + c; sh.pos[E + c] = c; }
