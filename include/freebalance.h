@@ -210,10 +210,16 @@ int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
 
 /* fb_predict_load with a router weight packed beforehand by fb_pack_router_weight (same E, H and
  * dtype): the per-batch call of a server that packs its routers at load time.  Results are
- * identical to fb_predict_load's on the same inputs.
+ * identical to fb_predict_load's on the same inputs, except in split mode (below).
  *   router_packed        device, as written by fb_pack_router_weight.
  *   router_packed_bytes  its size; FB_ENOSPC if below fb_router_packed_bytes(E, H, dtype).
- *   workspace            device, >= 2048 bytes, prepared by fb_predict_workspace_init.
+ *   workspace            device, >= 2048 bytes, prepared by fb_predict_workspace_init.  With at
+ *                        least fb_predict_split_workspace_bytes(T, E, H, dtype) bytes, a batch
+ *                        too small to occupy the GPU runs in split mode: the hidden dimension of
+ *                        every tile is split over several workgroups whose partial logits (kept
+ *                        in the workspace past its first 2048 bytes) are added in a fixed order
+ *                        by a second kernel.  Results are then deterministic and within the
+ *                        float32 summation-order tolerance of the fused path's.
  * Every other argument, and every error, as in fb_predict_load. */
 int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
                            int32_t dtype, const void* router_packed, size_t router_packed_bytes,
@@ -222,6 +228,10 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
                            int32_t* counts, int32_t* rank_loads, double* max_mean,
                            void* workspace, size_t workspace_bytes, int32_t* topk_idx,
                            float* logits, void* stream);
+
+/* Workspace bytes that let fb_predict_load_packed run a batch of T tokens in split mode on the
+ * current device (2048 when the batch runs fused anyway; 0 for invalid arguments). */
+size_t fb_predict_split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype);
 
 /* ---- Prediction-quality diagnostics (Sec. "Metrics" and the prediction-quality study) ----------
  * Device-side measurements of how well the early pass predicts the actual routing: run

@@ -24,6 +24,7 @@ from .api import (  # noqa: F401
     plan_swaps_timed,
     plan_swaps_timed_device,
     predict_load,
+    predict_split_workspace_bytes,
     swap_budget_from_cost,
 )
 from ._lib import FreeBalanceError, LIB_PATH, lib  # noqa: F401

@@ -163,17 +163,36 @@ def pack_router_weight(router_w: torch.Tensor,
     return PackedRouter(packed, E, H, router_w.dtype)
 
 
+def predict_split_workspace_bytes(T: int, E: int, H: int, dtype: torch.dtype,
+                                  device=None) -> int:
+    """fb_predict_split_workspace_bytes on `device`: the workspace size with which a packed batch
+    of T tokens runs in split mode (2048 when it runs fused anyway)."""
+    code = L.FB_BF16 if dtype == torch.bfloat16 else L.FB_F32 if dtype == torch.float32 else None
+    if code is None:
+        raise TypeError("dtype must be bfloat16 or float32")
+    dev = torch.device(device) if device is not None else torch.device("cuda")
+    with torch.cuda.device(dev):
+        n = int(L.lib().fb_predict_split_workspace_bytes(T, E, H, code))
+    if n == 0:
+        L.check(L.FB_EINVAL, "fb_predict_split_workspace_bytes")
+    return n
+
+
 class Predictor:
     """Holds the device workspace of fb_predict_load for one device.
 
     Calls on one Predictor must be ordered on one stream (they share the workspace).  The workspace
-    grows on demand to what fb_predict_workspace_bytes asks for the largest unpacked router seen."""
+    grows on demand to what fb_predict_workspace_bytes asks for the largest unpacked router seen
+    and, with split=True, to what fb_predict_split_workspace_bytes asks for packed batches too small
+    to occupy the GPU (those then run in split mode)."""
 
-    def __init__(self, device=None, stream: Optional[torch.cuda.Stream] = None):
+    def __init__(self, device=None, stream: Optional[torch.cuda.Stream] = None,
+                 split: bool = True):
         dev = torch.device(device) if device is not None else torch.device("cuda")
         if dev.index is None:
             dev = torch.device("cuda", torch.cuda.current_device())
         self.device = dev
+        self.split = split
         self.workspace = None
         self._reserve(2048, stream)
 
@@ -227,6 +246,11 @@ class Predictor:
             if need == 0:
                 L.check(L.FB_EUNSUPPORTED if E > 0 else L.FB_EINVAL, "fb_predict_workspace_bytes")
             self._reserve(need, stream)
+        elif self.split:
+            with torch.cuda.device(self.device):
+                need = int(lib.fb_predict_split_workspace_bytes(T, E, H, code))
+            if need > 0:
+                self._reserve(need, stream)
         if out is None:
             out = Prediction(torch.empty(E, dtype=torch.int32, device=self.device),
                              torch.empty(R, dtype=torch.int32, device=self.device),

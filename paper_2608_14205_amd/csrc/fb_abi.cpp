@@ -184,6 +184,8 @@ fb::PredictLaunch make_launch(const void* hidden, int64_t T, int32_t H, int64_t 
   a.logits = logits;
   a.stream = stream;
   a.num_cus = fb::device_cu_count();
+  a.partial = nullptr;
+  a.partial_bytes = 0;
   return a;
 }
 
@@ -230,10 +232,23 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
   if (router_packed_bytes < fb::router_packed_bytes(E, H, dtype)) return FB_ENOSPC;
   const int dc = fb::check_device();
   if (dc != FB_OK) return dc;
-  return fb::launch_predict(make_launch(hidden, T, H, ld_hidden, dtype, router_packed, E,
-                                        logit_bias, select_bias, scoring, expert_to_rank, R,
-                                        counts, rank_loads, max_mean, workspace, topk_idx, logits,
-                                        stream));
+  fb::PredictLaunch a = make_launch(hidden, T, H, ld_hidden, dtype, router_packed, E, logit_bias,
+                                    select_bias, scoring, expert_to_rank, R, counts, rank_loads,
+                                    max_mean, workspace, topk_idx, logits, stream);
+  // split mode when the caller's workspace holds the partial logits this batch needs
+  const size_t sb = fb::split_workspace_bytes(T, E, H, dtype, a.num_cus);
+  if (sb > 0 && workspace_bytes >= fb::kWsBytes + sb) {
+    a.partial = reinterpret_cast<float*>(static_cast<char*>(workspace) + fb::kWsBytes);
+    a.partial_bytes = workspace_bytes - fb::kWsBytes;
+  }
+  return fb::launch_predict(a);
+}
+
+size_t fb_predict_split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype) {
+  if (T < 0 || E < 1 || E > FB_MAX_EXPERTS || H < 1 || (dtype != FB_BF16 && dtype != FB_F32))
+    return 0;
+  const size_t sb = fb::split_workspace_bytes(T, E, H, dtype, fb::device_cu_count());
+  return fb::kWsBytes + sb;
 }
 
 int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,

@@ -30,7 +30,11 @@ struct PredictLaunch {
   float* logits;
   void* stream;
   int32_t num_cus;    // compute units of the device (tile-height choice)
+  float* partial;     // split mode: partial-logit buffer in the workspace, or NULL
+  size_t partial_bytes;
 };
+// Bytes of partial logits the split mode needs for a batch (0: that batch runs fused).
+size_t split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype, int num_cus);
 
 // Workspace layout (device): per-expert accumulator and the completion ticket.  Every completed
 // launch leaves both at zero.

@@ -94,7 +94,11 @@ struct Params {
   int32_t* topk_idx;
   float* logits;
   uint32_t nblocks;
-  int32_t nstages;
+  int32_t nstages;     // stages this workgroup contracts
+  int32_t st_base;     // first of them
+  int32_t st_total;    // stages of a whole row
+  int32_t ks;          // splits of the stage range (split mode); 1 otherwise
+  float* partial;      // split mode: partial logits, [tile][split][register][thread]
 };
 
 // Workgroup barrier that orders LDS only; outstanding global loads stay in flight across it.
@@ -327,7 +331,7 @@ __device__ __forceinline__ void contract(f32x16 (&acc)[FE][FT], const Params& p,
   // slices: the scheduling barriers keep other loads from moving into or across it.
   auto load_stage = [&](int bi, int st) {        // bi: stage buffer (wave-uniform)
     const bool live = st < nst;
-    const int sb = live ? st * kStageRowBytes : 0;
+    const int sb = live ? (p.st_base + st) * kStageRowBytes : 0;
     const int lim = live ? Hb - sb : 0;           // bytes of the stage inside the row (scalar)
     char* const dst = ring_lds + bi * STAGE + wave * LPW * 1024;
     __builtin_amdgcn_sched_barrier(0);
@@ -347,14 +351,14 @@ __device__ __forceinline__ void contract(f32x16 (&acc)[FE][FT], const Params& p,
   constexpr int kPackStage = EPAD * kStageRowBytes;
   const uint64_t wbase_addr = reinterpret_cast<uint64_t>(p.wpack);
   const i32x4 wr = {(int32_t)(uint32_t)wbase_addr, (int32_t)(uint32_t)(wbase_addr >> 32),
-                    nst * kPackStage, (int32_t)kRsrcWord3};
+                    p.st_total * kPackStage, (int32_t)kRsrcWord3};
   const uint32_t wbase = (uint32_t)(we * kNStep * FE * 1024 + lane * 16);
   auto load_w = [&](u32x4(&dst)[FE], int st, int q) {
     const bool ok = st < nst;
 #pragma unroll
     for (int fe = 0; fe < FE; ++fe)
       buffer_load_b128_acc(dst[fe], wr, ok ? wbase + (uint32_t)((q * FE + fe) * 1024) : kOobOffset,
-                           ok ? st * kPackStage : 0);
+                           ok ? (p.st_base + st) * kPackStage : 0);
   };
   // loads issued after the weight slice of k-step q (of any stage) by the time its MFMAs start: the
   // slices of the next kRingW - 1 k-steps, and the stage batches issued at k-step 7 of the stages
@@ -465,7 +469,11 @@ __device__ __forceinline__ void contract(f32x16 (&acc)[FE][FT], const Params& p,
 }
 
 // BM_: tokens per workgroup (the configuration's own, or half of it when that fills the chip better)
-template <bool BF16, int EPAD, int BM_>
+// MODE: kFused contracts the whole row and finishes the tile; kPartial (split mode, grid tiles x
+// ks) contracts one of ks stage ranges and stores its partial logits; kFinish (split mode, grid
+// tiles) sums a tile's partial logits in split order and finishes the tile.
+constexpr int kFused = 0, kPartial = 1, kFinish = 2;
+template <bool BF16, int EPAD, int BM_, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   using Cfg = TileCfg<EPAD>;
   constexpr int WE = Cfg::WE, WT = Cfg::WT, BM = BM_;
@@ -507,8 +515,10 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int we = wave % WE;
   const int wt = wave / WE;
-  const int64_t row0 = (int64_t)blockIdx.x * BM;
+  const int tile = MODE == kPartial ? (int)(blockIdx.x / (uint32_t)p.ks) : (int)blockIdx.x;
+  const int64_t row0 = (int64_t)tile * BM;
   const int E = p.E;
+  constexpr int NACC = FE * FT * 16;               // accumulator registers per thread
 
   for (int i = tid; i < EPAD; i += kThreads) {
     hist[i] = 0;
@@ -525,7 +535,39 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  if (row0 < p.T) contract<BF16, EPAD, FE, FT, NS, BM, TW>(acc, p, row0, wave, we, wt, lane, smem);
+  if constexpr (MODE == kFinish) {
+    // the tile's logits: its partial sums added in split order (the same order on every run)
+    const float* src = p.partial + (size_t)tile * p.ks * NACC * kThreads + tid;
+    for (int ks = 0; ks < p.ks; ++ks) {
+#pragma unroll
+      for (int a = 0; a < FE; ++a)
+#pragma unroll
+        for (int b = 0; b < FT; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            acc[a][b][r] += src[((size_t)ks * NACC + (a * FT + b) * 16 + r) * kThreads];
+    }
+  } else {
+    Params q = p;
+    if constexpr (MODE == kPartial) {
+      const int ks = (int)(blockIdx.x % (uint32_t)p.ks);
+      const int chunk = (p.st_total + p.ks - 1) / p.ks;
+      q.st_base = ks * chunk;
+      q.nstages = p.st_total - q.st_base < chunk ? p.st_total - q.st_base : chunk;
+    }
+    if (row0 < p.T && q.nstages > 0)
+      contract<BF16, EPAD, FE, FT, NS, BM, TW>(acc, q, row0, wave, we, wt, lane, smem);
+    if constexpr (MODE == kPartial) {
+      float* dst = p.partial + ((size_t)blockIdx.x * NACC) * kThreads + tid;
+#pragma unroll
+      for (int a = 0; a < FE; ++a)
+#pragma unroll
+        for (int b = 0; b < FT; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[(size_t)((a * FT + b) * 16 + r) * kThreads] = acc[a][b][r];
+      return;
+    }
+  }
   lds_barrier();
 
   // Group-limited routing where the kept groups fill exactly half of a token's lanes (as with 8
@@ -1009,6 +1051,39 @@ int epad_of(int32_t E) {
   return E <= 32 ? 32 : E <= 64 ? 64 : E <= 128 ? 128 : 256;
 }
 
+// Split mode: when the tiles would occupy at most half of the CUs, the stage range of every tile
+// is split over up to four workgroups (at least four stages each), so that more CUs stream the
+// hidden rows and each streams a share of the router weight.
+int split_count(int64_t T, int BM, int st_total, int num_cus) {
+  const int64_t tiles = (T + BM - 1) / BM;
+  if (T <= 0 || tiles * 2 > num_cus) return 1;
+  int64_t ks = num_cus / tiles;
+  if (ks > 4) ks = 4;
+  if (ks > st_total / 4) ks = st_total / 4;
+  return ks > 1 ? (int)ks : 1;
+}
+
+// Tile height of a launch (see launch_cfg).
+template <int EPAD>
+int tile_rows(int64_t T, int num_cus) {
+  constexpr int BM = TileCfg<EPAD>::BM;
+  if (EPAD == 256) {
+    const int64_t half_tiles = (T + BM / 2 - 1) / (BM / 2);
+    if (T > 0 && half_tiles <= num_cus) return BM / 2;
+  }
+  return BM;
+}
+
+template <int EPAD>
+size_t split_bytes_cfg(int64_t T, int32_t H, int32_t dtype, int num_cus) {
+  const int BM = tile_rows<EPAD>(T, num_cus);
+  const int st_total = (H * (dtype == FB_BF16 ? 2 : 4) + kStageRowBytes - 1) / kStageRowBytes;
+  const int ks = split_count(T, BM, st_total, num_cus);
+  if (ks <= 1) return 0;
+  const int64_t tiles = (T + BM - 1) / BM;
+  return (size_t)tiles * ks * BM * EPAD * sizeof(float);
+}
+
 template <int EPAD>
 int launch_pack_cfg(const void* w, int32_t E, int32_t Hbytes, void* out, void* stream) {
   const int32_t nst = (Hbytes + kStageRowBytes - 1) / kStageRowBytes;
@@ -1048,9 +1123,23 @@ int launch_cfg_bm(const PredictLaunch& a) {
   p.logits = a.logits;
   const int64_t tiles = (a.T + BM - 1) / BM;
   p.nblocks = (uint32_t)(tiles > 0 ? tiles : 1);
-  p.nstages = (p.Hbytes + kStageRowBytes - 1) / kStageRowBytes;
-  hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM>), dim3(p.nblocks), dim3(kThreads), 0,
-                     static_cast<hipStream_t>(a.stream), p);
+  p.st_total = (p.Hbytes + kStageRowBytes - 1) / kStageRowBytes;
+  p.nstages = p.st_total;
+  p.st_base = 0;
+  p.ks = split_count(a.T, BM, p.st_total, a.num_cus);
+  p.partial = a.partial;
+  hipStream_t st = static_cast<hipStream_t>(a.stream);
+  if (p.ks > 1 && a.partial != nullptr &&
+      a.partial_bytes >= (size_t)tiles * p.ks * BM * EPAD * sizeof(float)) {
+    hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM, kPartial>), dim3(p.nblocks * p.ks),
+                       dim3(kThreads), 0, st, p);
+    hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM, kFinish>), dim3(p.nblocks), dim3(kThreads),
+                       0, st, p);
+  } else {
+    p.ks = 1;
+    hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM, kFused>), dim3(p.nblocks), dim3(kThreads),
+                       0, st, p);
+  }
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
 }
 
@@ -1060,8 +1149,7 @@ int launch_cfg(const PredictLaunch& a) {
   // Half-height tiles when the full-height grid would leave CUs idle and the half-height one still
   // fits in a single wave of workgroups: every CU then streams the weight for fewer tokens.
   if constexpr (EPAD == 256) {
-    const int64_t half_tiles = (a.T + BM / 2 - 1) / (BM / 2);
-    if (a.T > 0 && half_tiles <= a.num_cus) return launch_cfg_bm<BF16, EPAD, BM / 2>(a);
+    if (tile_rows<EPAD>(a.T, a.num_cus) == BM / 2) return launch_cfg_bm<BF16, EPAD, BM / 2>(a);
   }
   return launch_cfg_bm<BF16, EPAD, BM>(a);
 }
@@ -1092,6 +1180,15 @@ int launch_pack(const void* router_w, int32_t E, int32_t H, int32_t dtype, void*
     case 64: return launch_pack_cfg<64>(router_w, E, Hbytes, packed, stream);
     case 128: return launch_pack_cfg<128>(router_w, E, Hbytes, packed, stream);
     default: return launch_pack_cfg<256>(router_w, E, Hbytes, packed, stream);
+  }
+}
+
+size_t split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype, int num_cus) {
+  switch (epad_of(E)) {
+    case 32: return split_bytes_cfg<32>(T, H, dtype, num_cus);
+    case 64: return split_bytes_cfg<64>(T, H, dtype, num_cus);
+    case 128: return split_bytes_cfg<128>(T, H, dtype, num_cus);
+    default: return split_bytes_cfg<256>(T, H, dtype, num_cus);
   }
 }
 

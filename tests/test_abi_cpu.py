@@ -34,7 +34,7 @@ def test_header_declares_the_boundary():
                             "fb_plan_swaps", "fb_plan_swaps_device", "fb_swap_budget_from_cost",
                             "fb_topk_hits", "fb_cosine_workspace_bytes", "fb_row_cosine_mean",
                             "fb_fold_rank_loads", "fb_plan_swaps_timed",
-                            "fb_plan_swaps_timed_device"])
+                            "fb_plan_swaps_timed_device", "fb_predict_split_workspace_bytes"])
 
 
 def test_library_exports_every_declared_symbol():

@@ -225,11 +225,40 @@ def test_pack_layout_and_packed_predict(E, H, dtype):
     ref = _pack_reference(np.ascontiguousarray(li.w).view(np.uint8), E, H * (2 if dtype == "bf16" else 4))
     assert got.size == ref.size and np.array_equal(got, ref)
     a = run_gpu(li, wl, e2r, packed=False)
-    b = run_gpu(li, wl, e2r, packed=True)
+    b = run_gpu(li, wl, e2r, packed=True, predictor=fb.Predictor(split=False))
     for key in ("counts", "rank_loads", "topk"):
         assert np.array_equal(a[key], b[key]), key
     assert a["max_mean"] == b["max_mean"]
     assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
+
+
+@pytest.mark.parametrize("name,T", [("tiny", 77), ("tiny", 512), ("mixtral", 1000), ("qwen3", 1091),
+                                    ("dsv3", 300), ("dsv3", 1100)])
+def test_split_mode_parity(name, T):
+    """Packed batches too small to occupy the GPU run in split mode (partial logits of stage ranges
+    on several workgroups, added in split order by a second kernel): oracle parity, repeats that
+    are bit-identical, and the fused path's selections where both match the oracle on every token."""
+    wl, e2r = _case(name, T)
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    need = fb.predict_split_workspace_bytes(T, wl.E, wl.H, dt)
+    _say(f"[split] {name} T={T} workspace {need}")
+    assert need > 2048, "this batch is expected to run in split mode"
+    li = make_layer(wl, 1)
+    pred = fb.Predictor()
+    a = run_gpu(li, wl, e2r, predictor=pred, packed=True)
+    assert pred.workspace.numel() >= need
+    stats = check_prediction(a, li, wl, e2r, label=f"split {name}/T={T}")
+    check_counts_consistent(a, wl, e2r)
+    b = run_gpu(li, wl, e2r, predictor=pred, packed=True)
+    for key in ("counts", "rank_loads", "topk"):
+        assert np.array_equal(a[key], b[key]), key
+    assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
+    fused = run_gpu(li, wl, e2r, predictor=fb.Predictor(split=False), packed=True)
+    fstats = check_prediction(fused, li, wl, e2r, label=f"fused {name}/T={T}")
+    if stats["mismatch"] == 0 and fstats["mismatch"] == 0:
+        assert np.array_equal(a["counts"], fused["counts"])
+        assert np.array_equal(np.sort(a["topk"], 1), np.sort(fused["topk"], 1))
+    _say(f"[split] {name} T={T} ok {stats}")
 
 
 def test_qwen3_layers_back_to_back():
