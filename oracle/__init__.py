@@ -15,10 +15,12 @@ Modules
 ``planner``    Sec. "Budgeted Expert-Swap Planning": pairwise-swap load update (Eq. 6-7), the load
                objective Phi (Eq. 8) evaluated literally with exact rationals, the deterministic greedy
                ordering and acceptance rule, the frontier restriction and the Alg. 1 loop.
+``replicas``   Replicated placements: replica shares of an expert's tokens and the rank loads they
+               give (the reading of the "EPLB + Ours" setting).
 ``cost``       Swap cost (Eq. 9) and attention-window budget (Eq. 10) as a swap count.
 ``exact``      Micro-oracle for tiny inputs: exact rational dot products rounded once to float32,
                brute-force selections with ``sorted``.
 
 Readings of points the paper leaves open are listed in each function's docstring.
 """
-from . import cost, exact, planner, predictor  # noqa: F401
+from . import cost, exact, planner, predictor, replicas  # noqa: F401

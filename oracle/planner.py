@@ -42,6 +42,13 @@ rank and per link), used when a cost model is given:
 * candidates are ordered by decreasing Delta / C, then by the same lexicographic tie-break;
 * after an accepted swap both ranks' and the link's remaining budgets drop by C.
 The swap cap and the per-rank cap still apply on top of the time budget.
+
+Replicated placements (oracle.replicas: slot value e + E * j is replica j of expert e): the items are
+the replicas with their shares as loads, real items keep their slot value as id and empty slots take
+the ids E * J + r * S + s (J = the largest replica count; J = 1 without replicas, which gives the ids
+above).  A candidate may not put a replica on a rank that already holds a replica of the same expert
+(this also rules out exchanging two replicas of one expert); every replica moves at most once.  Swaps
+report slot values, and expert_to_rank gives the rank of replica 0.
 """
 from __future__ import annotations
 
@@ -51,6 +58,7 @@ from typing import List, NamedTuple, Optional, Tuple
 import numpy as np
 
 from .cost import CostModel, swap_cost_ns
+from .replicas import decode, replica_counts, replica_share
 
 FRONTIER, FULL = "frontier", "full"
 
@@ -88,25 +96,25 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
     E = len(counts)
     table = np.asarray(slots, dtype=np.int64)
     R, S = table.shape
-    seen = set()
-    for e in table.reshape(-1):
-        if e < -1 or e >= E:
-            raise ValueError("slot table holds an invalid expert id")
-        if e >= 0:
-            if e in seen:
-                raise ValueError("expert placed twice")
-            seen.add(int(e))
-    if len(seen) != E:
-        raise ValueError("expert missing from the slot table")
+    reps = replica_counts(table, E)
     if max_swaps < 0 or tau < 0 or per_rank_cap < 0:
         raise ValueError("negative budget or threshold")
 
-    # items: slot contents; empty slots become virtual zero-load items with ids E + r*S + s
-    item = [[int(table[r, s]) if table[r, s] >= 0 else E + r * S + s for s in range(S)]
+    # items: slot contents; empty slots become virtual zero-load items with ids E*J + r*S + s
+    V = E * max(reps)               # slot values are below V; virtual ids start there
+    item = [[int(table[r, s]) if table[r, s] >= 0 else V + r * S + s for s in range(S)]
             for r in range(R)]
 
+    def expert_of(i: int) -> int:
+        return decode(i, E)[0] if i < V else -1
+
     def load_of(i: int) -> int:
-        return counts[i] if i < E else 0
+        if i >= V:
+            return 0
+        e, j = decode(i, E)
+        return replica_share(counts[e], reps[e], j)
+
+    held = [set(expert_of(i) for i in item[r] if i < V) for r in range(R)]
 
     L = [sum(load_of(i) for i in item[r]) for r in range(R)]
     before = np.array(L, dtype=np.int64)
@@ -132,7 +140,7 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
         link_used = {}
 
     def bytes_of(i: int) -> int:
-        return int(cost.expert_bytes[i]) if i < E else 0
+        return int(cost.expert_bytes[expert_of(i)]) if i < V else 0
 
     def lowest_argmax(vals):
         return max(range(len(vals)), key=lambda r: (vals[r], -r))
@@ -159,7 +167,9 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
             for p in range(S):
                 for q in range(S):
                     i, j = item[a][p], item[b][q]
-                    if i in moved or j in moved or (i >= E and j >= E):
+                    if i in moved or j in moved or (i >= V and j >= V):
+                        continue
+                    if (i < V and expert_of(i) in held[b]) or (j < V and expert_of(j) in held[a]):
                         continue
                     L2 = list(L)
                     L2[a] = L[a] - load_of(i) + load_of(j)     # Eq. 6
@@ -184,13 +194,18 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
         _, a, b, p, q, L2, delta, c = best
         i, j = item[a][p], item[b][q]
         item[a][p], item[b][q] = j, i
+        for r, gone, came in ((a, i, j), (b, j, i)):
+            if gone < V:
+                held[r].discard(expert_of(gone))
+            if came < V:
+                held[r].add(expert_of(came))
         L = L2
         moved.update((i, j))
         part[a] += 1
         part[b] += 1
         g = delta * g_den
         assert g.denominator == 1
-        swaps.append(Swap(a, b, p, q, i if i < E else -1, j if j < E else -1, int(g)))
+        swaps.append(Swap(a, b, p, q, i if i < V else -1, j if j < V else -1, int(g)))
         if cost is not None:
             rank_left[a] -= c
             rank_left[b] -= c
@@ -198,10 +213,10 @@ def plan_swaps(counts, slots, max_swaps: int, *, gamma: Optional[Tuple[int, int]
             link_used[link] = link_used.get(link, 0) + c
             costs.append(c)
 
-    new_slots = np.array([[i if i < E else -1 for i in row] for row in item], dtype=np.int32)
+    new_slots = np.array([[i if i < V else -1 for i in row] for row in item], dtype=np.int32)
     e2r = np.empty(E, dtype=np.int32)
     for r in range(R):
         for i in item[r]:
-            if i < E:
+            if i < E:               # replica 0 of expert i
                 e2r[i] = r
     return Plan(swaps, new_slots, e2r, np.array(L, dtype=np.int64), before, costs)
