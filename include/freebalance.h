@@ -273,12 +273,38 @@ int fb_row_cosine_mean(const void* a, const void* b, int64_t rows, int32_t cols,
 int fb_fold_rank_loads(const int32_t* counts, int32_t E, const int32_t* expert_to_rank, int32_t R,
                        int32_t* rank_loads, double* max_mean, void* stream);
 
+/* Rank loads and max-to-mean ratio of a count vector under a replicated placement, as produced by a
+ * history-driven placement that copies hot experts (the starting point of the "EPLB + Ours" runs of
+ * Table 1).  The paper leaves the split of an expert's tokens among its copies to the dispatch
+ * policy; here replica j of an expert with n tokens and c replicas carries floor(n / c) tokens, plus
+ * one if j < n mod c (a round-robin dispatch), and L_r sums the shares on rank r.
+ *   counts       device int32[E] (>= 0).
+ *   slot_expert  device int32[R * S] row-major: value e + E * j is replica j of expert e, -1 an
+ *                empty slot.  Every expert must have replicas 0 .. c_e - 1, each once, and no rank
+ *                may hold two replicas of one expert; a placement without replicas (every value
+ *                below E) is the plain slot table of fb_plan_swaps.  A violated rule or a negative
+ *                count makes *max_mean = -1.0.
+ *   rank_loads   device int32[R] out; max_mean device double out (1.0 if every load is 0).
+ * FB_EINVAL for null pointers, E, R or S < 1, or E > R * S; FB_EUNSUPPORTED for R > FB_MAX_RANKS or
+ * R * S > FB_MAX_SLOTS_TOTAL.  One workgroup, stream-ordered. */
+int fb_fold_slot_loads(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
+                       int32_t S, int32_t* rank_loads, double* max_mean, void* stream);
+
 /* Budgeted greedy expert-swap planner on the host (Sec. Budgeted Expert-Swap Planning, Eq. 6-8,
  * Alg. 1).  Pure and deterministic: identical inputs give a byte-identical plan.
  *   counts            host int32[E] (>= 0): the predicted per-expert workload, not rank loads.
  *   E                 experts, >= 1.
  *   slot_expert       host int32[R * S] row-major: expert in slot s of rank r, -1 = empty slot.
- *                     Every expert 0..E-1 must appear exactly once (FB_EINVAL otherwise).
+ *                     Every expert 0..E-1 must appear exactly once (FB_EINVAL otherwise), or, for
+ *                     a replicated placement (the "EPLB + Ours" setting of Table 1), value e + E * j
+ *                     is replica j of expert e: every expert then needs replicas 0 .. c_e - 1, each
+ *                     once, and no rank may hold two replicas of one expert.  Replica j carries
+ *                     floor(n_e / c_e) tokens, plus one if j < n_e mod c_e (as fb_fold_slot_loads),
+ *                     and keeps its ordinal when it moves; a swap may not put a replica on a rank
+ *                     that holds another replica of the same expert, and empty slots take the
+ *                     tie-break ids E * J + r * S + s (J = the largest c_e).  Swaps and
+ *                     new_slot_expert then report slot values, new_expert_to_rank the rank of
+ *                     replica 0.
  *   R, S              ranks (>= 1) and slots per rank (>= 1).
  *   budget            host, see fb_budget.
  *   swaps             host fb_swap[swaps_cap] out; swaps_cap >= budget->max_swaps (FB_ENOSPC).
@@ -303,7 +329,9 @@ int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* slot_expert, 
  *   new_expert_to_rank    device int32[E] out (required).
  *   new_rank_loads        device int64[R] out (required).
  *   status                device int32 out: FB_OK, or FB_EINVAL if the slot table is invalid or a
- *                         count is negative (then the plan is empty and the placement unchanged). */
+ *                         count is negative, or FB_EUNSUPPORTED for a replicated placement (a value
+ *                         >= E; the host planners take those); then the plan is empty and the
+ *                         placement unchanged. */
 int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
                          int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
                          int32_t* new_slot_expert, int32_t* new_expert_to_rank,

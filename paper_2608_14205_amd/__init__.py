@@ -15,6 +15,7 @@ from .api import (  # noqa: F401
     Predictor,
     Scoring,
     fold_rank_loads,
+    fold_slot_loads,
     pack_router_weight,
     prediction_quality,
     row_cosine_mean,

@@ -81,6 +81,7 @@ SIGNATURES = {
     "fb_cosine_workspace_bytes": (_SZ, []),
     "fb_row_cosine_mean": (ctypes.c_int, [_VP, _VP, _I64, _I32, _I64, _I64, _I32, _VP, _VP, _SZ, _VP]),
     "fb_fold_rank_loads": (ctypes.c_int, [_VP, _I32, _VP, _I32, _VP, _VP, _VP]),
+    "fb_fold_slot_loads": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32, _VP, _VP, _VP]),
 }
 
 _lock = threading.Lock()

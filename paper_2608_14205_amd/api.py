@@ -497,6 +497,26 @@ def fold_rank_loads(counts: torch.Tensor, expert_to_rank: torch.Tensor, R: int,
     return loads, mm
 
 
+def fold_slot_loads(counts: torch.Tensor, slots: torch.Tensor,
+                    stream: Optional[torch.cuda.Stream] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """fb_fold_slot_loads: rank loads of a (possibly replicated) R x S slot table, as
+    (rank_loads int32[R], max_mean float64[1]) on the device; max_mean is -1 for a table that breaks
+    the placement rules."""
+    if counts.dtype != torch.int32 or slots.dtype != torch.int32 or slots.dim() != 2:
+        raise ValueError("counts must be int32[E] and slots an int32 R x S table")
+    if not (counts.is_contiguous() and slots.is_contiguous()) or counts.device != slots.device:
+        raise ValueError("counts and slots must be contiguous and on one device")
+    dev = counts.device
+    R, S = slots.shape
+    loads = torch.empty(R, dtype=torch.int32, device=dev)
+    mm = torch.empty(1, dtype=torch.float64, device=dev)
+    with torch.cuda.device(dev):
+        L.check(L.lib().fb_fold_slot_loads(_ptr(counts), counts.numel(), _ptr(slots), R, S,
+                                           _ptr(loads), _ptr(mm), _stream_handle(dev, stream)),
+                "fb_fold_slot_loads")
+    return loads, mm
+
+
 def prediction_quality(pred: Prediction, actual: Prediction, hidden_prev: Optional[torch.Tensor] = None,
                        hidden_target: Optional[torch.Tensor] = None) -> Quality:
     """Hit rate and cosines of an early pass against the actual routing; both Predictions must

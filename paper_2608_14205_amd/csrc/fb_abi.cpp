@@ -377,4 +377,15 @@ int fb_fold_rank_loads(const int32_t* counts, int32_t E, const int32_t* expert_t
   return fb::launch_fold(counts, E, expert_to_rank, R, rank_loads, max_mean, stream);
 }
 
+int fb_fold_slot_loads(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
+                       int32_t S, int32_t* rank_loads, double* max_mean, void* stream) {
+  if (!counts || !slot_expert || !rank_loads || !max_mean || E < 1 || R < 1 || S < 1)
+    return FB_EINVAL;
+  if (R > FB_MAX_RANKS || (int64_t)R * S > FB_MAX_SLOTS_TOTAL) return FB_EUNSUPPORTED;
+  if (E > R * S) return FB_EINVAL;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  return fb::launch_slot_fold(counts, E, slot_expert, R, S, rank_loads, max_mean, stream);
+}
+
 }  // extern "C"

@@ -83,6 +83,8 @@ int launch_cosine(const void* a, const void* b, int64_t rows, int32_t cols, int6
                   int32_t dtype, double* out, void* workspace, void* stream);
 int launch_fold(const int32_t* counts, int32_t E, const int32_t* e2r, int32_t R, int32_t* rank_loads,
                 double* max_mean, void* stream);
+int launch_slot_fold(const int32_t* counts, int32_t E, const int32_t* slots, int32_t R, int32_t S,
+                     int32_t* rank_loads, double* max_mean, void* stream);
 
 // Current device must be gfx950; cached per device.  FB_OK, FB_EUNSUPPORTED or FB_EDEVICE.
 int check_device();

@@ -170,20 +170,23 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
     for (int e = tid; e < E; e += NT) {
       const int64_t b = a.expert_bytes[e];
       sh.ebytes[e] = b;
-      if (b < 0 || b > kCostLimit) sh.bad = 1;
+      if (b < 0 || b > kCostLimit) atomicOr(&sh.bad, 1);
     }
+  // bit 0 of bad: an invalid table or count; bit 1: a replica (value >= E), which the device planner
+  // does not take
   for (int c = tid; c < RS; c += NT) {
     const int e = a.slot_expert[c];
     if (e == -1) { sh.item[c] = E + c; sh.pos[E + c] = c; }
-    else if (e < 0 || e >= E) sh.bad = 1;
+    else if (e < 0) atomicOr(&sh.bad, 1);
+    else if (e >= E) atomicOr(&sh.bad, 2);
     else { sh.item[c] = e; sh.pos[e] = c; atomicAdd(&sh.seen[e], 1); }
   }
   __syncthreads();
   for (int e = tid; e < E; e += NT)
-    if (sh.seen[e] != 1 || sh.cnt[e] < 0) sh.bad = 1;
+    if (sh.seen[e] != 1 || sh.cnt[e] < 0) atomicOr(&sh.bad, 1);
   __syncthreads();
   if (sh.bad) {
-    if (tid == 0) { *a.n_swaps = 0; *a.status = FB_EINVAL; }
+    if (tid == 0) { *a.n_swaps = 0; *a.status = (sh.bad & 2) ? FB_EUNSUPPORTED : FB_EINVAL; }
     return;
   }
 
@@ -483,17 +486,19 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
   for (int c = lane; c < RS; c += 64) slot[c].x = (uint32_t)a.slot_expert[c];
   for (int r = lane; r < R; r += 64) part[r] = 0;
   __syncthreads();
-  int bad = 0;
+  int bad = 0, replica = 0;
   for (int c = lane; c < RS; c += 64) {
     const int e = (int)slot[c].x;
     if (e == -1) slot[c].x = (uint32_t)(E + c);
-    else if (e < 0 || e >= E) bad = 1;
+    else if (e < 0) bad = 1;
+    else if (e >= E) replica = 1;
     else atomicAdd(&seen[e], 1);
   }
   __syncthreads();
   for (int e = lane; e < E; e += 64) bad |= (seen[e] != 1) | (cnt[e] < 0);
-  if (__ballot(bad)) {
-    if (lane == 0) { *a.n_swaps = 0; *a.status = FB_EINVAL; }
+  const bool any_replica = __ballot(replica) != 0;
+  if (any_replica || __ballot(bad)) {
+    if (lane == 0) { *a.n_swaps = 0; *a.status = any_replica ? FB_EUNSUPPORTED : FB_EINVAL; }
     return;
   }
   for (int c = lane; c < RS; c += 64) {

@@ -19,10 +19,18 @@
 // 1000 / beta) ns on its link (Eq. 9), must fit what is left of both ranks' and the link's budgets
 // (Eq. 10, enforced per participant), and candidates are ranked by benefit / C, compared exactly as
 // gain_1 * C_2 vs gain_2 * C_1.
+//
+// Replicated placements (a history-driven placement that copies hot experts, on top of which the
+// paper also runs its planner): slot value v = e + E * j is replica j of expert e.  Replica j of an
+// expert with n tokens and c replicas carries floor(n / c) tokens, plus one if j < n mod c, and
+// keeps its ordinal when it moves, so Eq. 6-7 hold with these shares as the item loads.  Empty
+// slots then take the ids E * J + r * S + s (J = the largest replica count, 1 without replicas).
+// A candidate may not put a replica on a rank that already holds one of the same expert.
 #include <stdint.h>
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <unordered_map>
 #include <vector>
 
@@ -64,9 +72,10 @@ struct TimeBudget {
   std::vector<int64_t> rank_left;
   std::unordered_map<int64_t, int64_t> link_used;   // key a * R + b with a < b
 
-  int64_t cost(int32_t a, int32_t b, int64_t i, int64_t j) const {   // Eq. 9, whole ns
+  // Eq. 9 in whole ns for moving experts ei and ej (-1: an empty slot, which transfers nothing)
+  int64_t cost(int32_t a, int32_t b, int64_t ei, int64_t ej) const {
     const int t = rank_node[a] == rank_node[b] ? 0 : 1;
-    const int64_t bytes = (i < E ? expert_bytes[i] : 0) + (j < E ? expert_bytes[j] : 0);
+    const int64_t bytes = (ei >= 0 ? expert_bytes[ei] : 0) + (ej >= 0 ? expert_bytes[ej] : 0);
     const int64_t beta = m.beta_bytes_per_us[t];
     return m.alpha_ns[t] + (bytes * 1000 + beta - 1) / beta;
   }
@@ -100,20 +109,53 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
 
   const int64_t RS = (int64_t)R * S;
   if (E > RS) return FB_EINVAL;
-  std::vector<uint8_t> seen(E, 0);
-  for (int64_t c = 0; c < RS; ++c) {
-    const int32_t e = slot_expert[c];
-    if (e == -1) continue;
-    if (e < 0 || e >= E || seen[e]) return FB_EINVAL;
-    seen[e] = 1;
-  }
   for (int32_t e = 0; e < E; ++e)
-    if (!seen[e] || counts[e] < 0) return FB_EINVAL;
+    if (counts[e] < 0) return FB_EINVAL;
+  // placement rules: every replica once, ordinals 0 .. c_e - 1 of every expert, no rank with two
+  // replicas of one expert (so no ordinal reaches R)
+  std::vector<int32_t> vals;
+  vals.reserve(RS);
+  for (int64_t c = 0; c < RS; ++c) {
+    const int32_t v = slot_expert[c];
+    if (v == -1) continue;
+    if (v < 0 || v / E >= R) return FB_EINVAL;
+    vals.push_back(v);
+  }
+  std::sort(vals.begin(), vals.end());
+  std::vector<int32_t> reps(E, 0);
+  for (size_t u = 0; u < vals.size(); ++u) {
+    if (u > 0 && vals[u] == vals[u - 1]) return FB_EINVAL;
+    ++reps[vals[u] % E];
+  }
+  int32_t J = 1;
+  for (int32_t e = 0; e < E; ++e) {
+    if (reps[e] == 0) return FB_EINVAL;
+    J = reps[e] > J ? reps[e] : J;
+  }
+  // with distinct values, the ordinals of e are 0 .. c_e - 1 iff none reaches c_e
+  for (const int32_t v : vals)
+    if (v / E >= reps[v % E]) return FB_EINVAL;
+  const int64_t V = (int64_t)E * J;                  // slot values are below V
+  if (J > 1 && (int64_t)R * E > ((int64_t)1 << 28)) return FB_EUNSUPPORTED;
+  std::vector<uint8_t> held(J > 1 ? (size_t)R * E : 0, 0);   // held[r * E + e]: e on rank r
+  for (int32_t r = 0; r < R && J > 1; ++r)
+    for (int32_t s = 0; s < S; ++s) {
+      const int32_t v = slot_expert[(int64_t)r * S + s];
+      if (v < 0) continue;
+      uint8_t& h = held[(size_t)r * E + v % E];
+      if (h) return FB_EINVAL;
+      h = 1;
+    }
 
-  // items: slot contents; empty slot (r, s) becomes the zero-load item E + r*S + s
+  // items: slot contents; empty slot (r, s) becomes the zero-load item V + r*S + s
   std::vector<int64_t> item(RS);
-  for (int64_t c = 0; c < RS; ++c) item[c] = slot_expert[c] >= 0 ? slot_expert[c] : E + c;
-  auto load_of = [&](int64_t it) -> int64_t { return it < E ? counts[it] : 0; };
+  for (int64_t c = 0; c < RS; ++c) item[c] = slot_expert[c] >= 0 ? slot_expert[c] : V + c;
+  auto expert_of = [&](int64_t it) -> int64_t { return it < V ? it % E : -1; };
+  auto load_of = [&](int64_t it) -> int64_t {
+    if (it >= V) return 0;
+    const int64_t e = it % E, j = it / E, n = counts[e], c = reps[e];
+    return n / c + (j < n % c ? 1 : 0);
+  };
 
   std::vector<int64_t> L(R, 0);
   for (int32_t r = 0; r < R; ++r)
@@ -130,7 +172,7 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
   const i128 bound = g_den * (i128)N + g_num * 4 * (i128)N * (i128)N;
   if (bound > (i128)INT64_MAX) return FB_EUNSUPPORTED;
 
-  std::vector<uint8_t> moved(E + RS, 0);
+  std::vector<uint8_t> moved(V + RS, 0);
   std::vector<int32_t> part(R, 0);
   int32_t ns = 0;
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
@@ -164,7 +206,10 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
         if (moved[i]) continue;
         for (int32_t q = 0; q < S; ++q) {
           const int64_t j = item[(int64_t)b * S + q];
-          if (moved[j] || (i >= E && j >= E)) continue;
+          if (moved[j] || (i >= V && j >= V)) continue;
+          if (J > 1 && ((i < V && held[(size_t)b * E + i % E]) ||
+                        (j < V && held[(size_t)a * E + j % E])))
+            continue;
           const int64_t d = load_of(j) - load_of(i);
           const int64_t la = L[a] + d, lb = L[b] - d;
           int64_t m2 = la > lb ? la : lb;
@@ -173,7 +218,7 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
           if (gain <= 0) continue;
           int64_t c = 1;
           if (tb) {
-            c = tb->cost(a, b, i, j);
+            c = tb->cost(a, b, expert_of(i), expert_of(j));
             if (!tb->fits(a, b, c)) continue;
           }
           if (better(gain, c, a, b, i, j, best)) {
@@ -195,6 +240,16 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
     const int64_t d = load_of(best.j) - load_of(best.i);
     item[ca] = best.j;
     item[cb] = best.i;
+    if (J > 1) {
+      if (best.i < V) {
+        held[(size_t)best.a * E + best.i % E] = 0;
+        held[(size_t)best.b * E + best.i % E] = 1;
+      }
+      if (best.j < V) {
+        held[(size_t)best.b * E + best.j % E] = 0;
+        held[(size_t)best.a * E + best.j % E] = 1;
+      }
+    }
     L[best.a] += d;
     L[best.b] -= d;
     moved[best.i] = moved[best.j] = 1;
@@ -205,8 +260,8 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
     sw.dst_rank = best.b;
     sw.src_slot = best.p;
     sw.dst_slot = best.q;
-    sw.expert_src = best.i < E ? (int32_t)best.i : -1;
-    sw.expert_dst = best.j < E ? (int32_t)best.j : -1;
+    sw.expert_src = best.i < V ? (int32_t)best.i : -1;
+    sw.expert_dst = best.j < V ? (int32_t)best.j : -1;
     sw.gain = (int64_t)best.gain;
     if (tb) {
       tb->charge(best.a, best.b, best.cost);
@@ -216,8 +271,8 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
 
   *n_swaps = ns;
   if (new_slot_expert)
-    for (int64_t c = 0; c < RS; ++c) new_slot_expert[c] = item[c] < E ? (int32_t)item[c] : -1;
-  if (new_expert_to_rank)
+    for (int64_t c = 0; c < RS; ++c) new_slot_expert[c] = item[c] < V ? (int32_t)item[c] : -1;
+  if (new_expert_to_rank)   // the rank of replica 0
     for (int64_t c = 0; c < RS; ++c)
       if (item[c] < E) new_expert_to_rank[item[c]] = (int32_t)(c / S);
   if (new_rank_loads)

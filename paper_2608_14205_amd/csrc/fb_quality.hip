@@ -199,11 +199,119 @@ int launch_cosine(const void* a, const void* b, int64_t rows, int32_t cols, int6
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
 }
 
+// Rank loads of a replicated placement: slot value v = e + E * j is replica j of expert e, which
+// carries floor(n_e / c_e) tokens plus one if j < n_e mod c_e (c_e = replicas of e).  One workgroup
+// checks the placement rules (values in range, every expert present, the ordinals of every expert
+// exactly 0 .. c_e - 1, no rank with two replicas of one expert, counts >= 0) and sums the shares per
+// rank in LDS; a violated rule makes *max_mean = -1.  R * S <= FB_MAX_SLOTS_TOTAL and E <= R * S.
+namespace {
+__global__ __launch_bounds__(kQThreads) void slot_fold_kernel(
+    const int32_t* __restrict__ counts, int32_t E, const int32_t* __restrict__ slots, int32_t R,
+    int32_t S, int32_t* __restrict__ rank_loads, double* __restrict__ max_mean) {
+  __shared__ int32_t reps[FB_MAX_SLOTS_TOTAL];   // replicas per expert
+  __shared__ int32_t base[FB_MAX_SLOTS_TOTAL];   // exclusive prefix sum of reps
+  __shared__ int32_t seen[FB_MAX_SLOTS_TOTAL];   // one flag per (expert, ordinal), at base[e] + j
+  __shared__ int32_t sexp[FB_MAX_SLOTS_TOTAL];   // expert of every slot, -1 if empty or invalid
+  __shared__ int32_t rl[FB_MAX_RANKS];
+  __shared__ int32_t part[kQThreads];
+  __shared__ int32_t s_bad;
+  __shared__ long long s_mx[kQWaves], s_sum[kQWaves];
+  const int tid = threadIdx.x;
+  const int RS = R * S;
+  if (tid == 0) s_bad = 0;
+  for (int e = tid; e < E; e += kQThreads) reps[e] = 0;
+  for (int c = tid; c < RS; c += kQThreads) seen[c] = 0;
+  for (int r = tid; r < R; r += kQThreads) rl[r] = 0;
+  __syncthreads();
+  for (int c = tid; c < RS; c += kQThreads) {
+    const int v = slots[c];
+    int e = -1;
+    if (v != -1) {
+      if (v < 0 || v / E >= R) {
+        s_bad = 1;
+      } else {
+        e = v % E;
+        atomicAdd(&reps[e], 1);
+      }
+    }
+    sexp[c] = e;
+  }
+  __syncthreads();
+  // exclusive prefix sum of reps: each thread sums a contiguous chunk, thread 0 scans the chunks
+  const int chunk = (E + kQThreads - 1) / kQThreads;
+  const int e0 = tid * chunk, e1 = e0 + chunk < E ? e0 + chunk : E;
+  int acc = 0;
+  for (int e = e0; e < e1; ++e) acc += reps[e];
+  part[tid] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int t = 0; t < kQThreads; ++t) {
+      const int x = part[t];
+      part[t] = run;
+      run += x;
+    }
+  }
+  __syncthreads();
+  acc = part[tid];
+  for (int e = e0; e < e1; ++e) {
+    base[e] = acc;
+    acc += reps[e];
+    if (reps[e] == 0 || counts[e] < 0) s_bad = 1;
+  }
+  __syncthreads();
+  for (int c = tid; c < RS; c += kQThreads) {
+    const int e = sexp[c];
+    if (e < 0) continue;
+    const int j = slots[c] / E;
+    // base[e] + j stays below base[e] + reps[e] <= RS only when j < reps[e]
+    if (j >= reps[e] || atomicAdd(&seen[base[e] + j], 1) != 0) {
+      s_bad = 1;
+      continue;
+    }
+    // no other slot of the same rank holds this expert
+    const int r0 = (c / S) * S;
+    for (int c2 = r0; c2 < c; ++c2)
+      if (sexp[c2] == e) s_bad = 1;
+    const int n = counts[e], k = reps[e];
+    atomicAdd(&rl[c / S], n / k + (j < n % k ? 1 : 0));
+  }
+  __syncthreads();
+  long long mx = 0, sum = 0;
+  for (int r = tid; r < R; r += kQThreads) {
+    const int v = rl[r];
+    rank_loads[r] = v;
+    mx = v > mx ? v : mx;
+    sum += v;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const long long om = __shfl_xor(mx, off), os = __shfl_xor(sum, off);
+    mx = om > mx ? om : mx;
+    sum += os;
+  }
+  if ((tid & 63) == 0) { s_mx[tid >> 6] = mx; s_sum[tid >> 6] = sum; }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < kQWaves; ++w) { mx = s_mx[w] > mx ? s_mx[w] : mx; sum += s_sum[w]; }
+    *max_mean = s_bad ? -1.0 : (sum == 0 ? 1.0 : (double)mx * (double)R / (double)sum);
+  }
+}
+}  // namespace
+
 int launch_fold(const int32_t* counts, int32_t E, const int32_t* e2r, int32_t R, int32_t* rank_loads,
                 double* max_mean, void* stream) {
   (void)hipGetLastError();
   hipLaunchKernelGGL(fold_kernel, dim3(1), dim3(kQThreads), 0, static_cast<hipStream_t>(stream), counts,
                      E, e2r, R, rank_loads, max_mean);
+  return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
+}
+
+int launch_slot_fold(const int32_t* counts, int32_t E, const int32_t* slots, int32_t R, int32_t S,
+                     int32_t* rank_loads, double* max_mean, void* stream) {
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(slot_fold_kernel, dim3(1), dim3(kQThreads), 0, static_cast<hipStream_t>(stream),
+                     counts, E, slots, R, S, rank_loads, max_mean);
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
 }
 

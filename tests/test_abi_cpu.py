@@ -15,6 +15,7 @@ import paper_2608_14205_amd as fb
 from paper_2608_14205_amd import _lib as L
 from oracle import cost as OC
 from oracle import planner as OP
+from workloads import random_replicated_placement
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "freebalance.h")
@@ -34,7 +35,8 @@ def test_header_declares_the_boundary():
                             "fb_plan_swaps", "fb_plan_swaps_device", "fb_swap_budget_from_cost",
                             "fb_topk_hits", "fb_cosine_workspace_bytes", "fb_row_cosine_mean",
                             "fb_fold_rank_loads", "fb_plan_swaps_timed",
-                            "fb_plan_swaps_timed_device", "fb_predict_split_workspace_bytes"])
+                            "fb_plan_swaps_timed_device", "fb_predict_split_workspace_bytes",
+                            "fb_fold_slot_loads"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -167,6 +169,69 @@ def test_host_planner_rejects_bad_placement(bad):
     with pytest.raises(fb.FreeBalanceError) as ei:
         fb.plan_swaps(counts, slots, fb.Budget(1))
     assert ei.value.status == L.FB_EINVAL
+
+
+def test_host_planner_hand_worked_replicated_plans(golden_dir):
+    with open(os.path.join(golden_dir, "planner_replicas_hand.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        h = _host(c["counts"], c["slots"], max_swaps=c["max_swaps"], mode=c["mode"])
+        assert [list(s) for s in h.swaps] == c["swaps"], c["name"]
+        assert h.slots.tolist() == c["new_slots"], c["name"]
+        assert h.rank_loads.tolist() == c["rank_loads"], c["name"]
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.integers(2, 6), st.integers(1, 5), st.integers(0, 10 ** 9), st.integers(0, 6),
+       st.sampled_from(["frontier", "full"]), st.integers(0, 3), st.integers(0, 4),
+       st.sampled_from([None, (0, 1), (1, 7)]), st.booleans())
+def test_host_planner_matches_oracle_on_replicated_placements(R, S, seed, B, mode, cap, tau, gamma,
+                                                              timed):
+    g = np.random.default_rng(seed)
+    got = random_replicated_placement(g, R, S)
+    if got is None:
+        return
+    slots, E = got
+    counts = (g.integers(0, 40, size=E) * (g.random(E) < 0.9)).astype(np.int32)
+    kw = dict(gamma=gamma, tau=tau, mode=mode, per_rank_cap=cap)
+    if timed:
+        cm = OC.CostModel(g.integers(0, 2, size=R).tolist(), g.integers(0, 400, size=E).tolist(),
+                          (int(g.integers(1, 50)), int(g.integers(1, 200))),
+                          (int(g.integers(100, 2000)), int(g.integers(20, 400))),
+                          int(g.integers(0, 12000)), None)
+        ref = OP.plan_swaps(counts, slots, B, cost=cm, **kw)
+        host = fb.plan_swaps_timed(counts, slots, fb.Budget(B, **kw), fb.CostModel(*cm))
+        assert host.costs == ref.costs
+    else:
+        ref = OP.plan_swaps(counts, slots, B, **kw)
+        host = _host(counts, slots, max_swaps=B, **kw)
+    _same(host, ref)
+
+
+@pytest.mark.parametrize("slots", [
+    [[0, 1], [0, -1]],      # replica 0 of expert 0 twice
+    [[0, 1], [4, -1]],      # replica 2 of expert 0 without replica 1
+    [[0, 2], [1, -1]],      # two replicas of expert 0 on rank 0
+    [[0, 1], [2, 4]],       # ordinal 2 reaches R = 2
+])
+def test_host_planner_rejects_bad_replicated_placement(slots):
+    for call in (lambda: fb.plan_swaps([3, 1], slots, fb.Budget(1)),
+                 lambda: fb.plan_swaps_timed([3, 1], slots, fb.Budget(1),
+                                             fb.CostModel([0, 0], [1, 1], (1, 1), (1, 1), 10))):
+        with pytest.raises(fb.FreeBalanceError) as ei:
+            call()
+        assert ei.value.status == L.FB_EINVAL
+
+
+def test_slot_fold_validation_without_gpu():
+    lib = fb.lib()
+    p = ctypes.c_void_p(16)
+    assert lib.fb_fold_slot_loads(None, 2, p, 2, 2, p, p, None) == L.FB_EINVAL
+    assert lib.fb_fold_slot_loads(p, 0, p, 2, 2, p, p, None) == L.FB_EINVAL
+    assert lib.fb_fold_slot_loads(p, 2, p, 2, 0, p, p, None) == L.FB_EINVAL
+    assert lib.fb_fold_slot_loads(p, 5, p, 2, 2, p, p, None) == L.FB_EINVAL       # E > R * S
+    assert lib.fb_fold_slot_loads(p, 2, p, 1025, 1, p, p, None) == L.FB_EUNSUPPORTED
+    assert lib.fb_fold_slot_loads(p, 2, p, 64, 65, p, p, None) == L.FB_EUNSUPPORTED
 
 
 def test_host_planner_argument_checks():

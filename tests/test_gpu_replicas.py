@@ -1,0 +1,127 @@
+"""Replicated placements on MI355X: fb_fold_slot_loads against the oracle, the planners on a
+replicated placement, and the predicted-then-planned path of the "EPLB + Ours" setting."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_14205_amd as fb
+from oracle import planner as OP
+from oracle import predictor as OPR
+from oracle import replicas as RP
+from workloads import (CONFIGS, contiguous_placement, make_layer, random_replicated_placement,
+                       replicated_placement, truncated_zipf_probs)
+from gpu_util import run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _fold(counts, slots):
+    c = torch.from_numpy(np.ascontiguousarray(counts, np.int32)).cuda()
+    s = torch.from_numpy(np.ascontiguousarray(slots, np.int32)).cuda()
+    loads, mm = fb.fold_slot_loads(c, s)
+    torch.cuda.synchronize()
+    return loads.cpu().numpy().astype(np.int64), float(mm.item())
+
+
+def test_slot_fold_random_placements():
+    _say("[replicas] slot fold, random placements")
+    g = np.random.default_rng(11)
+    n = 0
+    for _ in range(150):
+        R = int(g.integers(1, 17))
+        S = int(g.integers(1, 9))
+        got = random_replicated_placement(g, R, S)
+        if got is None:
+            continue
+        slots, E = got
+        counts = (g.integers(0, 5000, size=E) * (g.random(E) < 0.9)).astype(np.int32)
+        loads, mm = _fold(counts, slots)
+        ref = RP.slot_rank_loads(counts, slots)
+        assert np.array_equal(loads, ref), (R, S, E)
+        assert mm == OPR.max_to_mean(ref)
+        n += 1
+    assert n > 100
+
+
+@pytest.mark.parametrize("R,S,E,s", [(8, 2, 8, 1.2), (32, 9, 256, 1.1), (32, 8, 128, 1.0),
+                                     (1024, 4, 4000, 1.1)])
+def test_slot_fold_history_placements(R, S, E, s):
+    # placements that replicate the most popular experts into the spare slots; the largest case
+    # fills every slot the fold accepts (R * S = 4096)
+    _say(f"[replicas] slot fold R={R} S={S} E={E}")
+    slots = replicated_placement(truncated_zipf_probs(s, E), R, S)
+    g = np.random.default_rng(R * S + E)
+    counts = g.integers(0, 20000, size=E).astype(np.int32)
+    loads, mm = _fold(counts, slots)
+    ref = RP.slot_rank_loads(counts, slots)
+    assert np.array_equal(loads, ref)
+    assert mm == OPR.max_to_mean(ref)
+
+
+def test_slot_fold_plain_placement_equals_rank_fold():
+    wl = CONFIGS["dsv3"]
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    counts = np.random.default_rng(3).integers(0, 3000, size=wl.E).astype(np.int32)
+    loads, mm = _fold(counts, slots)
+    ref = OPR.rank_loads(counts, e2r, wl.R)
+    assert np.array_equal(loads, ref)
+    assert mm == OPR.max_to_mean(ref)
+
+
+@pytest.mark.parametrize("slots,counts", [
+    ([[0, 1], [0, -1]], [3, 1]),     # replica 0 of expert 0 twice
+    ([[0, 1], [4, -1]], [3, 1]),     # replica 2 of expert 0 without replica 1
+    ([[0, 2], [1, -1]], [3, 1]),     # two replicas of expert 0 on rank 0
+    ([[0, 1], [2, 4]], [3, 1]),      # ordinal 2 reaches R = 2
+    ([[0, -1], [-1, -1]], [3, 1]),   # expert 1 missing
+    ([[0, -2], [1, -1]], [3, 1]),    # invalid value
+    ([[0, 1], [2, -1]], [3, -1]),    # negative count
+])
+def test_slot_fold_flags_broken_placements(slots, counts):
+    _, mm = _fold(counts, slots)
+    assert mm == -1.0
+
+
+def test_device_planner_refuses_replicated_placements():
+    slots = np.array([[0, 1], [2, -1]], np.int32)     # replica 1 of expert 0 on rank 1
+    c = torch.tensor([6, 2], dtype=torch.int32, device="cuda")
+    s = torch.from_numpy(slots).cuda()
+    for mode in ("frontier", "full"):
+        plan = fb.plan_swaps_device(c, s, fb.Budget(2, mode=mode))
+        torch.cuda.synchronize()
+        assert int(plan.status.item()) == fb._lib.FB_EUNSUPPORTED
+        assert int(plan.n_swaps.item()) == 0
+
+
+@pytest.mark.parametrize("name,S_extra,budget", [("mixtral", 0, 4), ("dsv3", 1, 8)])
+def test_predicted_counts_planned_on_a_replicated_placement(name, S_extra, budget):
+    """The "EPLB + Ours" path: counts predicted on the GPU, folded on the GPU under a placement that
+    replicates popular experts, planned by the host planner (= oracle), and the plan's loads equal
+    the GPU fold of the new slot table."""
+    wl = CONFIGS[name].with_T(4096)
+    S = wl.S + S_extra
+    _say(f"[replicas] {name} T={wl.T} R={wl.R} S={S}")
+    slots = replicated_placement(truncated_zipf_probs(wl.zipf_s[0], wl.E), wl.R, S)
+    _, e2r = contiguous_placement(wl.E, wl.R, wl.S) if wl.E % wl.R == 0 else (None, None)
+    li = make_layer(wl, 2)
+    got = run_gpu(li, wl, e2r, debug=False, packed=True)
+    counts = got["counts"].astype(np.int32)
+    loads, mm = _fold(counts, slots)
+    ref_loads = RP.slot_rank_loads(counts, slots)
+    assert np.array_equal(loads, ref_loads)
+    for mode in ("frontier", "full"):
+        host = fb.plan_swaps(counts, slots, fb.Budget(budget, mode=mode))
+        ref = OP.plan_swaps(counts, slots, budget, mode=mode)
+        assert [tuple(s) for s in host.swaps] == [tuple(s) for s in ref.swaps]
+        assert np.array_equal(host.slots, ref.slots)
+        after, mm_after = _fold(counts, host.slots)
+        assert np.array_equal(after, host.rank_loads)
+        assert mm_after <= mm
+        _say(f"[replicas] {name} {mode}: {len(host.swaps)} swaps, max/mean {mm:.4f} -> {mm_after:.4f}")

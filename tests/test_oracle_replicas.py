@@ -20,6 +20,7 @@ from hypothesis import strategies as st
 
 from oracle import planner as PL
 from oracle import replicas as RP
+from workloads import random_replicated_placement
 
 
 def _cases(golden_dir):
@@ -47,36 +48,11 @@ def test_shares_follow_round_robin_dispatch(n, c):
     assert [RP.replica_share(n, c, j) for j in range(c)] == got
 
 
-def _random_replicated(g, R, S, max_tries=50):
-    """A random valid replicated placement: E experts, replica counts c_e <= R, no two replicas of
-    one expert on one rank, and some empty slots."""
-    for _ in range(max_tries):
-        E = int(g.integers(1, R * S + 1))
-        c = [1] * E
-        spare = int(g.integers(0, R * S - E + 1))
-        for _ in range(spare):
-            e = int(g.integers(0, E))
-            if c[e] < R:
-                c[e] += 1
-        items = [(e, j) for e in range(E) for j in range(c[e])]
-        g.shuffle(items)
-        table = np.full((R, S), -1, dtype=np.int64)
-        fill = [0] * R
-        ok = True
-        for e, j in items:
-            ranks = [r for r in range(R) if fill[r] < S and
-                     all(v < 0 or v % E != e for v in table[r])]
-            if not ranks:
-                ok = False
-                break
-            r = ranks[int(g.integers(0, len(ranks)))]
-            table[r, fill[r]] = e + E * j
-            fill[r] += 1
-        if ok:
-            for r in range(R):
-                table[r] = table[r][g.permutation(S)]
-            return table, E
-    pytest.skip("no valid placement drawn")
+def _random_replicated(g, R, S):
+    got = random_replicated_placement(g, R, S)
+    if got is None:
+        pytest.skip("no valid placement drawn")
+    return got
 
 
 @settings(max_examples=120, deadline=None)

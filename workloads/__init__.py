@@ -12,6 +12,8 @@ from .synth import (  # noqa: F401
     bf16_bits_from_f32,
     contiguous_placement,
     make_layer,
+    random_replicated_placement,
+    replicated_placement,
     rng,
     sweep_workload,
     truncated_zipf_probs,

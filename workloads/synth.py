@@ -137,6 +137,82 @@ def contiguous_placement(E: int, R: int, S: int) -> Tuple[np.ndarray, np.ndarray
     return slots, e2r
 
 
+def random_replicated_placement(g: np.random.Generator, R: int, S: int,
+                                max_tries: int = 50) -> Optional[Tuple[np.ndarray, int]]:
+    """A random replicated slot table (value e + E * j = replica j of expert e, -1 = empty): a
+    random E <= R * S, random extra replicas (at most R per expert), replicas placed on random ranks
+    with a free slot and no replica of the same expert.  Returns (table int32 R x S, E), or None if
+    no draw succeeds."""
+    for _ in range(max_tries):
+        E = int(g.integers(1, R * S + 1))
+        c = [1] * E
+        for _ in range(int(g.integers(0, R * S - E + 1))):
+            e = int(g.integers(0, E))
+            if c[e] < R:
+                c[e] += 1
+        items = [(e, j) for e in range(E) for j in range(c[e])]
+        g.shuffle(items)
+        table = np.full((R, S), -1, dtype=np.int32)
+        fill = [0] * R
+        holds = [set() for _ in range(R)]
+        ok = True
+        for e, j in items:
+            ranks = [r for r in range(R) if fill[r] < S and e not in holds[r]]
+            if not ranks:
+                ok = False
+                break
+            r = ranks[int(g.integers(0, len(ranks)))]
+            table[r, fill[r]] = e + E * j
+            fill[r] += 1
+            holds[r].add(e)
+        if ok:
+            for r in range(R):
+                table[r] = table[r][g.permutation(S)]
+            return table, E
+    return None
+
+
+def replicated_placement(popularity: Sequence[float], R: int, S: int) -> np.ndarray:
+    """Stand-in for a history-driven placement that replicates hot experts (the starting point of
+    the paper's "EPLB + Ours" runs; not that system's algorithm).  ``popularity`` is the expected
+    share of tokens of every expert (here the cluster frequencies of the input recipe).  The
+    R * S - E spare slots take one extra replica each of the most popular experts (again from the
+    top while slots remain, at most R replicas per expert); then the replicas, heaviest first
+    (popularity / replicas, ties to the lower expert and ordinal), go to the rank with the least
+    popularity placed so far (lowest rank on ties) that has a free slot and no replica of that expert.
+    Returns the slot table (value e + E * j = replica j of expert e)."""
+    pop = np.asarray(popularity, dtype=np.float64)
+    E = pop.size
+    if E > R * S:
+        raise ValueError("more experts than slots")
+    order = sorted(range(E), key=lambda e: (-pop[e], e))
+    c = [1] * E
+    spare = R * S - E
+    while spare > 0 and any(v < R for v in c):
+        for e in order:
+            if spare == 0:
+                break
+            if c[e] < R:
+                c[e] += 1
+                spare -= 1
+    items = sorted(((pop[e] / c[e], e, j) for e in range(E) for j in range(c[e])),
+                   key=lambda t: (-t[0], t[1], t[2]))
+    table = np.full((R, S), -1, dtype=np.int32)
+    fill = [0] * R
+    placed = [0.0] * R
+    holds = [set() for _ in range(R)]
+    for w, e, j in items:
+        ranks = [r for r in range(R) if fill[r] < S and e not in holds[r]]
+        if not ranks:
+            raise ValueError("no rank can take the replica")
+        r = min(ranks, key=lambda q: (placed[q], q))
+        table[r, fill[r]] = e + E * j
+        fill[r] += 1
+        placed[r] += w
+        holds[r].add(e)
+    return table
+
+
 @dataclasses.dataclass
 class LayerInputs:
     """One layer's inputs.  ``x`` / ``h_target`` / ``w`` hold bf16 bit patterns (uint16) for bf16
