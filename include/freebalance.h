@@ -329,9 +329,10 @@ int fb_plan_swaps(const int32_t* counts, int32_t E, const int32_t* slot_expert, 
  *   new_expert_to_rank    device int32[E] out (required).
  *   new_rank_loads        device int64[R] out (required).
  *   status                device int32 out: FB_OK, or FB_EINVAL if the slot table is invalid or a
- *                         count is negative, or FB_EUNSUPPORTED for a replicated placement (a value
- *                         >= E; the host planners take those); then the plan is empty and the
- *                         placement unchanged. */
+ *                         count is negative, or FB_EUNSUPPORTED if a replicated placement's item
+ *                         ids do not fit the tie keys (E * max c_e + R * S > 2^21); then the plan
+ *                         is empty and the placement unchanged.
+ * Replicated placements are planned exactly as by fb_plan_swaps. */
 int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_expert, int32_t R,
                          int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
                          int32_t* new_slot_expert, int32_t* new_expert_to_rank,

@@ -23,6 +23,12 @@
 // every candidate also costs C = alpha + ceil(bytes * 1000 / beta) ns on its link, must fit what is
 // left of both ranks' and the link's budgets, and the best candidate is the largest benefit / C,
 // compared exactly as gain_1 * C_2 vs gain_2 * C_1 (gains < 2^63, costs < 2^42), then the tie key.
+//
+// Replicated placements (slot value v = e + E * j is replica j of expert e, as in the host planner):
+// an item's id is its slot value, or V + c for the empty slot c (V = E * J, J the largest replica
+// count; V = E without replicas), its load is its token share floor(n_e / c_e) + [j < n_e mod c_e],
+// held with the item in its slot, and a candidate may not put a replica on a rank that holds
+// another replica of the same expert.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -34,7 +40,8 @@ namespace {
 constexpr int kMaxRS = FB_MAX_SLOTS_TOTAL;
 constexpr int kMaxR = FB_MAX_RANKS;
 constexpr int kRankBits = 11;                 // R <= 1024 < 2^11
-constexpr int kItemBits = 13;                 // item ids < E + R * S <= 8192
+constexpr int kItemBits = 21;                 // item ids < V + R * S <= 2^21 (checked)
+constexpr int kSmallItemBits = 13;            // ... < E + R * S <= 8192 without replicas
 constexpr int64_t kLoadCap = (int64_t)1 << 43;  // loads <= 4096 experts * (2^31 - 1) < 2^43
 
 template <int CTRL>
@@ -81,16 +88,21 @@ __device__ __forceinline__ uint64_t tie_key(int a, int b, int i, int j) {
 }
 
 struct Shared {
-  int32_t item[kMaxRS];          // slot -> item (expert id, or E + slot for an empty slot)
-  int32_t pos[2 * kMaxRS];       // item -> slot
-  int32_t cnt[kMaxRS];           // expert -> count
-  int32_t seen[kMaxRS];
+  int32_t item[kMaxRS];          // slot -> item id (slot value, or V + slot for an empty slot)
+  int32_t sload[kMaxRS];         // slot -> load (token share) of its item
+  uint8_t mslot[kMaxRS];         // slot -> its item has moved
+  union {
+    struct {                     // placement check
+      int32_t reps[kMaxRS], base[kMaxRS], flag[kMaxRS];
+    } chk;
+    int64_t ebytes[kMaxRS];      // expert sizes (time budget), loaded after the check
+  } u;
+  int32_t scan[1024];
   int64_t L[kMaxR];
   int32_t part[kMaxR];
-  uint8_t moved[2 * kMaxRS];
   uint64_t wgain[16], wtie[16], wcost[16];
   int64_t N;
-  int32_t bad, stop, amax, amin, top[3], ns;
+  int32_t bad, stop, amax, amin, top[3], ns, J;
   int64_t other;
   // time budget: what is left of every rank's budget, rank nodes, and the accepted swaps' links
   // and costs (the link budgets are charged by scanning them)
@@ -98,8 +110,77 @@ struct Shared {
   int32_t node[kMaxR];
   int32_t acc_pair[kMaxTimedSwaps];   // a * kMaxR + b, a < b
   int64_t acc_cost[kMaxTimedSwaps];
-  int64_t ebytes[kMaxRS];             // expert sizes
 };
+
+// Placement check of both kernels (all NT threads of the workgroup call it): every value is -1 or
+// e + E * j with j < R, every expert has replicas 0 .. c_e - 1 each once, no rank holds two replicas
+// of one expert, every count is >= 0.  A violation sets bit 0 of *bad (zeroed by the caller before
+// the call).  On return, after a barrier, reps[e] = c_e and *jmax = the largest c_e.
+template <int NT>
+__device__ void check_placement(const PlanDeviceLaunch& a, int32_t* reps, int32_t* base,
+                                int32_t* flag, int32_t* scan, int32_t* bad, int32_t* jmax) {
+  const int tid = threadIdx.x;
+  const int E = a.E, R = a.R, S = a.S, RS = R * S;
+  for (int e = tid; e < E; e += NT) reps[e] = 0;
+  for (int c = tid; c < RS; c += NT) flag[c] = 0;
+  if (tid == 0) *jmax = 1;
+  __syncthreads();
+  for (int c = tid; c < RS; c += NT) {
+    const int v = a.slot_expert[c];
+    if (v == -1) continue;
+    if (v < 0 || v / E >= R) atomicOr(bad, 1);
+    else atomicAdd(&reps[v % E], 1);
+  }
+  __syncthreads();
+  // exclusive prefix sum of reps: chunk sums, one thread scans the NT partials
+  const int chunk = (E + NT - 1) / NT;
+  const int e0 = tid * chunk, e1 = e0 + chunk < E ? e0 + chunk : E;
+  int acc = 0, jm = 1;
+  for (int e = e0; e < e1; ++e) acc += reps[e];
+  scan[tid] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int t = 0; t < NT; ++t) {
+      const int x = scan[t];
+      scan[t] = run;
+      run += x;
+    }
+  }
+  __syncthreads();
+  acc = scan[tid];
+  for (int e = e0; e < e1; ++e) {
+    base[e] = acc;
+    acc += reps[e];
+    if (reps[e] == 0 || a.counts[e] < 0) atomicOr(bad, 1);
+    jm = reps[e] > jm ? reps[e] : jm;
+  }
+  atomicMax(jmax, jm);
+  __syncthreads();
+  for (int c = tid; c < RS; c += NT) {
+    const int v = a.slot_expert[c];
+    if (v < 0 || v / E >= R) continue;           // empty, or flagged above
+    const int e = v % E, j = v / E;
+    // base[e] + j < base[e] + reps[e] <= R * S only when j < reps[e]
+    if (j >= reps[e] || atomicAdd(&flag[base[e] + j], 1) != 0) {
+      atomicOr(bad, 1);
+      continue;
+    }
+    for (int c2 = (c / S) * S; c2 < c; ++c2) {
+      const int v2 = a.slot_expert[c2];
+      if (v2 >= 0 && v2 % E == e) atomicOr(bad, 1);
+    }
+  }
+  __syncthreads();
+}
+
+// Token share of the replica with slot value v (0 <= v, v / E < c_e).
+__device__ __forceinline__ int32_t replica_share(int v, int E, const int32_t* counts,
+                                                 const int32_t* reps) {
+  const int e = v % E, j = v / E;
+  const int n = counts[e], k = reps[e];
+  return n / k + (j < n % k ? 1 : 0);
+}
 
 // ceil(num / beta) for 0 <= num < 2^52 and 1 <= beta <= 2^40, exactly: a double-precision
 // quotient is within one of the truncated one (its relative error is below 2^-51), and one
@@ -112,11 +193,12 @@ __device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t beta, double in
   return q + (r > 0 ? 1 : 0);
 }
 
-// Eq. 9 in whole nanoseconds for a swap of items i (rank a) and j (rank b).
+// Eq. 9 in whole nanoseconds for a swap moving expert ei off rank ra and expert ej off rank rb
+// (-1: an empty slot, which transfers nothing).
 __device__ __forceinline__ int64_t swap_cost(const PlanDeviceLaunch& a, const Shared& sh, int ra,
-                                             int rb, int i, int j) {
+                                             int rb, int ei, int ej) {
   const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
-  const int64_t bytes = (i < a.E ? sh.ebytes[i] : 0) + (j < a.E ? sh.ebytes[j] : 0);
+  const int64_t bytes = (ei >= 0 ? sh.u.ebytes[ei] : 0) + (ej >= 0 ? sh.u.ebytes[ej] : 0);
   const int64_t beta = a.cost.beta_bytes_per_us[t];
   return a.cost.alpha_ns[t] + ceil_div(bytes * 1000, beta, 1.0 / (double)beta);
 }
@@ -160,44 +242,54 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   const fb_budget bg = a.budget;
 
   if (tid == 0) { sh.bad = 0; sh.ns = 0; sh.N = 0; }
-  for (int e = tid; e < E; e += NT) { sh.seen[e] = 0; sh.cnt[e] = a.counts[e]; }
-  for (int c = tid; c < E + RS; c += NT) sh.moved[c] = 0;
   for (int r = tid; r < R; r += NT) sh.part[r] = 0;
   if (a.timed)
     for (int r = tid; r < R; r += NT) { sh.node[r] = a.rank_node[r]; sh.rank_left[r] = a.cost.rank_budget_ns; }
-  __syncthreads();
+  check_placement<NT>(a, sh.u.chk.reps, sh.u.chk.base, sh.u.chk.flag, sh.scan, &sh.bad, &sh.J);
+  // bit 0 of bad: an invalid table or count; bit 1: item ids that would not fit the tie keys
+  const int J = sh.J;
+  const int V = E * J;                       // slot values are below V; empty-slot ids from V
+  if (!sh.bad) {
+    if ((int64_t)V + RS > ((int64_t)1 << kItemBits)) {
+      if (tid == 0) sh.bad = 2;
+    } else {
+      for (int c = tid; c < RS; c += NT) {
+        const int v = a.slot_expert[c];
+        sh.item[c] = v >= 0 ? v : V + c;
+        sh.sload[c] = v >= 0 ? replica_share(v, E, a.counts, sh.u.chk.reps) : 0;
+        sh.mslot[c] = 0;
+      }
+    }
+  }
+  __syncthreads();                           // the check's arrays are dead from here on
   if (a.timed)
     for (int e = tid; e < E; e += NT) {
       const int64_t b = a.expert_bytes[e];
-      sh.ebytes[e] = b;
+      sh.u.ebytes[e] = b;
       if (b < 0 || b > kCostLimit) atomicOr(&sh.bad, 1);
     }
-  // bit 0 of bad: an invalid table or count; bit 1: a replica (value >= E), which the device planner
-  // does not take
-  for (int c = tid; c < RS; c += NT) {
-    const int e = a.slot_expert[c];
-    if (e == -1) { sh.item[c] = E + c; sh.pos[E + c] = c; }
-    else if (e < 0) atomicOr(&sh.bad, 1);
-    else if (e >= E) atomicOr(&sh.bad, 2);
-    else { sh.item[c] = e; sh.pos[e] = c; atomicAdd(&sh.seen[e], 1); }
-  }
-  __syncthreads();
-  for (int e = tid; e < E; e += NT)
-    if (sh.seen[e] != 1 || sh.cnt[e] < 0) atomicOr(&sh.bad, 1);
   __syncthreads();
   if (sh.bad) {
-    if (tid == 0) { *a.n_swaps = 0; *a.status = (sh.bad & 2) ? FB_EUNSUPPORTED : FB_EINVAL; }
+    if (tid == 0) { *a.n_swaps = 0; *a.status = (sh.bad & 1) ? FB_EINVAL : FB_EUNSUPPORTED; }
     return;
   }
 
-  auto load_of = [&](int it) -> int64_t { return it < E ? (int64_t)sh.cnt[it] : 0; };
   for (int r = tid; r < R; r += NT) {
     int64_t v = 0;
-    for (int s = 0; s < S; ++s) v += load_of(sh.item[r * S + s]);
+    for (int s = 0; s < S; ++s) v += sh.sload[r * S + s];
     sh.L[r] = v;
     atomicAdd((unsigned long long*)&sh.N, (unsigned long long)v);
   }
   __syncthreads();
+  // does rank r hold a replica of the expert of item it (a replica id below V)?
+  auto holds = [&](int r, int it) -> bool {
+    const int e = it % E;
+    for (int s = 0; s < S; ++s) {
+      const int x = sh.item[r * S + s];
+      if (x < V && x % E == e) return true;
+    }
+    return false;
+  };
   const int64_t N = sh.N;
   int64_t g_num = bg.gamma_num, g_den = bg.gamma_den;
   if (g_den == 0) { g_num = N > 0 ? 1 : 0; g_den = N > 0 ? N : 1; }
@@ -255,10 +347,12 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
     uint64_t bgain = 0, btie = 0;     // gain 0: nothing found (every accepted gain is > 0)
     uint64_t bcost = 1;
     auto consider = [&](int ra, int rb, int p, int q, int64_t other) {
-      const int i = sh.item[ra * S + p], j = sh.item[rb * S + q];
-      if (sh.moved[i] || sh.moved[j] || (i >= E && j >= E)) return;
+      const int sa = ra * S + p, sb = rb * S + q;
+      const int i = sh.item[sa], j = sh.item[sb];
+      if (sh.mslot[sa] || sh.mslot[sb] || (i >= V && j >= V)) return;
+      if (J > 1 && ((i < V && holds(rb, i)) || (j < V && holds(ra, j)))) return;
       const int64_t La = sh.L[ra], Lb = sh.L[rb];
-      const int64_t d = load_of(j) - load_of(i);
+      const int64_t d = (int64_t)sh.sload[sb] - (int64_t)sh.sload[sa];
       const int64_t la = La + d, lb = Lb - d;
       int64_t m2 = la > lb ? la : lb;
       if (other > m2) m2 = other;
@@ -267,7 +361,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       if (gain <= 0) return;
       const uint64_t tk = tie_key(ra, rb, i, j);
       if (a.timed) {
-        const int64_t c = swap_cost(a, sh, ra, rb, i, j);
+        const int64_t c = swap_cost(a, sh, ra, rb, i < V ? i % E : -1, j < V ? j % E : -1);
         if (!swap_fits(a, sh, ra, rb, c)) return;
         if (ratio_better((uint64_t)gain, (uint64_t)c, tk, bgain, bcost, btie)) {
           bgain = (uint64_t)gain; bcost = (uint64_t)c; btie = tk;
@@ -335,18 +429,23 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       const int cb = (int)(t >> (2 * kItemBits)) & ((1 << kRankBits) - 1);
       const int ci = (int)(t >> kItemBits) & ((1 << kItemBits) - 1);
       const int cj = (int)t & ((1 << kItemBits) - 1);
-      const int sa = sh.pos[ci], sb = sh.pos[cj];
-      const int64_t d = load_of(cj) - load_of(ci);
-      sh.item[sa] = cj; sh.pos[cj] = sa;
-      sh.item[sb] = ci; sh.pos[ci] = sb;
+      int sa = ca * S, sb = cb * S;               // the winning items' slots (ids are unique)
+      for (int s = 0; s < S; ++s) {
+        if (sh.item[ca * S + s] == ci) sa = ca * S + s;
+        if (sh.item[cb * S + s] == cj) sb = cb * S + s;
+      }
+      const int32_t li = sh.sload[sa], lj = sh.sload[sb];
+      const int64_t d = (int64_t)lj - (int64_t)li;
+      sh.item[sa] = cj; sh.sload[sa] = lj;
+      sh.item[sb] = ci; sh.sload[sb] = li;
       sh.L[ca] += d;
       sh.L[cb] -= d;
-      sh.moved[ci] = 1; sh.moved[cj] = 1;
+      sh.mslot[sa] = 1; sh.mslot[sb] = 1;
       ++sh.part[ca]; ++sh.part[cb];
       fb_swap sw;
       sw.src_rank = ca; sw.dst_rank = cb; sw.src_slot = sa - ca * S; sw.dst_slot = sb - cb * S;
-      sw.expert_src = ci < E ? ci : -1;
-      sw.expert_dst = cj < E ? cj : -1;
+      sw.expert_src = ci < V ? ci : -1;
+      sw.expert_dst = cj < V ? cj : -1;
       sw.gain = (int64_t)g;
       a.swaps[sh.ns] = sw;
       if (a.timed) {
@@ -364,8 +463,8 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   __syncthreads();
   for (int c = tid; c < RS; c += NT) {
     const int it = sh.item[c];
-    a.new_slot_expert[c] = it < E ? it : -1;
-    if (it < E) a.new_expert_to_rank[it] = c / S;
+    a.new_slot_expert[c] = it < V ? it : -1;
+    if (it < E) a.new_expert_to_rank[it] = c / S;   // replica 0
   }
   for (int r = tid; r < R; r += NT) a.new_rank_loads[r] = sh.L[r];
   if (tid == 0) { *a.n_swaps = sh.ns; *a.status = FB_OK; }
@@ -391,8 +490,9 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
              max((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48)));
 }
 
-// Rounds of the one-wave planner when every rank sits in its own lane (R <= 64) and every load fits
-// 31 bits: loads, extremes and tie keys are 32-bit, rank ties are resolved by the lowest lane of a
+// Rounds of the one-wave planner when every rank sits in its own lane (R <= 64), every load fits
+// 31 bits and there are no replicas (item ids below E + R * S <= 8192): loads, extremes and tie keys
+// are 32-bit, rank ties are resolved by the lowest lane of a
 // ballot, and the tie key reduction runs only when two candidates share the best benefit.
 // Returns the number of swaps written.
 __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* slot, int32_t* part,
@@ -432,7 +532,7 @@ __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* sl
       const int64_t spread = g_num ? g_num * (2 * d * (Lmin - M - d)) : 0;
       gain = g_den * (M - m2) + spread;
       ok = !cap_hit && !((ea.x | eb.x) & kMoved) && !(i >= (uint32_t)E && j >= (uint32_t)E) && gain > 0;
-      tk = (i << kItemBits) | j;
+      tk = (i << kSmallItemBits) | j;
     }
     // largest benefit as two 32-bit reductions, then the smallest (i, j) among equal benefits
     const uint32_t ghi = wave_max_u32(ok ? (uint32_t)((uint64_t)gain >> 32) : 0u);
@@ -473,37 +573,28 @@ __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* sl
 // RPL: ranks per lane (R <= 64 * RPL); rank r lives in lane r % 64, register r / 64.
 template <int RPL>
 __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) {
-  __shared__ int32_t cnt[kMaxRS];
-  __shared__ int32_t seen[kMaxRS];
-  __shared__ uint2 slot[kMaxRS];     // x: item id | moved flag, y: the item's count
+  __shared__ int32_t reps[kMaxRS], base[kMaxRS], flag[kMaxRS];   // placement check
+  __shared__ int32_t scan[64];
+  __shared__ uint2 slot[kMaxRS];     // x: item id | moved flag, y: the item's load (token share)
   __shared__ int32_t part[kMaxR];
+  __shared__ int32_t s_bad, s_J;
   const int lane = threadIdx.x;
   const int E = a.E, R = a.R, S = a.S, RS = R * S;
   const fb_budget bg = a.budget;
 
-  // both input tables are fetched before the first wait
-  for (int e = lane; e < E; e += 64) { cnt[e] = a.counts[e]; seen[e] = 0; }
-  for (int c = lane; c < RS; c += 64) slot[c].x = (uint32_t)a.slot_expert[c];
   for (int r = lane; r < R; r += 64) part[r] = 0;
-  __syncthreads();
-  int bad = 0, replica = 0;
-  for (int c = lane; c < RS; c += 64) {
-    const int e = (int)slot[c].x;
-    if (e == -1) slot[c].x = (uint32_t)(E + c);
-    else if (e < 0) bad = 1;
-    else if (e >= E) replica = 1;
-    else atomicAdd(&seen[e], 1);
-  }
-  __syncthreads();
-  for (int e = lane; e < E; e += 64) bad |= (seen[e] != 1) | (cnt[e] < 0);
-  const bool any_replica = __ballot(replica) != 0;
-  if (any_replica || __ballot(bad)) {
-    if (lane == 0) { *a.n_swaps = 0; *a.status = any_replica ? FB_EUNSUPPORTED : FB_EINVAL; }
+  if (lane == 0) s_bad = 0;
+  check_placement<64>(a, reps, base, flag, scan, &s_bad, &s_J);
+  const int J = s_J;
+  const int V = E * J;               // slot values are below V; empty-slot ids from V
+  if (s_bad || (int64_t)V + RS > ((int64_t)1 << kItemBits)) {
+    if (lane == 0) { *a.n_swaps = 0; *a.status = s_bad ? FB_EINVAL : FB_EUNSUPPORTED; }
     return;
   }
   for (int c = lane; c < RS; c += 64) {
-    const uint32_t it = slot[c].x;
-    slot[c].y = it < (uint32_t)E ? cnt[it] : 0;
+    const int v = a.slot_expert[c];
+    slot[c] = v >= 0 ? make_uint2((uint32_t)v, (uint32_t)replica_share(v, E, a.counts, reps))
+                     : make_uint2((uint32_t)(V + c), 0u);
   }
   __syncthreads();
   int64_t Lr[RPL];                   // load of rank lane + 64 m (0 past R)
@@ -533,7 +624,7 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
   bool small_done = false;
   if constexpr (RPL == 1) {
-    if (active && N < (int64_t)0x7fffffff) {
+    if (active && N < (int64_t)0x7fffffff && J == 1) {
       uint32_t Lu = (uint32_t)Lr[0];
       ns = rounds_small(a, slot, part, Lu, g_num, g_den);
       Lr[0] = Lu;
@@ -573,7 +664,17 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
       eb = slot[amin * S + ql];
       const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
       const uint32_t i = ea.x & ~kMovedBit, j = eb.x & ~kMovedBit;
-      const bool ok = !cap_hit && !((ea.x | eb.x) & kMovedBit) && !(i >= (uint32_t)E && j >= (uint32_t)E);
+      bool ok = !cap_hit && !((ea.x | eb.x) & kMovedBit) && !(i >= (uint32_t)V && j >= (uint32_t)V);
+      if (J > 1 && ok) {
+        // no replica may join another replica of its expert
+        const int ei = i < (uint32_t)V ? (int)(i % (uint32_t)E) : -1;
+        const int ej = j < (uint32_t)V ? (int)(j % (uint32_t)E) : -1;
+        for (int s2 = 0; s2 < S; ++s2) {
+          const uint32_t xb = slot[amin * S + s2].x & ~kMovedBit, xa = slot[amax * S + s2].x & ~kMovedBit;
+          if (ei >= 0 && xb < (uint32_t)V && (int)(xb % (uint32_t)E) == ei) ok = false;
+          if (ej >= 0 && xa < (uint32_t)V && (int)(xa % (uint32_t)E) == ej) ok = false;
+        }
+      }
       const int64_t d = (int64_t)(int32_t)eb.y - (int64_t)(int32_t)ea.y;
       const int64_t la = M + d, lb = Lmin - d;
       int64_t m2 = la > lb ? la : lb;
@@ -603,8 +704,8 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
       ++part[amin];
       fb_swap sw;
       sw.src_rank = amax; sw.dst_rank = amin; sw.src_slot = wp; sw.dst_slot = wq;
-      sw.expert_src = wi < E ? wi : -1;
-      sw.expert_dst = wj < E ? wj : -1;
+      sw.expert_src = wi < V ? wi : -1;
+      sw.expert_dst = wj < V ? wj : -1;
       sw.gain = (int64_t)g;
       a.swaps[ns] = sw;
     }
@@ -619,8 +720,8 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
 
   for (int c = lane; c < RS; c += 64) {
     const int it = (int)(slot[c].x & ~kMovedBit);
-    a.new_slot_expert[c] = it < E ? it : -1;
-    if (it < E) a.new_expert_to_rank[it] = c / S;
+    a.new_slot_expert[c] = it < V ? it : -1;
+    if (it < E) a.new_expert_to_rank[it] = c / S;   // replica 0
   }
 #pragma unroll
   for (int m = 0; m < RPL; ++m) {

@@ -1,5 +1,6 @@
-"""Replicated placements on MI355X: fb_fold_slot_loads against the oracle, the planners on a
-replicated placement, and the predicted-then-planned path of the "EPLB + Ours" setting."""
+"""Replicated placements on MI355X: fb_fold_slot_loads against the oracle, the device planners
+against the host planner and the oracle, and the predicted-then-planned path of the "EPLB + Ours"
+setting."""
 import sys
 
 import numpy as np
@@ -89,21 +90,73 @@ def test_slot_fold_flags_broken_placements(slots, counts):
     assert mm == -1.0
 
 
-def test_device_planner_refuses_replicated_placements():
-    slots = np.array([[0, 1], [2, -1]], np.int32)     # replica 1 of expert 0 on rank 1
-    c = torch.tensor([6, 2], dtype=torch.int32, device="cuda")
-    s = torch.from_numpy(slots).cuda()
-    for mode in ("frontier", "full"):
-        plan = fb.plan_swaps_device(c, s, fb.Budget(2, mode=mode))
-        torch.cuda.synchronize()
-        assert int(plan.status.item()) == fb._lib.FB_EUNSUPPORTED
-        assert int(plan.n_swaps.item()) == 0
+def _device(counts, slots, budget, cost=None):
+    c = torch.from_numpy(np.ascontiguousarray(counts, np.int32)).cuda()
+    s = torch.from_numpy(np.ascontiguousarray(slots, np.int32)).cuda()
+    if cost is None:
+        return fb.plan_swaps_device(c, s, budget).to_host()
+    return fb.plan_swaps_timed_device(c, s, budget, cost).to_host()
+
+
+def _same(a, b):
+    assert [tuple(x) for x in a.swaps] == [tuple(x) for x in b.swaps]
+    assert np.array_equal(a.slots, b.slots)
+    assert np.array_equal(a.expert_to_rank, b.expert_to_rank)
+    assert np.array_equal(a.rank_loads, b.rank_loads)
+
+
+@pytest.mark.parametrize("R_max,S_max", [(8, 8), (70, 3), (300, 2), (16, 12)])
+def test_device_planner_replicated_placements(R_max, S_max):
+    """device = host (= oracle on the smaller ones) on random replicated placements, in every launch
+    shape: the one-wave frontier kernel (S * S <= 64, 1 to 16 ranks per lane) and the general kernel
+    (full mode, larger S, time budgets)."""
+    _say(f"[replicas] device planner R <= {R_max}, S <= {S_max}")
+    g = np.random.default_rng(R_max * 100 + S_max)
+    n = 0
+    for it in range(40):
+        R = int(g.integers(2, R_max + 1))
+        S = int(g.integers(1, S_max + 1))
+        got = random_replicated_placement(g, R, S)
+        if got is None:
+            continue
+        slots, E = got
+        counts = (g.integers(0, 3000, size=E) * (g.random(E) < 0.9)).astype(np.int32)
+        mode = ("frontier", "full")[it % 2] if R * R * S * S <= 200000 else "frontier"
+        B = int(g.integers(0, 9))
+        bg = fb.Budget(B, mode=mode, per_rank_cap=int(g.integers(0, 3)))
+        host = fb.plan_swaps(counts, slots, bg)
+        _same(_device(counts, slots, bg), host)
+        if R * S <= 40:
+            ref = OP.plan_swaps(counts, slots, B, mode=mode, per_rank_cap=bg.per_rank_cap)
+            assert [tuple(x) for x in ref.swaps] == [tuple(x) for x in host.swaps]
+        if it % 4 == 0:
+            cm = fb.CostModel(g.integers(0, 2, size=R).tolist(), g.integers(0, 400, size=E).tolist(),
+                              (int(g.integers(1, 50)), int(g.integers(1, 200))),
+                              (int(g.integers(100, 2000)), int(g.integers(20, 400))),
+                              int(g.integers(0, 12000)), None)
+            th = fb.plan_swaps_timed(counts, slots, bg, cm)
+            td = _device(counts, slots, bg, cm)
+            _same(td, th)
+            assert td.costs == th.costs
+        n += 1
+    assert n >= 30
+
+
+def test_device_planner_flags_broken_replicated_placements():
+    c = torch.tensor([3, 1], dtype=torch.int32, device="cuda")
+    for slots in ([[0, 1], [0, -1]], [[0, 1], [4, -1]], [[0, 2], [1, -1]], [[0, 1], [2, 4]]):
+        s = torch.tensor(slots, dtype=torch.int32, device="cuda")
+        for mode in ("frontier", "full"):
+            plan = fb.plan_swaps_device(c, s, fb.Budget(2, mode=mode))
+            torch.cuda.synchronize()
+            assert int(plan.status.item()) == fb._lib.FB_EINVAL
+            assert int(plan.n_swaps.item()) == 0
 
 
 @pytest.mark.parametrize("name,S_extra,budget", [("mixtral", 0, 4), ("dsv3", 1, 8)])
 def test_predicted_counts_planned_on_a_replicated_placement(name, S_extra, budget):
     """The "EPLB + Ours" path: counts predicted on the GPU, folded on the GPU under a placement that
-    replicates popular experts, planned by the host planner (= oracle), and the plan's loads equal
+    replicates popular experts, planned on the device (= host = oracle), and the plan's loads equal
     the GPU fold of the new slot table."""
     wl = CONFIGS[name].with_T(4096)
     S = wl.S + S_extra
@@ -121,6 +174,7 @@ def test_predicted_counts_planned_on_a_replicated_placement(name, S_extra, budge
         ref = OP.plan_swaps(counts, slots, budget, mode=mode)
         assert [tuple(s) for s in host.swaps] == [tuple(s) for s in ref.swaps]
         assert np.array_equal(host.slots, ref.slots)
+        _same(_device(counts, slots, fb.Budget(budget, mode=mode)), host)
         after, mm_after = _fold(counts, host.slots)
         assert np.array_equal(after, host.rank_loads)
         assert mm_after <= mm
