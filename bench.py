@@ -105,7 +105,8 @@ def measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t,
                    out, stream):
     """The rest of the hot path's entry points on the same workload, each timed back to back:
     the predict -> plan step replayed from a HIP graph, the prediction-quality diagnostics (row
-    cosine of two hidden-state batches, top-k hits, rank fold) and the time-budgeted planner."""
+    cosine of two hidden-state batches, top-k hits, rank fold), the time-budgeted planner and the
+    fold and plan of a replicated placement."""
     K = max(10, args.steps // 4)
     res = {}
     # predict -> plan captured once per hidden-state buffer, replayed in rotation
@@ -149,6 +150,16 @@ def measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t,
         res[f"plan_timed_{mode}_ms"] = _time_ms(
             torch, stream, lambda i: fb.plan_swaps_timed_device(out.counts, slots_t, bg_t, cm, out=tplan), K)
         res[f"plan_timed_{mode}_swaps"] = len(tplan.to_host().swaps)
+    # a placement that replicates popular experts (32 ranks x 9 slots: the 32 most popular experts
+    # twice): the GPU fold and the device plan of the predicted counts
+    from workloads import replicated_placement, truncated_zipf_probs
+    rslots = torch.from_numpy(replicated_placement(truncated_zipf_probs(wl.zipf_s[0], wl.E), wl.R,
+                                                   wl.S + 1)).to(out.counts.device)
+    res["fold_slot_loads_ms"] = _time_ms(torch, stream, lambda i: fb.fold_slot_loads(out.counts, rslots), K)
+    rplan = fb.plan_swaps_device(out.counts, rslots, budget)
+    res["plan_replicated_ms"] = _time_ms(
+        torch, stream, lambda i: fb.plan_swaps_device(out.counts, rslots, budget, out=rplan), K)
+    res["plan_replicated_swaps"] = len(rplan.to_host().swaps)
     return res
 
 

@@ -93,11 +93,11 @@ struct Shared {
   uint8_t mslot[kMaxRS];         // slot -> its item has moved
   union {
     struct {                     // placement check
-      int32_t reps[kMaxRS], base[kMaxRS], flag[kMaxRS];
+      int32_t cnt[kMaxRS], ej[kMaxRS], reps[kMaxRS], base[kMaxRS], flag[kMaxRS];
     } chk;
     int64_t ebytes[kMaxRS];      // expert sizes (time budget), loaded after the check
   } u;
-  int32_t scan[1024];
+  int32_t wsum[16];
   int64_t L[kMaxR];
   int32_t part[kMaxR];
   uint64_t wgain[16], wtie[16], wcost[16];
@@ -112,73 +112,90 @@ struct Shared {
   int64_t acc_cost[kMaxTimedSwaps];
 };
 
-// Placement check of both kernels (all NT threads of the workgroup call it): every value is -1 or
-// e + E * j with j < R, every expert has replicas 0 .. c_e - 1 each once, no rank holds two replicas
-// of one expert, every count is >= 0.  A violation sets bit 0 of *bad (zeroed by the caller before
-// the call).  On return, after a barrier, reps[e] = c_e and *jmax = the largest c_e.
+// Exclusive prefix sum of v over the NT threads of the workgroup (every thread calls it; wsum holds
+// NT / 64 entries): shuffles within each wave, then the totals of the waves before.
 template <int NT>
-__device__ void check_placement(const PlanDeviceLaunch& a, int32_t* reps, int32_t* base,
-                                int32_t* flag, int32_t* scan, int32_t* bad, int32_t* jmax) {
+__device__ __forceinline__ int block_exclusive_scan(int v, int32_t* wsum) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if constexpr (NT > 64) {
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    for (int u = 0; u < w; ++u) x += wsum[u];
+  }
+  return x - v;
+}
+
+// Placement check of both kernels (all NT threads of the workgroup call it) on the slot values and
+// counts the caller has put in LDS (vals[R * S], cnt[E]; *bad zeroed; all published by the first
+// barrier here): every value is -1 or e + E * j with j < R, every expert has replicas 0 .. c_e - 1
+// each once, no rank holds two replicas of one expert, every count is >= 0.  A violation sets bit
+// 0 of *bad.  On return, after a barrier, reps[e] = c_e, *jmax = the largest c_e, and ej[c] =
+// (j << 12) | e for the replica in slot c (-1 for an empty or invalid slot; E <= 4096).
+template <int NT>
+__device__ void check_placement(int E, int R, int S, const int32_t* vals, const int32_t* cnt,
+                                int32_t* ej, int32_t* reps, int32_t* base, int32_t* flag,
+                                int32_t* wsum, int32_t* bad, int32_t* jmax) {
   const int tid = threadIdx.x;
-  const int E = a.E, R = a.R, S = a.S, RS = R * S;
+  const int RS = R * S;
   for (int e = tid; e < E; e += NT) reps[e] = 0;
   for (int c = tid; c < RS; c += NT) flag[c] = 0;
   if (tid == 0) *jmax = 1;
   __syncthreads();
   for (int c = tid; c < RS; c += NT) {
-    const int v = a.slot_expert[c];
-    if (v == -1) continue;
-    if (v < 0 || v / E >= R) atomicOr(bad, 1);
-    else atomicAdd(&reps[v % E], 1);
+    const int v = vals[c];
+    int x = -1;
+    if (v < -1 || v >= E * R) {
+      atomicOr(bad, 1);
+    } else if (v >= 0) {
+      const int j = v / E, e = v - j * E;       // the only division per slot
+      x = (j << 12) | e;
+      atomicAdd(&reps[e], 1);
+    }
+    ej[c] = x;
   }
   __syncthreads();
-  // exclusive prefix sum of reps: chunk sums, one thread scans the NT partials
+  // exclusive prefix sum of reps over contiguous chunks of experts
   const int chunk = (E + NT - 1) / NT;
   const int e0 = tid * chunk, e1 = e0 + chunk < E ? e0 + chunk : E;
   int acc = 0, jm = 1;
   for (int e = e0; e < e1; ++e) acc += reps[e];
-  scan[tid] = acc;
-  __syncthreads();
-  if (tid == 0) {
-    int run = 0;
-    for (int t = 0; t < NT; ++t) {
-      const int x = scan[t];
-      scan[t] = run;
-      run += x;
-    }
-  }
-  __syncthreads();
-  acc = scan[tid];
+  acc = block_exclusive_scan<NT>(acc, wsum);
   for (int e = e0; e < e1; ++e) {
     base[e] = acc;
     acc += reps[e];
-    if (reps[e] == 0 || a.counts[e] < 0) atomicOr(bad, 1);
+    if (reps[e] == 0 || cnt[e] < 0) atomicOr(bad, 1);
     jm = reps[e] > jm ? reps[e] : jm;
   }
   atomicMax(jmax, jm);
   __syncthreads();
   for (int c = tid; c < RS; c += NT) {
-    const int v = a.slot_expert[c];
-    if (v < 0 || v / E >= R) continue;           // empty, or flagged above
-    const int e = v % E, j = v / E;
+    const int x = ej[c];
+    if (x < 0) continue;                         // empty, or flagged above
+    const int e = x & 4095, j = x >> 12;
     // base[e] + j < base[e] + reps[e] <= R * S only when j < reps[e]
     if (j >= reps[e] || atomicAdd(&flag[base[e] + j], 1) != 0) {
       atomicOr(bad, 1);
       continue;
     }
     for (int c2 = (c / S) * S; c2 < c; ++c2) {
-      const int v2 = a.slot_expert[c2];
-      if (v2 >= 0 && v2 % E == e) atomicOr(bad, 1);
+      const int x2 = ej[c2];
+      if (x2 >= 0 && (x2 & 4095) == e) atomicOr(bad, 1);
     }
   }
   __syncthreads();
 }
 
-// Token share of the replica with slot value v (0 <= v, v / E < c_e).
-__device__ __forceinline__ int32_t replica_share(int v, int E, const int32_t* counts,
-                                                 const int32_t* reps) {
-  const int e = v % E, j = v / E;
+// Token share of the replica x = (j << 12) | e (as check_placement leaves it; j < c_e).
+__device__ __forceinline__ int32_t replica_share(int x, const int32_t* counts, const int32_t* reps) {
+  const int e = x & 4095, j = x >> 12;
   const int n = counts[e], k = reps[e];
+  if (k == 1) return n;
   return n / k + (j < n % k ? 1 : 0);
 }
 
@@ -241,12 +258,44 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   const int E = a.E, R = a.R, S = a.S, RS = R * S;
   const fb_budget bg = a.budget;
 
-  if (tid == 0) { sh.bad = 0; sh.ns = 0; sh.N = 0; }
+  // bits of bad: 1 an invalid table or count, 2 item ids that would not fit the tie keys, 4 a
+  // replica (a value >= E) seen by the short check
+  if (tid == 0) { sh.bad = 0; sh.ns = 0; sh.N = 0; sh.J = 1; }
+  // every input table is fetched before the first wait; item[] holds the raw slot values until the
+  // check is done, and the expert sizes of a time budget wait in registers until the check's LDS
+  // space is free
+  for (int c = tid; c < RS; c += NT) sh.item[c] = a.slot_expert[c];
+  for (int e = tid; e < E; e += NT) { sh.u.chk.cnt[e] = a.counts[e]; sh.u.chk.reps[e] = 0; }
+  constexpr int kEB = (kMaxRS + NT - 1) / NT;
+  int64_t eb[kEB];
+#pragma unroll
+  for (int u = 0; u < kEB; ++u) {
+    const int e = tid + u * NT;
+    eb[u] = a.timed && e < E ? a.expert_bytes[e] : 0;
+  }
   for (int r = tid; r < R; r += NT) sh.part[r] = 0;
   if (a.timed)
     for (int r = tid; r < R; r += NT) { sh.node[r] = a.rank_node[r]; sh.rank_left[r] = a.cost.rank_budget_ns; }
-  check_placement<NT>(a, sh.u.chk.reps, sh.u.chk.base, sh.u.chk.flag, sh.scan, &sh.bad, &sh.J);
-  // bit 0 of bad: an invalid table or count; bit 1: item ids that would not fit the tie keys
+  __syncthreads();
+  // short check of a plain placement: every expert exactly once
+  for (int c = tid; c < RS; c += NT) {
+    const int v = sh.item[c];
+    if (v < -1) atomicOr(&sh.bad, 1);
+    else if (v >= E) atomicOr(&sh.bad, 4);
+    else if (v >= 0) atomicAdd(&sh.u.chk.reps[v], 1);
+  }
+  __syncthreads();
+  const bool replicated = (sh.bad & 4) != 0;
+  __syncthreads();
+  if (replicated) {
+    if (tid == 0) sh.bad = 0;
+    check_placement<NT>(E, R, S, sh.item, sh.u.chk.cnt, sh.u.chk.ej, sh.u.chk.reps, sh.u.chk.base,
+                        sh.u.chk.flag, sh.wsum, &sh.bad, &sh.J);
+  } else {
+    for (int e = tid; e < E; e += NT)
+      if (sh.u.chk.reps[e] != 1 || sh.u.chk.cnt[e] < 0) atomicOr(&sh.bad, 1);
+    __syncthreads();
+  }
   const int J = sh.J;
   const int V = E * J;                       // slot values are below V; empty-slot ids from V
   if (!sh.bad) {
@@ -254,20 +303,26 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       if (tid == 0) sh.bad = 2;
     } else {
       for (int c = tid; c < RS; c += NT) {
-        const int v = a.slot_expert[c];
+        const int v = sh.item[c];
         sh.item[c] = v >= 0 ? v : V + c;
-        sh.sload[c] = v >= 0 ? replica_share(v, E, a.counts, sh.u.chk.reps) : 0;
+        sh.sload[c] = v < 0 ? 0
+                    : J == 1 ? sh.u.chk.cnt[v]
+                             : replica_share(sh.u.chk.ej[c], sh.u.chk.cnt, sh.u.chk.reps);
         sh.mslot[c] = 0;
       }
     }
   }
   __syncthreads();                           // the check's arrays are dead from here on
-  if (a.timed)
-    for (int e = tid; e < E; e += NT) {
-      const int64_t b = a.expert_bytes[e];
-      sh.u.ebytes[e] = b;
-      if (b < 0 || b > kCostLimit) atomicOr(&sh.bad, 1);
+  if (a.timed) {
+#pragma unroll
+    for (int u = 0; u < kEB; ++u) {
+      const int e = tid + u * NT;
+      if (e < E) {
+        sh.u.ebytes[e] = eb[u];
+        if (eb[u] < 0 || eb[u] > kCostLimit) atomicOr(&sh.bad, 1);
+      }
     }
+  }
   __syncthreads();
   if (sh.bad) {
     if (tid == 0) { *a.n_swaps = 0; *a.status = (sh.bad & 1) ? FB_EINVAL : FB_EUNSUPPORTED; }
@@ -573,8 +628,8 @@ __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* sl
 // RPL: ranks per lane (R <= 64 * RPL); rank r lives in lane r % 64, register r / 64.
 template <int RPL>
 __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) {
+  __shared__ int32_t vals[kMaxRS], cnt[kMaxRS], ej[kMaxRS];     // the input tables
   __shared__ int32_t reps[kMaxRS], base[kMaxRS], flag[kMaxRS];   // placement check
-  __shared__ int32_t scan[64];
   __shared__ uint2 slot[kMaxRS];     // x: item id | moved flag, y: the item's load (token share)
   __shared__ int32_t part[kMaxR];
   __shared__ int32_t s_bad, s_J;
@@ -582,19 +637,40 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
   const int E = a.E, R = a.R, S = a.S, RS = R * S;
   const fb_budget bg = a.budget;
 
+  // both input tables are fetched before the first wait
+  for (int e = lane; e < E; e += 64) { cnt[e] = a.counts[e]; reps[e] = 0; }
+  for (int c = lane; c < RS; c += 64) vals[c] = a.slot_expert[c];
   for (int r = lane; r < R; r += 64) part[r] = 0;
-  if (lane == 0) s_bad = 0;
-  check_placement<64>(a, reps, base, flag, scan, &s_bad, &s_J);
-  const int J = s_J;
+  __syncthreads();
+  // short check of a plain placement (every expert exactly once); a replica (a value >= E) sends the
+  // table to the full check
+  int bad = 0, replica = 0;
+  for (int c = lane; c < RS; c += 64) {
+    const int v = vals[c];
+    if (v < -1) bad = 1;
+    else if (v >= E) replica = 1;
+    else if (v >= 0) atomicAdd(&reps[v], 1);
+  }
+  __syncthreads();
+  int J = 1;
+  if (__ballot(replica)) {
+    if (lane == 0) s_bad = 0;
+    check_placement<64>(E, R, S, vals, cnt, ej, reps, base, flag, nullptr, &s_bad, &s_J);
+    J = s_J;
+    bad = s_bad;
+  } else {
+    for (int e = lane; e < E; e += 64) bad |= (reps[e] != 1) | (cnt[e] < 0);
+  }
   const int V = E * J;               // slot values are below V; empty-slot ids from V
-  if (s_bad || (int64_t)V + RS > ((int64_t)1 << kItemBits)) {
-    if (lane == 0) { *a.n_swaps = 0; *a.status = s_bad ? FB_EINVAL : FB_EUNSUPPORTED; }
+  const bool any_bad = __ballot(bad) != 0;
+  if (any_bad || (int64_t)V + RS > ((int64_t)1 << kItemBits)) {
+    if (lane == 0) { *a.n_swaps = 0; *a.status = any_bad ? FB_EINVAL : FB_EUNSUPPORTED; }
     return;
   }
   for (int c = lane; c < RS; c += 64) {
-    const int v = a.slot_expert[c];
-    slot[c] = v >= 0 ? make_uint2((uint32_t)v, (uint32_t)replica_share(v, E, a.counts, reps))
-                     : make_uint2((uint32_t)(V + c), 0u);
+    const int v = vals[c];
+    slot[c] = v < 0 ? make_uint2((uint32_t)(V + c), 0u)
+                    : make_uint2((uint32_t)v, (uint32_t)(J == 1 ? cnt[v] : replica_share(ej[c], cnt, reps)));
   }
   __syncthreads();
   int64_t Lr[RPL];                   // load of rank lane + 64 m (0 past R)
