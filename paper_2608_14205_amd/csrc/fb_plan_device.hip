@@ -191,6 +191,17 @@ __device__ void check_placement(int E, int R, int S, const int32_t* vals, const 
   __syncthreads();
 }
 
+// Expert of the replica id it (it mod E) for 0 <= it < 2^21 and 1 <= E <= 4096, with no integer
+// division: the float quotient is within 0.25 of it / E (both roundings are below 2^-24 relative),
+// so the truncated estimate is off by at most one, which one correction of the remainder settles.
+__device__ __forceinline__ int expert_of(int it, int E, float inv_e) {
+  const int q = (int)((float)it * inv_e);
+  int r = it - q * E;
+  if (r < 0) r += E;
+  else if (r >= E) r -= E;
+  return r;
+}
+
 // Token share of the replica x = (j << 12) | e (as check_placement leaves it; j < c_e).
 __device__ __forceinline__ int32_t replica_share(int x, const int32_t* counts, const int32_t* reps) {
   const int e = x & 4095, j = x >> 12;
@@ -337,11 +348,12 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   }
   __syncthreads();
   // does rank r hold a replica of the expert of item it (a replica id below V)?
+  const float inv_e = 1.0f / (float)E;
   auto holds = [&](int r, int it) -> bool {
-    const int e = it % E;
+    const int e = expert_of(it, E, inv_e);
     for (int s = 0; s < S; ++s) {
       const int x = sh.item[r * S + s];
-      if (x < V && x % E == e) return true;
+      if (x < V && expert_of(x, E, inv_e) == e) return true;
     }
     return false;
   };
@@ -416,7 +428,9 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       if (gain <= 0) return;
       const uint64_t tk = tie_key(ra, rb, i, j);
       if (a.timed) {
-        const int64_t c = swap_cost(a, sh, ra, rb, i < V ? i % E : -1, j < V ? j % E : -1);
+        const int ei = i >= V ? -1 : J == 1 ? i : expert_of(i, E, inv_e);
+        const int ej = j >= V ? -1 : J == 1 ? j : expert_of(j, E, inv_e);
+        const int64_t c = swap_cost(a, sh, ra, rb, ei, ej);
         if (!swap_fits(a, sh, ra, rb, c)) return;
         if (ratio_better((uint64_t)gain, (uint64_t)c, tk, bgain, bcost, btie)) {
           bgain = (uint64_t)gain; bcost = (uint64_t)c; btie = tk;
@@ -743,12 +757,13 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
       bool ok = !cap_hit && !((ea.x | eb.x) & kMovedBit) && !(i >= (uint32_t)V && j >= (uint32_t)V);
       if (J > 1 && ok) {
         // no replica may join another replica of its expert
-        const int ei = i < (uint32_t)V ? (int)(i % (uint32_t)E) : -1;
-        const int ej = j < (uint32_t)V ? (int)(j % (uint32_t)E) : -1;
+        const float inv_e = 1.0f / (float)E;
+        const int ei = i < (uint32_t)V ? expert_of((int)i, E, inv_e) : -1;
+        const int ej = j < (uint32_t)V ? expert_of((int)j, E, inv_e) : -1;
         for (int s2 = 0; s2 < S; ++s2) {
           const uint32_t xb = slot[amin * S + s2].x & ~kMovedBit, xa = slot[amax * S + s2].x & ~kMovedBit;
-          if (ei >= 0 && xb < (uint32_t)V && (int)(xb % (uint32_t)E) == ei) ok = false;
-          if (ej >= 0 && xa < (uint32_t)V && (int)(xa % (uint32_t)E) == ej) ok = false;
+          if (ei >= 0 && xb < (uint32_t)V && expert_of((int)xb, E, inv_e) == ei) ok = false;
+          if (ej >= 0 && xa < (uint32_t)V && expert_of((int)xa, E, inv_e) == ej) ok = false;
         }
       }
       const int64_t d = (int64_t)(int32_t)eb.y - (int64_t)(int32_t)ea.y;

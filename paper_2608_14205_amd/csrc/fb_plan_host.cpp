@@ -136,7 +136,7 @@ int plan_impl(const int32_t* counts, int32_t E, const int32_t* slot_expert, int3
   for (const int32_t v : vals)
     if (v / E >= reps[v % E]) return FB_EINVAL;
   const int64_t V = (int64_t)E * J;                  // slot values are below V
-  if (J > 1 && (int64_t)R * E > ((int64_t)1 << 28)) return FB_EUNSUPPORTED;
+  if (J > 1 && (int64_t)R * E > ((int64_t)1 << 24)) return FB_EUNSUPPORTED;   // held[] <= 16 MB
   std::vector<uint8_t> held(J > 1 ? (size_t)R * E : 0, 0);   // held[r * E + e]: e on rank r
   for (int32_t r = 0; r < R && J > 1; ++r)
     for (int32_t s = 0; s < S; ++s) {
