@@ -73,6 +73,43 @@ def test_shape_sweep(E, k, kind, groups, dtype):
     check_counts_consistent(gpu, wl, e2r)
 
 
+def _random_shape(g, i):
+    E = int(g.choice([8, 16, 24, 32, 40, 64, 96, 128, 160, 192, 256]))
+    kind = "sigmoid" if g.random() < 0.5 else "softmax"
+    # group sizes the kernel takes: powers of two (whole 16-expert lane blocks, or within a lane)
+    n_group = int(g.choice([d for d in (1, 2, 4, 8) if E % d == 0 and
+                            (d == 1 or (E // d) & (E // d - 1) == 0)]))
+    gsz = E // n_group
+    topk_group = int(g.integers(1, n_group + 1))
+    topn = int(g.integers(1, min(2, gsz) + 1))
+    k = int(g.integers(1, min(32, topk_group * gsz) + 1))
+    dtype = "f32" if g.random() < 0.25 else "bf16"
+    H = int(g.integers(1, 129)) * (16 if dtype == "f32" else 32)
+    T = int(g.integers(1, 2500))
+    R = int(g.choice([d for d in (1, 2, 4, 8) if E % d == 0]))
+    return dataclasses.replace(CONFIGS["dsv3"], name=f"rand{i}", cfg_id=100 + i, T=T, H=H, E=E, k=k,
+                               dtype=dtype, kind=kind, n_group=n_group, topk_group=topk_group,
+                               group_topn=topn, select_bias=(kind == "sigmoid"), R=R,
+                               S=max(1, E // R), n_clusters=E)
+
+
+def test_random_shapes():
+    """Seeded random shapes (E, k, scoring, groups, dtype, H, T, ranks), fused and split launches,
+    each against the oracle on every token."""
+    g = np.random.default_rng(2608)
+    pred = fb.Predictor()
+    for i in range(40):
+        wl = _random_shape(g, i)
+        packed = bool(i % 2)
+        _say(f"[random {i}] T={wl.T} H={wl.H} E={wl.E} k={wl.k} {wl.kind} groups=({wl.n_group},"
+             f"{wl.topk_group},{wl.group_topn}) {wl.dtype} R={wl.R} packed={packed}")
+        e2r = (np.arange(wl.E) * wl.R // wl.E).astype(np.int32)
+        li = make_layer(wl, 0)
+        gpu = run_gpu(li, wl, e2r, predictor=pred, packed=packed)
+        check_prediction(gpu, li, wl, e2r, label=wl.name)
+        check_counts_consistent(gpu, wl, e2r)
+
+
 @pytest.mark.parametrize("T", [0, 1, 63, 64, 65, 127, 128, 129, 255, 257])
 def test_token_edges(T):
     _say(f"[edges] T={T}")
