@@ -172,6 +172,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=400)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    # The bench line is the DeepSeek-V3-shaped batch.  The other input shapes can be timed the same
+    # way for context (same step, roofline fields without counter traffic, no extras or CPU leg).
+    ap.add_argument("--workload", default="deepseek-v3",
+                    choices=["deepseek-v3", "mixtral", "qwen3", "sweep-4096", "sweep-16384",
+                             "sweep-65536"])
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the predictor shards over tokens with one 1 KB count "
@@ -180,9 +185,13 @@ def main():
 
     import torch
     import paper_2608_14205_amd as fb
-    from workloads import CONFIGS, contiguous_placement, make_layer
+    from workloads import CONFIGS, contiguous_placement, make_layer, sweep_workload
 
-    wl = CONFIGS["dsv3"]
+    default = args.workload == "deepseek-v3"
+    if args.workload.startswith("sweep-"):
+        wl = sweep_workload(int(args.workload.split("-")[1]))
+    else:
+        wl = CONFIGS[{"deepseek-v3": "dsv3", "mixtral": "mixtral", "qwen3": "qwen3"}[args.workload]]
     slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
     li = make_layer(wl, 0)
     dev = torch.device("cuda", 0)
@@ -191,7 +200,7 @@ def main():
 
     x0 = torch.from_numpy(li.x.view(np.int16)).to(dev).view(torch.bfloat16)
     w = torch.from_numpy(li.w.view(np.int16)).to(dev).view(torch.bfloat16)
-    sb = torch.from_numpy(li.select_bias).to(dev)
+    sb = torch.from_numpy(li.select_bias).to(dev) if li.select_bias is not None else None
     e2r_t = torch.from_numpy(e2r).to(dev)
     slots_t = torch.from_numpy(slots).to(dev)
     nbuf = max(2, math.ceil(768e6 / x0.numel() / 2))
@@ -264,8 +273,8 @@ def main():
 
     counts = out.counts.cpu().numpy()
     host_plan = plan.to_host()
-    extras = measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t, slots_t, sb,
-                            pred, out, stream)
+    extras = (measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t, slots_t,
+                             sb, pred, out, stream) if default else None)
 
     # the same step with fb_predict_load, which repacks the router weight on every call
     u_start = torch.cuda.Event(enable_timing=True)
@@ -298,14 +307,20 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "deepseek-v3-shaped prefill", "T": wl.T, "H": wl.H, "E": wl.E,
-                   "k": wl.k, "scoring": "sigmoid+bias, 8 groups keep 4 (top-2 sum)",
+        "config": {"workload": f"{args.workload}-shaped prefill", "T": wl.T, "H": wl.H, "E": wl.E,
+                   "k": wl.k,
+                   "scoring": (f"{wl.kind}" + ("+bias" if wl.select_bias else "") +
+                               (f", {wl.n_group} groups keep {wl.topk_group} (top-{wl.group_topn} sum)"
+                                if wl.n_group > 1 else "")),
                    "ranks": wl.R, "slots_per_rank": wl.S, "swap_budget": wl.budget,
+                   "split_mode": fb.predict_split_workspace_bytes(wl.T, wl.E, wl.H, torch.bfloat16,
+                                                                  dev) > 2048,
                    "step": "fb_predict_load_packed + fb_plan_swaps_device, one stream",
                    "router_packing": "once, before timing (fb_pack_router_weight)"},
         "ms_per_step_repacking_router": unpacked_ms,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic_from_profile(),
+                     "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": traffic_from_profile() if default else None,
                      "bytes_per_launch": nbytes, "kernel_ms": avg_kernel_s * 1e3,
                      "mfma": {"achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                               "frac": tflops / PEAK_BF16_TFLOPS}},
@@ -318,7 +333,7 @@ def main():
                  "max_mean_before": float(out.max_mean.item()),
                  "max_mean_after": float(host_plan.rank_loads.max() * wl.R / host_plan.rank_loads.sum())},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and default:
         result["cpu_baseline"] = cpu_baseline(wl, li, e2r, slots, args.cpu_seconds)
     else:
         result["cpu_baseline"] = None
