@@ -12,8 +12,8 @@
 // term and partial product is bounded by it (0 <= M' <= N, |d| <= N, |L_b - L_a - d| <= N).
 //
 // Two kernels:
-//   * plan_frontier_wave, one wave, for frontier mode with S * S <= 64 (the common case).  Rank
-//     loads live in registers (ranks lane + 64 m), each lane owns one candidate (p, q), slot entries
+//   * plan_frontier_wave, one wave, for frontier mode with S * S <= 128 (the common case).  Rank
+//     loads live in registers (ranks lane + 64 m), each lane owns one or two candidates (p, q), slot entries
 //     carry the item, its moved flag and its count so that a candidate costs one LDS round trip,
 //     and a round is a handful of wave reductions with no workgroup barrier.
 //   * plan_general<NT> for everything else (full mode, larger S, a time budget): state in LDS,
@@ -564,14 +564,24 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 // are 32-bit, rank ties are resolved by the lowest lane of a
 // ballot, and the tie key reduction runs only when two candidates share the best benefit.
 // Returns the number of swaps written.
+// CPL: candidates per lane (1 when S * S <= 64, else 2).
+template <int CPL>
 __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* slot, int32_t* part,
                                             uint32_t& Lu, int64_t g_num, int64_t g_den) {
   const int lane = threadIdx.x;
   const int E = a.E, R = a.R, S = a.S;
   const fb_budget bg = a.budget;
   const bool valid = lane < R;
-  const int pl = lane / S, ql = lane - pl * S;
-  const bool has_cand = lane < S * S;
+  // candidates (p, q) = (c / S, c mod S) for c = lane (+ 64)
+  int pc[CPL], qc[CPL];
+  bool hc[CPL];
+#pragma unroll
+  for (int h = 0; h < CPL; ++h) {
+    const int c = lane + 64 * h;
+    hc[h] = c < S * S;
+    pc[h] = hc[h] ? c / S : 0;
+    qc[h] = hc[h] ? c - pc[h] * S : 0;
+  }
   const bool capped = bg.per_rank_cap != 0;
   constexpr uint32_t kMoved = 0x80000000u;
   int ns = 0;
@@ -585,23 +595,44 @@ __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* sl
     const uint32_t ko = wave_max_u32(valid && lane != amax && lane != amin ? Lu + 1u : 0u);
     const int64_t other = ko ? (int64_t)ko - 1 : INT64_MIN;
 
+    // this lane's better candidate: larger benefit, then smaller (i, j)
     bool ok = false;
     int64_t gain = 0;
     uint32_t tk = 0;
     uint2 ea = {0u, 0u}, eb = {0u, 0u};
-    if (has_cand) {
-      ea = slot[amax * S + pl];
-      eb = slot[amin * S + ql];
-      const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
-      const uint32_t i = ea.x & ~kMoved, j = eb.x & ~kMoved;
-      const int64_t d = (int64_t)(int32_t)eb.y - (int64_t)(int32_t)ea.y;
+    int pl = 0, ql = 0;
+    const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
+    auto eval = [&](int p, int q, uint2& xa, uint2& xb, int64_t& gh, uint32_t& th) -> bool {
+      xa = slot[amax * S + p];
+      xb = slot[amin * S + q];
+      const uint32_t i = xa.x & ~kMoved, j = xb.x & ~kMoved;
+      const int64_t d = (int64_t)(int32_t)xb.y - (int64_t)(int32_t)xa.y;
       const int64_t la = M + d, lb = Lmin - d;
       int64_t m2 = la > lb ? la : lb;
       if (other > m2) m2 = other;
       const int64_t spread = g_num ? g_num * (2 * d * (Lmin - M - d)) : 0;
-      gain = g_den * (M - m2) + spread;
-      ok = !cap_hit && !((ea.x | eb.x) & kMoved) && !(i >= (uint32_t)E && j >= (uint32_t)E) && gain > 0;
-      tk = (i << kSmallItemBits) | j;
+      gh = g_den * (M - m2) + spread;
+      th = (i << kSmallItemBits) | j;
+      return !cap_hit && !((xa.x | xb.x) & kMoved) && !(i >= (uint32_t)E && j >= (uint32_t)E) && gh > 0;
+    };
+    if constexpr (CPL == 1) {
+      if (hc[0]) {
+        ok = eval(pc[0], qc[0], ea, eb, gain, tk);
+        pl = pc[0];
+        ql = qc[0];
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < CPL; ++h) {
+        if (!hc[h]) continue;
+        uint2 xa, xb;
+        int64_t gh;
+        uint32_t th;
+        const bool okh = eval(pc[h], qc[h], xa, xb, gh, th);
+        if (okh && (!ok || gh > gain || (gh == gain && th < tk))) {
+          ok = true; gain = gh; tk = th; ea = xa; eb = xb; pl = pc[h]; ql = qc[h];
+        }
+      }
     }
     // largest benefit as two 32-bit reductions, then the smallest (i, j) among equal benefits
     const uint32_t ghi = wave_max_u32(ok ? (uint32_t)((uint64_t)gain >> 32) : 0u);
@@ -640,7 +671,8 @@ __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* sl
 }
 
 // RPL: ranks per lane (R <= 64 * RPL); rank r lives in lane r % 64, register r / 64.
-template <int RPL>
+// CPL: candidates per lane, 1 for S * S <= 64, 2 for S * S <= 128.
+template <int RPL, int CPL>
 __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) {
   __shared__ int32_t vals[kMaxRS], cnt[kMaxRS], ej[kMaxRS];     // the input tables
   __shared__ int32_t reps[kMaxRS], base[kMaxRS], flag[kMaxRS];   // placement check
@@ -707,8 +739,16 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
     return;
   }
 
-  const int pl = lane / S, ql = lane - pl * S;   // this lane's candidate slots
-  const bool has_cand = lane < S * S;
+  // this lane's candidates (p, q) = (c / S, c mod S) for c = lane (+ 64)
+  int pc[CPL], qc[CPL];
+  bool hc[CPL];
+#pragma unroll
+  for (int h = 0; h < CPL; ++h) {
+    const int c = lane + 64 * h;
+    hc[h] = c < S * S;
+    pc[h] = hc[h] ? c / S : 0;
+    qc[h] = hc[h] ? c - pc[h] * S : 0;
+  }
   const bool capped = bg.per_rank_cap != 0;
   int ns = 0;
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
@@ -716,7 +756,7 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
   if constexpr (RPL == 1) {
     if (active && N < (int64_t)0x7fffffff && J == 1) {
       uint32_t Lu = (uint32_t)Lr[0];
-      ns = rounds_small(a, slot, part, Lu, g_num, g_den);
+      ns = rounds_small<CPL>(a, slot, part, Lu, g_num, g_den);
       Lr[0] = Lu;
       small_done = true;
     }
@@ -749,43 +789,61 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
     uint64_t gk = 0, tk = 0;
     int64_t dl = 0;
     uint2 ea = {0u, 0u}, eb = {0u, 0u};
-    if (has_cand) {
-      ea = slot[amax * S + pl];
-      eb = slot[amin * S + ql];
-      const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
-      const uint32_t i = ea.x & ~kMovedBit, j = eb.x & ~kMovedBit;
-      bool ok = !cap_hit && !((ea.x | eb.x) & kMovedBit) && !(i >= (uint32_t)V && j >= (uint32_t)V);
+    const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
+    // with replicas: the experts on the two ranks (-1 for an empty slot), read once per round
+    constexpr int kMaxS = 11;                   // S * S <= 128
+    const float inv_e = 1.0f / (float)E;
+    int ex_a[kMaxS], ex_b[kMaxS];
+#pragma unroll
+    for (int s2 = 0; s2 < kMaxS; ++s2) {
+      ex_a[s2] = -1;
+      ex_b[s2] = -1;
+      if (J > 1 && s2 < S) {
+        const uint32_t ya = slot[amax * S + s2].x & ~kMovedBit, yb = slot[amin * S + s2].x & ~kMovedBit;
+        ex_a[s2] = ya < (uint32_t)V ? expert_of((int)ya, E, inv_e) : -1;
+        ex_b[s2] = yb < (uint32_t)V ? expert_of((int)yb, E, inv_e) : -1;
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) {
+      if (!hc[h]) continue;
+      const int pl = pc[h], ql = qc[h];
+      const uint2 xa = slot[amax * S + pl], xb = slot[amin * S + ql];
+      const uint32_t i = xa.x & ~kMovedBit, j = xb.x & ~kMovedBit;
+      bool ok = !cap_hit && !((xa.x | xb.x) & kMovedBit) && !(i >= (uint32_t)V && j >= (uint32_t)V);
       if (J > 1 && ok) {
         // no replica may join another replica of its expert
-        const float inv_e = 1.0f / (float)E;
         const int ei = i < (uint32_t)V ? expert_of((int)i, E, inv_e) : -1;
         const int ej = j < (uint32_t)V ? expert_of((int)j, E, inv_e) : -1;
-        for (int s2 = 0; s2 < S; ++s2) {
-          const uint32_t xb = slot[amin * S + s2].x & ~kMovedBit, xa = slot[amax * S + s2].x & ~kMovedBit;
-          if (ei >= 0 && xb < (uint32_t)V && expert_of((int)xb, E, inv_e) == ei) ok = false;
-          if (ej >= 0 && xa < (uint32_t)V && expert_of((int)xa, E, inv_e) == ej) ok = false;
+#pragma unroll
+        for (int s2 = 0; s2 < kMaxS; ++s2) {
+          if (ei >= 0 && ex_b[s2] == ei) ok = false;
+          if (ej >= 0 && ex_a[s2] == ej) ok = false;
         }
       }
-      const int64_t d = (int64_t)(int32_t)eb.y - (int64_t)(int32_t)ea.y;
+      const int64_t d = (int64_t)(int32_t)xb.y - (int64_t)(int32_t)xa.y;
       const int64_t la = M + d, lb = Lmin - d;
       int64_t m2 = la > lb ? la : lb;
       if (other > m2) m2 = other;
       const int64_t spread = g_num ? g_num * (2 * d * (Lmin - M - d)) : 0;
       const int64_t gain = g_den * (M - m2) + spread;
-      if (ok && gain > 0) {
+      // tie order inside the fixed pair (amax, amin): item ids; the slots ride along below them
+      const uint64_t th = ((((uint64_t)i << kItemBits) | j) << 8) | ((uint64_t)pl << 4) | (uint64_t)ql;
+      if (ok && gain > 0 && (gk == 0 || (uint64_t)gain > gk || ((uint64_t)gain == gk && th < tk))) {
         gk = (uint64_t)gain;
-        // tie order inside the fixed pair (amax, amin): item ids; the slots ride along below them
-        tk = ((((uint64_t)i << kItemBits) | j) << 6) | ((uint64_t)pl << 3) | (uint64_t)ql;
+        tk = th;
         dl = d;
+        ea = xa;
+        eb = xb;
       }
     }
     const uint64_t g = wave_max_u64(gk);
     if (g == 0) break;                          // no admissible candidate with positive benefit
     const uint64_t t = ~wave_max_u64(gk == g ? ~tk : 0ull);
-    const int wp = (int)(t >> 3) & 7, wq = (int)t & 7;
-    const int wi = (int)(t >> (6 + kItemBits)) & ((1 << kItemBits) - 1);
-    const int wj = (int)(t >> 6) & ((1 << kItemBits) - 1);
-    const int wl = __builtin_amdgcn_readfirstlane(wp * S + wq);
+    const int wp = (int)(t >> 4) & 15, wq = (int)t & 15;
+    const int wi = (int)(t >> (8 + kItemBits)) & ((1 << kItemBits) - 1);
+    const int wj = (int)(t >> 8) & ((1 << kItemBits) - 1);
+    const int wl = __builtin_amdgcn_readfirstlane((wp * S + wq) & 63);   // the lane that holds it
     const int64_t d = (int64_t)readlane_u64((uint64_t)dl, wl);
     const int32_t ci = __builtin_amdgcn_readlane((int)ea.y, wl), cj = __builtin_amdgcn_readlane((int)eb.y, wl);
     if (lane == 0) {
@@ -827,11 +885,18 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
 int launch_plan_device(const PlanDeviceLaunch& a) {
   (void)hipGetLastError();
   hipStream_t st = static_cast<hipStream_t>(a.stream);
-  if (!a.timed && a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 64) {
-    if (a.R <= 64) hipLaunchKernelGGL(plan_frontier_wave<1>, dim3(1), dim3(64), 0, st, a);
-    else if (a.R <= 128) hipLaunchKernelGGL(plan_frontier_wave<2>, dim3(1), dim3(64), 0, st, a);
-    else if (a.R <= 256) hipLaunchKernelGGL(plan_frontier_wave<4>, dim3(1), dim3(64), 0, st, a);
-    else hipLaunchKernelGGL(plan_frontier_wave<16>, dim3(1), dim3(64), 0, st, a);
+  if (!a.timed && a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 128) {
+    if ((int64_t)a.S * a.S <= 64) {
+      if (a.R <= 64) hipLaunchKernelGGL((plan_frontier_wave<1, 1>), dim3(1), dim3(64), 0, st, a);
+      else if (a.R <= 128) hipLaunchKernelGGL((plan_frontier_wave<2, 1>), dim3(1), dim3(64), 0, st, a);
+      else if (a.R <= 256) hipLaunchKernelGGL((plan_frontier_wave<4, 1>), dim3(1), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((plan_frontier_wave<16, 1>), dim3(1), dim3(64), 0, st, a);
+    } else {
+      if (a.R <= 64) hipLaunchKernelGGL((plan_frontier_wave<1, 2>), dim3(1), dim3(64), 0, st, a);
+      else if (a.R <= 128) hipLaunchKernelGGL((plan_frontier_wave<2, 2>), dim3(1), dim3(64), 0, st, a);
+      else if (a.R <= 256) hipLaunchKernelGGL((plan_frontier_wave<4, 2>), dim3(1), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((plan_frontier_wave<16, 2>), dim3(1), dim3(64), 0, st, a);
+    }
   }
   else if (a.budget.mode == FB_FRONTIER)
     hipLaunchKernelGGL(plan_general<256>, dim3(1), dim3(256), 0, st, a);
