@@ -219,3 +219,38 @@ def test_timed_device_planner_reports_bad_sizes():
     out = fb.plan_swaps_timed_device(c, slots, fb.Budget(2), cm)
     torch.cuda.synchronize()
     assert int(out.status.item()) == -1 and int(out.n_swaps.item()) == 0
+
+
+def test_device_planner_seeded_fuzz():
+    """device = host on 1000 seeded random instances: plain and replicated placements, R up to 299,
+    S up to 11 (both one-wave kernel instantiations and the general kernel), both modes, per-rank
+    caps, tau, gamma, layer ids and counts up to 2^20."""
+    from workloads import random_replicated_placement
+    print("[plan] seeded fuzz", flush=True)
+    g = np.random.default_rng(20261)
+    n = 0
+    for it in range(1000):
+        R = int(g.integers(2, [9, 40, 130, 300][it % 4]))
+        S = int(g.integers(1, 12))
+        if R * S > 4096:
+            continue
+        if g.random() < 0.5:
+            got = random_replicated_placement(g, R, S)
+            if got is None:
+                continue
+            slots, E = got
+        else:
+            E = int(g.integers(1, R * S + 1))
+            t = np.full(R * S, -1, np.int32)
+            t[g.permutation(R * S)[:E]] = np.arange(E)
+            slots = t.reshape(R, S)
+        hi = [5, 60, 3000, 2 ** 20][int(g.integers(0, 4))]
+        counts = (g.integers(0, hi, size=E) * (g.random(E) < 0.9)).astype(np.int32)
+        mode = "frontier" if g.random() < 0.7 or R * R * S * S > 300000 else "full"
+        gamma = [None, (0, 1), (1, 7), (3, 2)][int(g.integers(0, 4))]
+        bg = fb.Budget(int(g.integers(0, 12)), mode=mode, per_rank_cap=int(g.integers(0, 3)),
+                       tau=int(g.integers(0, 3)), gamma=gamma, layer_id=int(g.integers(0, 5)))
+        host = fb.plan_swaps(counts, slots, bg)
+        _same(_dev(counts, slots, bg), host)
+        n += 1
+    assert n > 900
