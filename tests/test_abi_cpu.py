@@ -511,3 +511,17 @@ def test_timed_device_planner_validation_without_gpu():
     bad = fb.CostModel([0, 0], [1] * 4, (5, 5), (0, 100), 1000).to_c()
     a = list(args); a[6] = ctypes.byref(bad)
     assert lib.fb_plan_swaps_timed_device(*a) == L.FB_EINVAL
+
+
+def test_split_workspace_sizes_without_gpu():
+    # invalid arguments give 0; with no device the query assumes 256 CUs: a 4096-token DS-V3-shaped
+    # batch splits its 64 half-height tiles four ways (64 x 4 x 64 x 256 float partials past the
+    # first 2048 bytes), the 32768-token batch fills the chip and runs fused (2048 bytes)
+    lib = fb.lib()
+    for args in [(-1, 256, 7168, 0), (100, 0, 7168, 0), (100, 257, 7168, 0), (100, 256, 0, 0),
+                 (100, 256, 7168, 5)]:
+        assert lib.fb_predict_split_workspace_bytes(*args) == 0
+    assert lib.fb_predict_split_workspace_bytes(4096, 256, 7168, 0) == 2048 + 64 * 4 * 64 * 256 * 4
+    assert lib.fb_predict_split_workspace_bytes(32768, 256, 7168, 0) == 2048
+    # a batch of 77 tokens with E = 16 (128-token tiles, H = 1024 fp32: 16 stages) splits 4 ways
+    assert lib.fb_predict_split_workspace_bytes(77, 16, 1024, 1) == 2048 + 1 * 4 * 128 * 32 * 4
