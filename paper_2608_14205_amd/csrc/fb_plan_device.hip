@@ -178,14 +178,29 @@ __device__ void check_placement(int E, int R, int S, const int32_t* vals, const 
     const int x = ej[c];
     if (x < 0) continue;                         // empty, or flagged above
     const int e = x & 4095, j = x >> 12;
-    // base[e] + j < base[e] + reps[e] <= R * S only when j < reps[e]
-    if (j >= reps[e] || atomicAdd(&flag[base[e] + j], 1) != 0) {
-      atomicOr(bad, 1);
-      continue;
-    }
-    for (int c2 = (c / S) * S; c2 < c; ++c2) {
-      const int x2 = ej[c2];
-      if (x2 >= 0 && (x2 & 4095) == e) atomicOr(bad, 1);
+    // base[e] + j < base[e] + reps[e] <= R * S only when j < reps[e]; the entry records the
+    // replica's rank + 1, and a second replica with the same ordinal finds it taken
+    if (j >= reps[e] || atomicCAS(&flag[base[e] + j], 0, c / S + 1) != 0) atomicOr(bad, 1);
+  }
+  __syncthreads();
+  // no rank holds two replicas of one expert.  Every slot of a pair takes the same branch (it
+  // depends on the expert only): with few replicas the later ordinal finds the earlier one's rank
+  // among the entries recorded above, otherwise the later slot finds the earlier one on its rank;
+  // either way a slot reads at most min(c_e, S) words
+  for (int c = tid; c < RS; c += NT) {
+    const int x = ej[c];
+    if (x < 0) continue;
+    const int e = x & 4095, j = x >> 12, k = reps[e];
+    if (j >= k) continue;                        // flagged above
+    if (k <= S) {
+      const int b = base[e], me = c / S + 1;
+      for (int w = 0; w < j; ++w)
+        if (flag[b + w] == me) atomicOr(bad, 1);
+    } else {
+      for (int c2 = (c / S) * S; c2 < c; ++c2) {
+        const int x2 = ej[c2];
+        if (x2 >= 0 && (x2 & 4095) == e) atomicOr(bad, 1);
+      }
     }
   }
   __syncthreads();

@@ -84,6 +84,7 @@ def test_slot_fold_plain_placement_equals_rank_fold():
     ([[0, -1], [-1, -1]], [3, 1]),   # expert 1 missing
     ([[0, -2], [1, -1]], [3, 1]),    # invalid value
     ([[0, 1], [2, -1]], [3, -1]),    # negative count
+    ([[0, 1], [2, -1]], [7]),        # one expert, three replicas, two on rank 0
 ])
 def test_slot_fold_flags_broken_placements(slots, counts):
     _, mm = _fold(counts, slots)
@@ -142,15 +143,36 @@ def test_device_planner_replicated_placements(R_max, S_max):
     assert n >= 30
 
 
-def test_device_planner_flags_broken_replicated_placements():
-    c = torch.tensor([3, 1], dtype=torch.int32, device="cuda")
-    for slots in ([[0, 1], [0, -1]], [[0, 1], [4, -1]], [[0, 2], [1, -1]], [[0, 1], [2, 4]]):
-        s = torch.tensor(slots, dtype=torch.int32, device="cuda")
-        for mode in ("frontier", "full"):
-            plan = fb.plan_swaps_device(c, s, fb.Budget(2, mode=mode))
-            torch.cuda.synchronize()
-            assert int(plan.status.item()) == fb._lib.FB_EINVAL
-            assert int(plan.n_swaps.item()) == 0
+@pytest.mark.parametrize("counts,slots", [
+    ([3, 1], [[0, 1], [0, -1]]), ([3, 1], [[0, 1], [4, -1]]), ([3, 1], [[0, 2], [1, -1]]),
+    ([3, 1], [[0, 1], [2, 4]]),
+    # one expert with more replicas than a rank has slots, two of them on rank 0
+    ([7], [[0, 1], [2, -1]]), ([7], [[0, -1], [1, -1], [3, 2]]),
+])
+def test_device_planner_flags_broken_replicated_placements(counts, slots):
+    c = torch.tensor(counts, dtype=torch.int32, device="cuda")
+    s = torch.tensor(slots, dtype=torch.int32, device="cuda")
+    for mode in ("frontier", "full"):
+        plan = fb.plan_swaps_device(c, s, fb.Budget(2, mode=mode))
+        torch.cuda.synchronize()
+        assert int(plan.status.item()) == fb._lib.FB_EINVAL
+        assert int(plan.n_swaps.item()) == 0
+
+
+@pytest.mark.parametrize("R,S", [(64, 1), (40, 3), (200, 2)])
+def test_device_planner_experts_replicated_on_many_ranks(R, S):
+    # a few experts, each with far more replicas than a rank has slots (the check's per-rank branch)
+    g = np.random.default_rng(R + S)
+    E = S
+    slots = np.array([[e + E * r for e in range(S)] for r in range(R)], np.int32)
+    for r in range(R):
+        slots[r] = slots[r][g.permutation(S)]
+    slots[R - 1][slots[R - 1] == E * (R - 1)] = -1     # expert 0 keeps R - 1 replicas
+    assert RP.replica_counts(slots, E) == [R - 1] + [R] * (E - 1)
+    counts = g.integers(100, 5000, size=E).astype(np.int32)
+    for mode in ("frontier", "full"):
+        bg = fb.Budget(4, mode=mode)
+        _same(_device(counts, slots, bg), fb.plan_swaps(counts, slots, bg))
 
 
 @pytest.mark.parametrize("name,S_extra,budget", [("mixtral", 0, 4), ("dsv3", 1, 8)])
