@@ -805,18 +805,30 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
     int64_t dl = 0;
     uint2 ea = {0u, 0u}, eb = {0u, 0u};
     const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
-    // with replicas: the experts on the two ranks (-1 for an empty slot), read once per round
-    constexpr int kMaxS = 11;                   // S * S <= 128
-    const float inv_e = 1.0f / (float)E;
-    int ex_a[kMaxS], ex_b[kMaxS];
+    // with replicas: eq(p, q) says that slot p of amax and slot q of amin hold replicas of one
+    // expert.  Candidate (p, q) may not put a replica beside another replica of its expert, nor
+    // exchange two replicas of one expert (eq(p, q) itself): row p and column q of eq must be
+    // empty.  The wave ballots eq once per round (S <= 11, so a row or column set fits in 32 bits);
+    // its set bits are rare and are walked with uniform values
+    uint32_t eq_rows = 0, eq_cols = 0;
+    if (J > 1) {
+      const float inv_e = 1.0f / (float)E;
 #pragma unroll
-    for (int s2 = 0; s2 < kMaxS; ++s2) {
-      ex_a[s2] = -1;
-      ex_b[s2] = -1;
-      if (J > 1 && s2 < S) {
-        const uint32_t ya = slot[amax * S + s2].x & ~kMovedBit, yb = slot[amin * S + s2].x & ~kMovedBit;
-        ex_a[s2] = ya < (uint32_t)V ? expert_of((int)ya, E, inv_e) : -1;
-        ex_b[s2] = yb < (uint32_t)V ? expert_of((int)yb, E, inv_e) : -1;
+      for (int h = 0; h < CPL; ++h) {
+        bool eqh = false;
+        if (hc[h]) {
+          const uint32_t ya = slot[amax * S + pc[h]].x & ~kMovedBit;
+          const uint32_t yb = slot[amin * S + qc[h]].x & ~kMovedBit;
+          eqh = ya < (uint32_t)V && yb < (uint32_t)V &&
+                expert_of((int)ya, E, inv_e) == expert_of((int)yb, E, inv_e);
+        }
+        uint64_t m = __ballot(eqh);
+        while (m) {
+          const int c = __builtin_ctzll(m) + 64 * h;
+          m &= m - 1;
+          eq_rows |= 1u << (c / S);
+          eq_cols |= 1u << (c % S);
+        }
       }
     }
 #pragma unroll
@@ -825,17 +837,8 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
       const int pl = pc[h], ql = qc[h];
       const uint2 xa = slot[amax * S + pl], xb = slot[amin * S + ql];
       const uint32_t i = xa.x & ~kMovedBit, j = xb.x & ~kMovedBit;
-      bool ok = !cap_hit && !((xa.x | xb.x) & kMovedBit) && !(i >= (uint32_t)V && j >= (uint32_t)V);
-      if (J > 1 && ok) {
-        // no replica may join another replica of its expert
-        const int ei = i < (uint32_t)V ? expert_of((int)i, E, inv_e) : -1;
-        const int ej = j < (uint32_t)V ? expert_of((int)j, E, inv_e) : -1;
-#pragma unroll
-        for (int s2 = 0; s2 < kMaxS; ++s2) {
-          if (ei >= 0 && ex_b[s2] == ei) ok = false;
-          if (ej >= 0 && ex_a[s2] == ej) ok = false;
-        }
-      }
+      bool ok = !cap_hit && !((xa.x | xb.x) & kMovedBit) && !(i >= (uint32_t)V && j >= (uint32_t)V) &&
+                !(((eq_rows >> pl) | (eq_cols >> ql)) & 1u);
       const int64_t d = (int64_t)(int32_t)xb.y - (int64_t)(int32_t)xa.y;
       const int64_t la = M + d, lb = Lmin - d;
       int64_t m2 = la > lb ? la : lb;
