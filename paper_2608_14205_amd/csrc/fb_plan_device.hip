@@ -95,7 +95,12 @@ struct Shared {
     struct {                     // placement check
       int32_t cnt[kMaxRS], ej[kMaxRS], reps[kMaxRS], base[kMaxRS], flag[kMaxRS];
     } chk;
-    int64_t ebytes[kMaxRS];      // expert sizes (time budget), loaded after the check
+    struct {                     // after the check
+      int64_t ebytes[kMaxRS];    // expert sizes (time budget)
+      // frontier rounds with replicas: slot p of amax (row) or q of amin (column) holds a replica
+      // of an expert that the other rank also holds
+      uint8_t mrow[kMaxRS], mcol[kMaxRS];
+    } run;
   } u;
   int32_t wsum[16];
   int64_t L[kMaxR];
@@ -241,7 +246,7 @@ __device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t beta, double in
 __device__ __forceinline__ int64_t swap_cost(const PlanDeviceLaunch& a, const Shared& sh, int ra,
                                              int rb, int ei, int ej) {
   const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
-  const int64_t bytes = (ei >= 0 ? sh.u.ebytes[ei] : 0) + (ej >= 0 ? sh.u.ebytes[ej] : 0);
+  const int64_t bytes = (ei >= 0 ? sh.u.run.ebytes[ei] : 0) + (ej >= 0 ? sh.u.run.ebytes[ej] : 0);
   const int64_t beta = a.cost.beta_bytes_per_us[t];
   return a.cost.alpha_ns[t] + ceil_div(bytes * 1000, beta, 1.0 / (double)beta);
 }
@@ -344,7 +349,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
     for (int u = 0; u < kEB; ++u) {
       const int e = tid + u * NT;
       if (e < E) {
-        sh.u.ebytes[e] = eb[u];
+        sh.u.run.ebytes[e] = eb[u];
         if (eb[u] < 0 || eb[u] > kCostLimit) atomicOr(&sh.bad, 1);
       }
     }
@@ -383,7 +388,10 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
 
   const bool frontier = bg.mode == FB_FRONTIER;
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
+  const bool marks = frontier && J > 1;
   for (int round = 0; active && round < bg.max_swaps; ++round) {
+    if (marks)                        // the previous round's reads ended at its last barrier
+      for (int s2 = tid; s2 < S; s2 += NT) { sh.u.run.mrow[s2] = 0; sh.u.run.mcol[s2] = 0; }
     // ---- wave 0: argmax, argmin and the loads of the ranks outside a candidate pair ------------
     if (wave == 0) {
       uint64_t kmax = 0, kmin = 0;
@@ -425,6 +433,20 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
 
     // ---- candidates ----------------------------------------------------------------------------
     const int amax = sh.amax, amin = sh.amin;
+    if (marks) {
+      // candidate (p, q) would put a replica beside another replica of its expert, or exchange two
+      // replicas of one expert, exactly when row p or column q of the pair's same-expert matrix
+      // has an entry: one pass over the matrix replaces a scan of the other rank per candidate
+      for (int idx = tid; idx < S * S; idx += NT) {
+        const int p = idx / S, q = idx - p * S;
+        const int i = sh.item[amax * S + p], j = sh.item[amin * S + q];
+        if (i < V && j < V && expert_of(i, E, inv_e) == expert_of(j, E, inv_e)) {
+          sh.u.run.mrow[p] = 1;
+          sh.u.run.mcol[q] = 1;
+        }
+      }
+      __syncthreads();
+    }
     const int64_t M = sh.L[amax];
     uint64_t bgain = 0, btie = 0;     // gain 0: nothing found (every accepted gain is > 0)
     uint64_t bcost = 1;
@@ -432,7 +454,13 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       const int sa = ra * S + p, sb = rb * S + q;
       const int i = sh.item[sa], j = sh.item[sb];
       if (sh.mslot[sa] || sh.mslot[sb] || (i >= V && j >= V)) return;
-      if (J > 1 && ((i < V && holds(rb, i)) || (j < V && holds(ra, j)))) return;
+      if (J > 1) {
+        if (marks) {                  // frontier: (ra, rb) = (amax, amin)
+          if (sh.u.run.mrow[p] | sh.u.run.mcol[q]) return;
+        } else if ((i < V && holds(rb, i)) || (j < V && holds(ra, j))) {
+          return;
+        }
+      }
       const int64_t La = sh.L[ra], Lb = sh.L[rb];
       const int64_t d = (int64_t)sh.sload[sb] - (int64_t)sh.sload[sa];
       const int64_t la = La + d, lb = Lb - d;
