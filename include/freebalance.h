@@ -6,7 +6,7 @@
  * hidden state h_{l-1} that leaves layer l-1 (Sec. "Residual Workload Prediction", Eq. 2 and the
  * linear router of Eq. 4), applies the routed model's own top-k rule, counts how many tokens chose
  * each expert (the predicted workload, Eq. 5) and folds the counts into per-rank loads under the
- * expert-to-rank placement (Alg. 1, "aggregate expert workloads into rank loads"), reporting the
+ * expert-to-rank placement (Alg. 1, the step that sums expert counts per rank), reporting the
  * max-to-mean rank-load ratio of Sec. "Metrics".  The planner turns counts and a slot table into a
  * budget-feasible list of pairwise expert swaps (Sec. "Budgeted Expert-Swap Planning", Eq. 6-8 and
  * Alg. 1); fb_swap_budget_from_cost converts the cost model of Eq. 9-10 into a swap count.
@@ -71,7 +71,11 @@ extern "C" {
  *               Requires E % n_group == 0 and either (E / n_group) % 16 == 0 with (E / n_group) / 16
  *               a power of two, or 16 % (E / n_group) == 0 (FB_EUNSUPPORTED otherwise).
  *   topk_group  1 <= topk_group <= n_group, and k <= topk_group * E / n_group.
- *   group_topn  1 (group max) or 2 (sum of the two best scores); ignored when n_group == 1. */
+ *   group_topn  1 (group max) or 2 (sum of the two best scores); ignored when n_group == 1.
+ *               Softmax routing takes group_topn 1 only (FB_EUNSUPPORTED for 2): softmax keeps the
+ *               order of single scores, so the group maximum of the logits names the same groups
+ *               as that of the probabilities, but it does not keep the order of sums (logits
+ *               (10, -100) outrank (5, 5) on probabilities and not on logits). */
 typedef struct fb_scoring {
   int32_t kind;
   int32_t k;

@@ -101,6 +101,8 @@ def brute_select(z_row: Sequence[float], k: int, kind: str = "softmax",
                  bias: Optional[Sequence[float]] = None, n_group: int = 1, topk_group: int = 1,
                  group_topn: int = 1) -> List[int]:
     """Top-k (with optional group limit) of one token by explicit sorting."""
+    if kind == "softmax" and n_group > 1 and group_topn > 1:
+        raise ValueError("softmax routing takes group_topn 1 only")
     s = brute_scores(z_row, kind, bias)
     E = len(s)
     allowed = list(range(E))

@@ -12,15 +12,17 @@ Follows Sec. "Budgeted Expert-Swap Planning" and Alg. 1:
 * a candidate is accepted only if neither expert has been selected already and the budgets allow it;
   loads and residual budgets are updated after every accepted swap;
 * in the default frontier mode only experts on the most loaded and the least loaded rank are
-  considered; Alg. 1 repeats "select a beneficial swap between overloaded and underloaded ranks"
-  while the imbalance exceeds tau and budget remains, and stops when no such swap exists.
+  considered; Alg. 1 keeps choosing a positive-benefit swap between a heavier and a lighter rank
+  while its loop condition (imbalance above tau) holds and budget remains, and stops when no such
+  swap exists.
 
 Readings of points the paper leaves open:
 
 * Iterative reading of Alg. 1: every round re-enumerates and re-scores the candidates at the current
   loads and accepts the best one.  Sorting once up front would let stale scores accept swaps whose
   benefit has become negative.
-* "Rank-pair imbalance exceeds tau" is L_max - L_min > tau (integer tokens, default tau = 0).
+* The loop condition of Alg. 1 (an imbalance above tau) is read as L_max - L_min > tau (integer
+  tokens, default tau = 0).
 * gamma is a rational gamma_num / gamma_den (passed as the pair); the default is gamma = 1 / N with
   N = sum of counts.
 * The source rank is the more loaded one (its load drops), the destination the less loaded one.

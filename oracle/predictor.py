@@ -8,7 +8,7 @@ Follows Sec. "Residual Workload Prediction":
 * the model's own top-k rule applied to G^_l gives the estimated assignments T^_l(i) (Sec.
   "Mixture-of-Expert Architecture": W_l, I_l = topk(G(h_l)));
 * Eq. 5  predicted workload  n^_{l,e} = sum_i 1[e in T^_l(i)];
-* Alg. 1 "aggregate expert workloads into rank loads under pi_l":  L_r = sum_{e: pi(e) = r} n^_e;
+* Alg. 1, the aggregation step under the placement pi_l:  L_r = sum_{e: pi(e) = r} n^_e;
 * Sec. "Metrics": max-to-mean rank-load ratio, 1 = perfect balance.
 
 Precision: hidden states and router weights are widened exactly to float64, the contraction is a
@@ -27,7 +27,8 @@ Routing rules ("the original top-k rule" of the routed model):
 * group-limited selection (``n_group`` > 1): experts are split into ``n_group`` contiguous groups, a
   group's score is the float32 sum of its ``group_topn`` largest scores (largest first), the
   ``topk_group`` best groups are kept (score descending, lower group index first on ties) and the k
-  experts are chosen among the kept groups only.
+  experts are chosen among the kept groups only.  With softmax scoring only the group maximum
+  (``group_topn`` = 1) is taken, the one group score that ranks logits and probabilities alike.
 
 Ties between equal float32 scores go to the lower expert index, everywhere.
 """
@@ -130,7 +131,13 @@ def topk_experts(s: np.ndarray, k: int, allowed: Optional[np.ndarray] = None) ->
 
 def select(z: np.ndarray, k: int, kind: str, select_bias=None, n_group: int = 1,
            topk_group: int = 1, group_topn: int = 1):
-    """The routed model's top-k rule on float32 logits.  Returns (topk T x k, scores, allowed)."""
+    """The routed model's top-k rule on float32 logits.  Returns (topk T x k, scores, allowed).
+
+    Softmax routing with groups scored by the sum of their two best scores is rejected: the
+    probabilities' sums do not rank groups like the logits' sums, and a selection computed on logits
+    would not be the routed model's.  The group maximum ranks them alike (softmax is monotone)."""
+    if kind == SOFTMAX and n_group > 1 and group_topn > 1:
+        raise ValueError("softmax routing takes group_topn 1 only")
     s = router_scores(z, kind, select_bias)
     allowed = group_keep_mask(s, n_group, topk_group, group_topn)
     return topk_experts(s, k, allowed if n_group > 1 else None), s, allowed

@@ -66,6 +66,8 @@ int check_scoring(const fb_scoring& s, int32_t E, const float* select_bias) {
   if (s.n_group > 1) {
     if (s.topk_group < 1 || s.topk_group > s.n_group) return FB_EINVAL;
     if (s.group_topn != 1 && s.group_topn != 2) return FB_EINVAL;
+    // a sum of logits does not order groups like the sum of their softmax probabilities
+    if (s.kind == FB_SOFTMAX && s.group_topn == 2) return FB_EUNSUPPORTED;
     const int gsz = E / s.n_group;
     if ((int64_t)s.k > (int64_t)s.topk_group * gsz) return FB_EINVAL;
     if (s.group_topn > gsz) return FB_EINVAL;
@@ -132,14 +134,13 @@ int fb_pack_router_weight(const void* router_w, int32_t E, int32_t H, int32_t dt
 
 namespace {
 
-// Checks shared by both predictor entry points; FB_OK when a launch may proceed.
-int check_predict(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
-                  int32_t E, const float* select_bias, const fb_scoring* scoring,
-                  const int32_t* expert_to_rank, int32_t R, const int32_t* counts,
-                  const int32_t* rank_loads, const double* max_mean, const void* workspace,
-                  size_t workspace_bytes, size_t workspace_need) {
-  if (!scoring || !expert_to_rank || !counts || !rank_loads || !max_mean || !workspace)
-    return FB_EINVAL;
+// Checks shared by the predictor entry points, except those of the workspace; FB_OK when a launch
+// may proceed.
+int check_predict_args(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
+                       int32_t E, const float* select_bias, const fb_scoring* scoring,
+                       const int32_t* expert_to_rank, int32_t R, const int32_t* counts,
+                       const int32_t* rank_loads, const double* max_mean) {
+  if (!scoring || !expert_to_rank || !counts || !rank_loads || !max_mean) return FB_EINVAL;
   if (T < 0 || H < 1 || E < 1 || R < 1 || ld_hidden < H) return FB_EINVAL;
   if (T > 0 && !hidden) return FB_EINVAL;
   if (dtype != FB_BF16 && dtype != FB_F32) return FB_EINVAL;
@@ -151,9 +152,21 @@ int check_predict(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, i
   if (ld_hidden * elem * 128 >= ((int64_t)1 << 31) ||
       fb::router_packed_bytes(E, H, dtype) >= ((size_t)1 << 31))
     return FB_EUNSUPPORTED;
-  if (!aligned16(workspace)) return FB_EINVAL;
-  if (workspace_bytes < workspace_need) return FB_ENOSPC;
   return check_scoring(*scoring, E, select_bias);
+}
+
+// check_predict_args plus the caller's workspace.
+int check_predict(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden, int32_t dtype,
+                  int32_t E, const float* select_bias, const fb_scoring* scoring,
+                  const int32_t* expert_to_rank, int32_t R, const int32_t* counts,
+                  const int32_t* rank_loads, const double* max_mean, const void* workspace,
+                  size_t workspace_bytes, size_t workspace_need) {
+  const int ac = check_predict_args(hidden, T, H, ld_hidden, dtype, E, select_bias, scoring,
+                                    expert_to_rank, R, counts, rank_loads, max_mean);
+  if (ac != FB_OK) return ac;
+  if (!workspace || !aligned16(workspace)) return FB_EINVAL;
+  if (workspace_bytes < workspace_need) return FB_ENOSPC;
+  return FB_OK;
 }
 
 fb::PredictLaunch make_launch(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,

@@ -322,6 +322,7 @@ def _predict_call(**over):
     (dict(sc=fb.Scoring("sigmoid", 2, 4, 2, 3).to_c()), L.FB_EINVAL),    # group_topn not 1 or 2
     (dict(E=48, sc=fb.Scoring("sigmoid", 2, 2, 1, 2).to_c()), L.FB_EUNSUPPORTED),  # group of 24
     (dict(E=64, sc=fb.Scoring("softmax", 33).to_c()), L.FB_EUNSUPPORTED),         # k > 32
+    (dict(sc=fb.Scoring("softmax", 2, 4, 2, 2).to_c()), L.FB_EUNSUPPORTED),       # softmax, top-2 sums
 ])
 def test_predict_validation_without_gpu(over, code):
     assert _predict_call(**over) == code

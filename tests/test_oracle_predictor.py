@@ -75,6 +75,13 @@ def test_selection_matches_brute_force(kind, groups, ties):
     n_group, topk_group, topn = groups
     E, T, k = 16 if n_group <= 4 else 32, 40, 3
     z = _random_case(7 + n_group, T, E, ties)
+    if kind == "softmax" and n_group > 1 and topn > 1:
+        # sums of logits do not rank groups like sums of probabilities: refused on both sides
+        with pytest.raises(ValueError):
+            P.select(z, k, kind, None, n_group, topk_group, topn)
+        with pytest.raises(ValueError):
+            exact.brute_select(z[0].tolist(), k, kind, None, n_group, topk_group, topn)
+        return
     g = np.random.default_rng(5)
     bias = (g.standard_normal(E) * 0.01).astype(np.float32) if kind == "sigmoid" else None
     if ties and bias is not None:
@@ -96,6 +103,31 @@ def test_softmax_selection_equals_probability_selection():
     by_prob = np.lexsort((eid, -p), axis=-1)[:, :8]
     topk, _, _ = P.select(z, 8, "softmax")
     assert np.array_equal(np.sort(by_prob, 1), np.sort(topk, 1))
+
+
+def test_softmax_group_max_ranks_groups_like_probabilities():
+    """Softmax with groups scored by their maximum: groups kept and experts chosen on logits equal
+    those chosen on explicit float64 probabilities (brute force per token)."""
+    g = np.random.default_rng(11)
+    z = (g.standard_normal((300, 32)) * 3).astype(np.float32)
+    topk, _, _ = P.select(z, 4, "softmax", None, 8, 3, 1)
+    z64 = z.astype(np.float64)
+    p = np.exp(z64 - z64.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    for t in range(z.shape[0]):
+        gmax = [max(p[t, 4 * q:4 * q + 4]) for q in range(8)]
+        kept = sorted(range(8), key=lambda q: (-gmax[q], q))[:3]
+        ref = sorted((e for e in range(32) if e // 4 in kept), key=lambda e: (-p[t, e], e))[:4]
+        assert topk[t].tolist() == ref
+
+
+def test_softmax_group_sum_is_not_a_logit_rule():
+    """Why softmax routing refuses group sums: logits (10, -100) outrank (5, 5) on the sum of
+    probabilities and not on the sum of logits."""
+    z = np.array([10.0, -100.0, 5.0, 5.0])
+    p = np.exp(z - z.max())
+    p /= p.sum()
+    assert p[0] + p[1] > p[2] + p[3] and z[0] + z[1] < z[2] + z[3]
 
 
 def test_group_limit_degenerates_to_plain_topk():
