@@ -233,6 +233,28 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
                            void* workspace, size_t workspace_bytes, int32_t* topk_idx,
                            float* logits, void* stream);
 
+/* fb_predict_load_packed for callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): no workspace argument, no allocation.  The
+ * library keeps a fixed scratch array in device memory instead, FB_NOALLOC_SCRATCH_BYTES per device
+ * (2048 bytes of accumulators and completion ticket, then 32 MiB for split-mode partial logits),
+ * held by every device the call runs on until the process ends.  The first call on a device looks
+ * up that device's copy and zeroes its header with a fill kernel on `stream`; every completed call
+ * leaves the header zeroed again.  All calls on one device share the array: calls that overlap
+ * on one device (other streams, other threads) race and give undefined results, so order them on
+ * one stream.  Batches too small to occupy the GPU run in split mode as with a large enough
+ * workspace; FB_ENOSPC if a batch's split-mode partials would exceed the 32 MiB (no batch on a
+ * 256-CU MI355X does).  Results are identical to fb_predict_load_packed's with a workspace of
+ * fb_predict_split_workspace_bytes(T, E, H, dtype) bytes.  Every other argument and error as in
+ * fb_predict_load_packed; FB_EDEVICE if the scratch cannot be located. */
+#define FB_NOALLOC_SCRATCH_BYTES (2048u + (32u << 20))
+int fb_predict_load_packed_noalloc(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                                   int32_t dtype, const void* router_packed,
+                                   size_t router_packed_bytes, int32_t E, const float* logit_bias,
+                                   const float* select_bias, const fb_scoring* scoring,
+                                   const int32_t* expert_to_rank, int32_t R, int32_t* counts,
+                                   int32_t* rank_loads, double* max_mean, int32_t* topk_idx,
+                                   float* logits, void* stream);
+
 /* Workspace bytes that let fb_predict_load_packed run a batch of T tokens in split mode on the
  * current device (2048 when the batch runs fused anyway; 0 for invalid arguments). */
 size_t fb_predict_split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype);

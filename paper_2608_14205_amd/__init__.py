@@ -25,6 +25,7 @@ from .api import (  # noqa: F401
     plan_swaps_timed,
     plan_swaps_timed_device,
     predict_load,
+    predict_load_packed_noalloc,
     predict_split_workspace_bytes,
     swap_budget_from_cost,
 )

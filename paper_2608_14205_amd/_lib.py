@@ -64,6 +64,9 @@ SIGNATURES = {
     "fb_predict_load_packed": (ctypes.c_int, [_VP, _I64, _I32, _I64, _I32, _VP, _SZ, _I32, _VP,
                                               _VP, ctypes.POINTER(fb_scoring), _VP, _I32, _VP,
                                               _VP, _VP, _VP, _SZ, _VP, _VP, _VP]),
+    "fb_predict_load_packed_noalloc": (ctypes.c_int, [_VP, _I64, _I32, _I64, _I32, _VP, _SZ, _I32,
+                                                      _VP, _VP, ctypes.POINTER(fb_scoring), _VP,
+                                                      _I32, _VP, _VP, _VP, _VP, _VP, _VP]),
     "fb_predict_split_workspace_bytes": (_SZ, [_I64, _I32, _I32, _I32]),
     "fb_plan_swaps": (ctypes.c_int, [_VP, _I32, _VP, _I32, _I32, ctypes.POINTER(fb_budget), _VP,
                                      _I32, _VP, _VP, _VP, _VP]),

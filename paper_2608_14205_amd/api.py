@@ -281,6 +281,48 @@ class Predictor:
         return out
 
 
+def predict_load_packed_noalloc(hidden: torch.Tensor, router: PackedRouter, scoring: Scoring,
+                                expert_to_rank: torch.Tensor, R: int, out: Prediction, *,
+                                logit_bias=None, select_bias=None,
+                                stream: Optional[torch.cuda.Stream] = None) -> Prediction:
+    """fb_predict_load_packed_noalloc: the packed prediction with the library's fixed device
+    scratch instead of a workspace.  Allocates nothing: every output lives in `out` (counts,
+    rank_loads, max_mean, and topk / logits when they are not None).  Calls on one device share the
+    scratch, so they must be ordered on one stream."""
+    if hidden.dim() != 2 or (hidden.numel() > 0 and hidden.stride(1) != 1):
+        raise ValueError("hidden must be T x H with contiguous rows")
+    T, H = hidden.shape
+    if router.H != H or router.dtype != hidden.dtype:
+        raise ValueError("packed router was built for another H or dtype")
+    dev = hidden.device
+    for t in (router.data, expert_to_rank, logit_bias, select_bias, out.counts, out.rank_loads,
+              out.max_mean, out.topk, out.logits):
+        if t is not None and t.device != dev:
+            raise ValueError("all tensors must live on the hidden states' device")
+    E = router.E
+    if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
+        raise ValueError("expert_to_rank must be int32[E]")
+    if (out.counts.dtype != torch.int32 or out.counts.numel() < E or out.rank_loads.dtype != torch.int32
+            or out.rank_loads.numel() < R or out.max_mean.dtype != torch.float64):
+        raise ValueError("out must hold int32[E] counts, int32[R] rank_loads and a float64 max_mean")
+    if out.topk is not None and (out.topk.dtype != torch.int32 or out.topk.numel() < T * scoring.k):
+        raise ValueError("out.topk must be int32[T * k]")
+    if out.logits is not None and (out.logits.dtype != torch.float32 or out.logits.numel() < T * E):
+        raise ValueError("out.logits must be float32[T * E]")
+    for b in (logit_bias, select_bias):
+        if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
+            raise ValueError("biases must be contiguous float32[E]")
+    sc = scoring.to_c()
+    with torch.cuda.device(dev):
+        st = L.lib().fb_predict_load_packed_noalloc(
+            _ptr(hidden), T, H, hidden.stride(0) if T > 0 else H, _dtype_code(hidden),
+            _ptr(router.data), router.data.numel(), E, _ptr(logit_bias), _ptr(select_bias),
+            ctypes.byref(sc), _ptr(expert_to_rank), R, _ptr(out.counts), _ptr(out.rank_loads),
+            _ptr(out.max_mean), _ptr(out.topk), _ptr(out.logits), _stream_handle(dev, stream))
+    L.check(st, "fb_predict_load_packed_noalloc")
+    return out
+
+
 _default_predictors = {}
 
 

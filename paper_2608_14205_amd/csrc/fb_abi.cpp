@@ -257,6 +257,38 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
   return fb::launch_predict(a);
 }
 
+int fb_predict_load_packed_noalloc(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                                   int32_t dtype, const void* router_packed,
+                                   size_t router_packed_bytes, int32_t E, const float* logit_bias,
+                                   const float* select_bias, const fb_scoring* scoring,
+                                   const int32_t* expert_to_rank, int32_t R, int32_t* counts,
+                                   int32_t* rank_loads, double* max_mean, int32_t* topk_idx,
+                                   float* logits, void* stream) {
+  if (!router_packed) return FB_EINVAL;
+  const int vc = check_predict_args(hidden, T, H, ld_hidden, dtype, E, select_bias, scoring,
+                                    expert_to_rank, R, counts, rank_loads, max_mean);
+  if (vc != FB_OK) return vc;
+  if (!aligned16(router_packed)) return FB_EUNSUPPORTED;
+  if (router_packed_bytes < fb::router_packed_bytes(E, H, dtype)) return FB_ENOSPC;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  // the split mode's partial logits must fit the scratch; every batch that runs split on a
+  // 256-CU device does (the bound is in fb_internal.h)
+  const size_t sb = fb::split_workspace_bytes(T, E, H, dtype, fb::device_cu_count());
+  if (sb > fb::kNoAllocPartialBytes) return FB_ENOSPC;
+  void* scratch = nullptr;
+  const int sc = fb::noalloc_scratch(&scratch, stream);
+  if (sc != FB_OK) return sc;
+  fb::PredictLaunch a = make_launch(hidden, T, H, ld_hidden, dtype, router_packed, E, logit_bias,
+                                    select_bias, scoring, expert_to_rank, R, counts, rank_loads,
+                                    max_mean, scratch, topk_idx, logits, stream);
+  if (sb > 0) {
+    a.partial = reinterpret_cast<float*>(static_cast<char*>(scratch) + fb::kWsBytes);
+    a.partial_bytes = fb::kNoAllocPartialBytes;
+  }
+  return fb::launch_predict(a);
+}
+
 size_t fb_predict_split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype) {
   if (T < 0 || E < 1 || E > FB_MAX_EXPERTS || H < 1 || (dtype != FB_BF16 && dtype != FB_F32))
     return 0;

@@ -42,6 +42,15 @@ constexpr size_t kWsAccOffset = 0;
 constexpr size_t kWsTicketOffset = 1024;
 constexpr size_t kWsBytes = 2048;
 
+// Scratch of fb_predict_load_packed_noalloc: a workspace header, then room for the split mode's
+// partial logits of the largest batch that runs split on 256 CUs (at most 128 tiles, 4 splits, 64
+// tokens x 256 experts or 128 x 32 per tile: 128 * 4 * 64 * 256 * 4 bytes = 32 MiB).
+constexpr size_t kNoAllocPartialBytes = (size_t)32 << 20;
+constexpr size_t kNoAllocScratchBytes = kWsBytes + kNoAllocPartialBytes;
+// Device address of this device's scratch (set up once per device: symbol lookup, then a fill
+// kernel on `stream` that zeroes its header).  FB_OK, FB_EDEVICE or FB_EUNSUPPORTED.
+int noalloc_scratch(void** ptr, void* stream);
+
 // Bytes of the packed router weight for E experts of H elements of `dtype`.
 size_t router_packed_bytes(int32_t E, int32_t H, int32_t dtype);
 // Rewrites the E x H row-major router weight into the fragment-major layout the predictor kernel

@@ -33,6 +33,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "fb_internal.h"
@@ -1202,6 +1203,43 @@ int launch_workspace_zero(void* workspace, size_t bytes, void* stream) {
   hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(256), 0, static_cast<hipStream_t>(stream),
                      static_cast<uint32_t*>(workspace), bytes / 4);
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
+}
+
+// ---- scratch of the no-allocation entry point ----------------------------------------------------
+// fb_predict_load_packed_noalloc runs the kernels above with this array as its workspace.  In host
+// code its name is not a device address: the address of each device's copy comes from
+// hipGetSymbolAddress and is kept per device.
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxScratchDevices];
+}  // namespace
+
+int noalloc_scratch(void** ptr, void* stream) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+    (void)hipGetLastError();
+    return FB_EDEVICE;
+  }
+  if (dev >= kMaxScratchDevices) return FB_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return FB_EDEVICE;
+    }
+    // The header (accumulators and ticket) must start at zero; every completed call leaves it
+    // zeroed again.  A fill kernel rather than a memset node, so a first call made under graph
+    // capture stays valid on every replay.
+    const int zc = launch_workspace_zero(p, kWsBytes, stream);
+    if (zc != FB_OK) return zc;
+    g_scratch_addr[dev] = p;
+  }
+  *ptr = g_scratch_addr[dev];
+  return FB_OK;
 }
 
 }  // namespace fb

@@ -36,7 +36,7 @@ def test_header_declares_the_boundary():
                             "fb_topk_hits", "fb_cosine_workspace_bytes", "fb_row_cosine_mean",
                             "fb_fold_rank_loads", "fb_plan_swaps_timed",
                             "fb_plan_swaps_timed_device", "fb_predict_split_workspace_bytes",
-                            "fb_fold_slot_loads"])
+                            "fb_fold_slot_loads", "fb_predict_load_packed_noalloc"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -354,6 +354,36 @@ def _predict_packed_call(**over):
 ])
 def test_predict_packed_validation_without_gpu(over, code):
     assert _predict_packed_call(**over) == code
+
+
+def _predict_noalloc_call(**over):
+    """fb_predict_load_packed_noalloc with fake (never dereferenced) pointers."""
+    a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, wp=0x2000, wpb=8192, E=16, lb=None,
+             sb=None, sc=fb.Scoring("softmax", 2).to_c(), e2r=0x3000, R=4, counts=0x4000,
+             rl=0x5000, mm=0x6000, topk=None, logits=None, stream=None)
+    a.update(over)
+    sc = a["sc"]
+    return fb.lib().fb_predict_load_packed_noalloc(
+        a["hidden"], a["T"], a["H"], a["ld"], a["dtype"], a["wp"], a["wpb"], a["E"], a["lb"],
+        a["sb"], ctypes.byref(sc) if sc is not None else None, a["e2r"], a["R"], a["counts"],
+        a["rl"], a["mm"], a["topk"], a["logits"], a["stream"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(wp=None), L.FB_EINVAL),
+    (dict(wp=0x2008), L.FB_EUNSUPPORTED),
+    (dict(wpb=8191), L.FB_ENOSPC),
+    (dict(counts=None), L.FB_EINVAL),
+    (dict(mm=None), L.FB_EINVAL),
+    (dict(sc=None), L.FB_EINVAL),
+    (dict(T=-2), L.FB_EINVAL),
+    (dict(H=48), L.FB_EUNSUPPORTED),
+    (dict(R=5000), L.FB_EUNSUPPORTED),
+    (dict(sb=0x8000), L.FB_EINVAL),
+])
+def test_predict_noalloc_validation_without_gpu(over, code):
+    """Arguments are checked before the scratch is looked up or anything is launched."""
+    assert _predict_noalloc_call(**over) == code
 
 
 def test_unpacked_predict_needs_room_for_the_packed_weight():
