@@ -59,32 +59,146 @@ def traffic_from_profile():
         return None
 
 
-def cpu_baseline(wl, li, e2r, slots, target_s: float):
-    """The CPU oracle, as it stands, on a bounded prefix of the same workload."""
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, li, e2r, slots, target_s: float, gpu_topk, gpu_counts):
+    """The CPU oracle, as it stands, on the same workload: whole batches repeated for about
+    target_s seconds over the BLAS threads NumPy uses, plus one-thread passes of the Tiny and
+    Mixtral-shaped configs.  Also checks the timed layer's GPU counts against the oracle's: the
+    difference is exactly the histogram difference of the tokens whose selections differ, so
+    ||n_gpu - n_oracle||_1 <= 2k * #differing, and at most 0.2% of the tokens may differ."""
     import oracle.planner as OPL
     import oracle.predictor as OPR
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max(int(i.get("num_threads", 1)) for i in threadpool_info()) if threadpool_info() else 1
-    except Exception:  # pragma: no cover - threadpoolctl is optional
-        cores = os.cpu_count() or 1
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from workloads import CONFIGS, contiguous_placement, make_layer
 
-    def run():
+    info = threadpool_info()
+    blas = [{"api": i.get("internal_api"), "version": i.get("version"),
+             "threads": int(i.get("num_threads", 1))} for i in info if i.get("user_api") == "blas"]
+    cores = max([b["threads"] for b in blas] or [1])
+
+    def run(w, l, e2r_, slots_, B):
         t0 = time.perf_counter()
-        out = OPR.predict_load(li.x, li.w, wl.dtype, wl.k, wl.kind, e2r, wl.R,
-                               select_bias=li.select_bias, n_group=wl.n_group,
-                               topk_group=wl.topk_group, group_topn=wl.group_topn)
-        OPL.plan_swaps(out["counts"], slots, wl.budget)
-        return time.perf_counter() - t0
+        out = OPR.predict_load(l.x, l.w, w.dtype, w.k, w.kind, e2r_, w.R, select_bias=l.select_bias,
+                               n_group=w.n_group, topk_group=w.topk_group, group_topn=w.group_topn)
+        OPL.plan_swaps(out["counts"], slots_, B)
+        return time.perf_counter() - t0, out
 
-    reps, dt = 0, 0.0
+    reps, dt, ref = 0, 0.0, None
     while reps == 0 or dt < target_s:
-        dt += run()
+        d, ref = run(wl, li, e2r, slots, wl.budget)
+        dt += d
         reps += 1
+    # the timed layer's GPU result against the oracle
+    differ = int(np.count_nonzero(np.any(np.sort(gpu_topk, 1) != np.sort(ref["topk"], 1), axis=1)))
+    l1 = int(np.abs(np.asarray(gpu_counts, np.int64) - ref["counts"]).sum())
+    assert np.array_equal(np.bincount(gpu_topk.reshape(-1), minlength=wl.E)[:wl.E], gpu_counts), \
+        "GPU counts are not the histogram of its selections"
+    assert differ <= 0.002 * wl.T and l1 <= 2 * wl.k * differ, \
+        f"GPU counts against the oracle: {differ} tokens differ, L1 {l1}"
+    single = {}
+    with threadpool_limits(limits=1):
+        for name in ("tiny", "mixtral"):
+            w = CONFIGS[name]
+            sl, er = contiguous_placement(w.E, w.R, w.S)
+            lw = make_layer(w, 0)
+            n, t = 0, 0.0
+            while n == 0 or t < 1.0:
+                t += run(w, lw, er, sl, w.budget)[0]
+                n += 1
+            single[name] = {"tokens_per_s": n * w.T / t, "passes": n, "T": w.T, "H": w.H, "E": w.E}
     return {"value": reps * wl.T / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": f"the whole {wl.T}-token DeepSeek-V3-shaped batch (layer 0), {reps} passes: "
                       f"float64 router GEMM, scoring, group-limited top-8, histogram, rank fold and "
-                      f"the frontier planner (B={wl.budget}); {dt:.1f} s"}
+                      f"the frontier planner (B={wl.budget}); {dt:.1f} s",
+            "cpu_model": _cpu_model(), "blas": blas,
+            "single_thread": single,
+            "gpu_vs_oracle": {"tokens_differing": differ, "counts_l1": l1}}
+
+
+def attention_standin(torch, dev, seqs=4, seq_len=8192, heads=128, head_dim=128, group=16):
+    """An attention-shaped stand-in for one DeepSeek-V3-shaped prefill layer: for each of `seqs`
+    sequences of seq_len tokens and each of `heads` heads of head_dim, S = Q K^T and O = S V as bf16
+    batched GEMMs (groups of `group` heads per call).  Returns run(stream), which enqueues one layer
+    of it.  The operands are contiguous (K is stored transposed)."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    n = seqs * heads
+    q = torch.randn((n, seq_len, head_dim), generator=g, device=dev, dtype=torch.bfloat16)
+    kt = torch.randn((n, head_dim, seq_len), generator=g, device=dev, dtype=torch.bfloat16)
+    v = torch.randn((n, seq_len, head_dim), generator=g, device=dev, dtype=torch.bfloat16)
+    sc = torch.empty((group, seq_len, seq_len), device=dev, dtype=torch.bfloat16)
+    o = torch.empty((group, seq_len, head_dim), device=dev, dtype=torch.bfloat16)
+    flops = 2 * 2.0 * n * seq_len * seq_len * head_dim
+
+    def run(stream):
+        with torch.cuda.stream(stream):
+            for i in range(0, n, group):
+                torch.bmm(q[i:i + group], kt[i:i + group], out=sc)
+                torch.bmm(sc, v[i:i + group], out=o)
+    return run, flops
+
+
+def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, counts_for_plan):
+    """The paper's overlap (Fig. 1, stages 1-2 under attention): the attention stand-in on one
+    stream, the predictor and the device planner on a side stream.  Times attention alone,
+    prediction + planning alone and both together; the attention time gives the layer's migration
+    budget B_l = max(0, T_attn - delta) (Eq. 10, with delta = the prediction + planning time it
+    must also cover), which the time-budgeted device planner then spends."""
+    dev = x.device
+    main = torch.cuda.current_stream(dev)
+    side = torch.cuda.Stream(dev)
+    attn, attn_flops = attention_standin(torch, dev)
+    pred = fb.Predictor(dev, stream=side)
+    out = pred.predict_load(x, wp, scoring, e2r_t, wl.R, select_bias=sb, stream=side)
+    plan = fb.plan_swaps_device(out.counts, slots_t, budget, stream=side)
+    torch.cuda.synchronize()
+
+    def timed(use_attn, use_pp, reps=3):
+        best = None
+        for _ in range(reps):
+            st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e_side = torch.cuda.Event()
+            torch.cuda.synchronize()
+            st.record(main)
+            side.wait_event(st)
+            if use_attn:
+                attn(main)
+            if use_pp:
+                pred.predict_load(x, wp, scoring, e2r_t, wl.R, select_bias=sb, out=out, stream=side)
+                fb.plan_swaps_device(out.counts, slots_t, budget, out=plan, stream=side)
+            e_side.record(side)
+            main.wait_event(e_side)
+            en.record(main)
+            torch.cuda.synchronize()
+            ms = st.elapsed_time(en)
+            best = ms if best is None else min(best, ms)
+        return best
+
+    timed(True, True, 2)
+    t_attn, t_pp, t_both = timed(True, False), timed(False, True), timed(True, True)
+    hidden = (t_attn + t_pp - t_both) / t_pp if t_pp > 0 else None
+    B_ns = max(0, int((t_attn - t_pp) * 1e6))
+    nodes_t = torch.tensor([r // 8 for r in range(wl.R)], dtype=torch.int32, device=dev)
+    sizes_t = torch.full((wl.E,), 3 * 7168 * 2048 * 2, dtype=torch.int64, device=dev)
+    cm = fb.CostModel(nodes_t, sizes_t, (20_000, 50_000), (100_000, 25_000), B_ns)
+    tplan = fb.plan_swaps_timed_device(counts_for_plan, slots_t, fb.Budget(64), cm).to_host()
+    return {"attention_standin": "4 sequences x 8192 tokens x 128 heads x 128 dims: S = QK^T and "
+                                 "O = SV as bf16 batched GEMMs (hipBLASLt via torch.bmm), main stream",
+            "attention_tflops": attn_flops / (t_attn * 1e-3) / 1e12,
+            "t_attn_ms": t_attn, "t_predict_plan_ms": t_pp, "t_both_ms": t_both,
+            "hidden_fraction": hidden,
+            "B_l_ns": B_ns, "B_l_rule": "max(0, T_attn - delta), delta = predict + plan time",
+            "timed_plan_swaps": len(tplan.swaps), "timed_plan_cost_ns": sum(tplan.costs or [])}
 
 
 def _time_ms(torch, stream, fn, K):
@@ -167,9 +281,11 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    # The chip needs roughly 20-40 ms of sustained load before its clocks settle (measured: the first
-    # launches take up to 1.5x the steady-state time), so the default warm-up is long.
-    ap.add_argument("--warmup", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=20)
+    # The chip needs roughly 20-40 ms of sustained load before its clocks settle (the first launches
+    # take up to 1.5x the steady-state time), and the CPU leg leaves it idle for seconds: before the
+    # warm-up steps, steps run for at least this long (not counted as warm-up or timed steps).
+    ap.add_argument("--settle-ms", type=float, default=300.0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     # The bench line is the DeepSeek-V3-shaped batch.  The other input shapes can be timed the same
@@ -219,11 +335,33 @@ def main():
         pred.predict_load(xs[i % nbuf], router, scoring, e2r_t, wl.R, select_bias=sb, out=out)
         fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
 
+    # the timed layer once with its selections, for the check against the oracle in the CPU leg
+    dbg = pred.predict_load(x0, wp, scoring, e2r_t, wl.R, select_bias=sb, return_topk=True)
+    torch.cuda.synchronize()
+    gpu_topk, gpu_counts = dbg.topk.cpu().numpy(), dbg.counts.cpu().numpy().astype(np.int64)
+    cpu = None
+    if not args.no_cpu_baseline and default:
+        cpu = cpu_baseline(wl, li, e2r, slots, args.cpu_seconds, gpu_topk, gpu_counts)
+    extras = None
+    if default:
+        extras = measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t,
+                                slots_t, sb, pred, out, stream)
+        extras["overlap"] = measure_overlap(fb, torch, wl, x0, wp, scoring, budget, e2r_t, slots_t,
+                                            sb, dbg.counts)
+
+    # clocks to their sustained state, then the warm-up steps
+    t0 = time.perf_counter()
+    n_settle = 0
+    while (time.perf_counter() - t0) * 1e3 < args.settle_ms:
+        for i in range(20):
+            step(n_settle + i, wp)
+        n_settle += 20
+        torch.cuda.synchronize()
     for i in range(args.warmup):
         step(i, wp)
-        step(i, w)
     torch.cuda.synchronize()
 
+    # the timed steps
     K = args.steps
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
@@ -235,17 +373,23 @@ def main():
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
 
-    # the predictor kernel alone: K launches back to back, bracketed by events on its stream.  With
-    # no idle gap between launches the chip sustains a slightly lower clock than inside the step,
-    # so this duration is the conservative one.
-    k_start = torch.cuda.Event(enable_timing=True)
-    k_end = torch.cuda.Event(enable_timing=True)
-    k_start.record(stream)
-    for i in range(K):
-        pred.predict_load(xs[i % nbuf], wp, scoring, e2r_t, wl.R, select_bias=sb, out=out)
-    k_end.record(stream)
+    # the same K steps again with the predictor launch of every step bracketed by events on its
+    # stream: the kernel's own duration (the markers between launches add a few microseconds to
+    # each step, so the step time above is taken without them)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    i_start = torch.cuda.Event(enable_timing=True)
+    i_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    avg_kernel_s = k_start.elapsed_time(k_end) / K / 1e3
+    i_start.record(stream)
+    for i in range(K):
+        ev[i][0].record(stream)
+        pred.predict_load(xs[i % nbuf], wp, scoring, e2r_t, wl.R, select_bias=sb, out=out)
+        ev[i][1].record(stream)
+        fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
+    i_end.record(stream)
+    torch.cuda.synchronize()
+    avg_kernel_s = sum(a.elapsed_time(b) for a, b in ev) / K / 1e3
+    instrumented_ms = i_start.elapsed_time(i_end) / K
 
     # the device planner alone, K launches back to back on the final counts
     p_start = torch.cuda.Event(enable_timing=True)
@@ -262,7 +406,7 @@ def main():
     g_start = torch.cuda.Event(enable_timing=True)
     g_end = torch.cuda.Event(enable_timing=True)
     wt = w.t()
-    for i in range(min(args.warmup, 50)):
+    for i in range(20):
         torch.matmul(xs[i % nbuf], wt)
     g_start.record(stream)
     for i in range(K):
@@ -273,8 +417,6 @@ def main():
 
     counts = out.counts.cpu().numpy()
     host_plan = plan.to_host()
-    extras = (measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t, slots_t,
-                             sb, pred, out, stream) if default else None)
 
     # the same step with fb_predict_load, which repacks the router weight on every call
     u_start = torch.cuda.Event(enable_timing=True)
@@ -287,6 +429,7 @@ def main():
     torch.cuda.synchronize()
     unpacked_ms = u_start.elapsed_time(u_end) / K
     assert np.array_equal(out.counts.cpu().numpy(), counts), "packed and repacking paths disagree"
+    assert np.array_equal(counts.astype(np.int64), gpu_counts), "timed steps disagree with the checked run"
     assert int(counts.sum()) == wl.T * wl.k, "predictor output failed its invariant"
     assert len(host_plan.swaps) <= wl.budget
 
@@ -317,11 +460,15 @@ def main():
                                                                   dev) > 2048,
                    "step": "fb_predict_load_packed + fb_plan_swaps_device, one stream",
                    "router_packing": "once, before timing (fb_pack_router_weight)"},
+        "clock_settle": {"ms": args.settle_ms, "steps": n_settle},
+        "ms_per_step_with_launch_events": instrumented_ms,
         "ms_per_step_repacking_router": unpacked_ms,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,
                      "traffic": traffic_from_profile() if default else None,
                      "bytes_per_launch": nbytes, "kernel_ms": avg_kernel_s * 1e3,
+                     "kernel_ms_from": "HIP events around every predictor launch of K steps run "
+                                       "right after the timed ones",
                      "mfma": {"achieved": tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                               "frac": tflops / PEAK_BF16_TFLOPS}},
         "context": {"hipblaslt_router_gemm_ms": gemm_ms,
@@ -332,11 +479,8 @@ def main():
         "plan": {"swaps": len(host_plan.swaps), "kernel_ms": plan_ms,
                  "max_mean_before": float(out.max_mean.item()),
                  "max_mean_after": float(host_plan.rank_loads.max() * wl.R / host_plan.rank_loads.sum())},
+        "cpu_baseline": cpu,
     }
-    if not args.no_cpu_baseline and default:
-        result["cpu_baseline"] = cpu_baseline(wl, li, e2r, slots, args.cpu_seconds)
-    else:
-        result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)
 
 

@@ -6,9 +6,10 @@ stream, extra])))`` so that any (workload, layer, stream) can be regenerated on 
 * ``STREAM_ROUTER``  router weight of the layer, N(0, 0.02^2), shape E x H;
 * ``STREAM_BIAS``    per-expert selection bias, N(0, 0.01^2) (sigmoid-scored workloads only);
 * ``STREAM_CLUSTER`` token -> cluster draw, shared by every layer of a workload (layer slot 0);
-* ``STREAM_NOISE``   per-layer hidden-state noise N(0, 1);
+* ``STREAM_NOISE``   per-layer hidden-state noise N(0, 1), one generator per 2048-row chunk
+  (``extra`` = chunk index + 1);
 * ``STREAM_RESID``   per-layer residual update N(0, sigma^2) that turns h_{l-1} into the target
-  router input H_l.
+  router input H_l, one generator per chunk like the noise.
 
 The hidden state entering layer l is ``h = 3 * w_l[z_t] + N(0, 1)`` for token cluster ``z_t``, so a
 token's own cluster expert gets a large logit and the cluster frequencies (truncated Zipf) become the
@@ -21,6 +22,8 @@ the planner.
 from __future__ import annotations
 
 import dataclasses
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Optional, Sequence, Tuple
 
 import numpy as np
@@ -246,13 +249,23 @@ def _store(wl: Workload, a: np.ndarray) -> np.ndarray:
     return bf16_bits_from_f32(a) if wl.dtype == "bf16" else np.ascontiguousarray(a, np.float32)
 
 
+def _workers() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover - non-Linux
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
 def make_layer(wl: Workload, layer: int = 0, with_target: bool = False,
                rows: Optional[Sequence[int]] = None) -> LayerInputs:
     """Generate layer ``layer`` of workload ``wl``.
 
-    ``rows`` restricts the returned hidden states to those token rows (the bytes of each row are
-    identical to the full generation); the chunked draw still visits every chunk up to the last row
-    requested, which keeps sampled rows bit-identical to a full run.
+    Token rows come in chunks of ``_CHUNK`` rows; chunk c draws its hidden-state noise and its
+    residual update from generators of their own (``extra`` = c + 1), so chunks are generated
+    independently (in parallel threads) and any subset of rows is bit-identical to the full draw.
+    ``rows`` restricts the returned hidden states to those token rows (only the chunks holding them
+    are generated).
     """
     T, H, E = wl.T, wl.H, wl.E
     w32 = rng(wl.cfg_id, layer, STREAM_ROUTER).normal(0.0, 0.02, size=(E, H)).astype(np.float32)
@@ -263,31 +276,39 @@ def make_layer(wl: Workload, layer: int = 0, with_target: bool = False,
     centers = np.float32(3.0) * w32
 
     want = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
-    last = int(want.max()) + 1 if want.size else 0
-    pos = {int(t): i for i, t in enumerate(want)} if rows is not None else None
     store_dtype = np.uint16 if wl.dtype == "bf16" else np.float32
     x_out = np.empty((want.size, H), dtype=store_dtype)
     h_out = np.empty((want.size, H), dtype=store_dtype) if with_target else None
-    g_noise = rng(wl.cfg_id, layer, STREAM_NOISE)
-    g_res = rng(wl.cfg_id, layer, STREAM_RESID)
-    for c0 in range(0, last, _CHUNK):
+    if rows is None:
+        chunks = list(range(0, T, _CHUNK))
+    else:
+        chunks = sorted({int(t) // _CHUNK * _CHUNK for t in want})
+
+    def one(c0: int) -> None:
         c1 = min(T, c0 + _CHUNK)
-        h = centers[clusters[c0:c1]] + g_noise.standard_normal((c1 - c0, H), dtype=np.float32)
+        cid = c0 // _CHUNK + 1
+        h = centers[clusters[c0:c1]] + rng(wl.cfg_id, layer, STREAM_NOISE, cid).standard_normal(
+            (c1 - c0, H), dtype=np.float32)
         if with_target:
-            upd = g_res.standard_normal((c1 - c0, H), dtype=np.float32)
+            upd = rng(wl.cfg_id, layer, STREAM_RESID, cid).standard_normal((c1 - c0, H), dtype=np.float32)
             # sigma = 0 must give H_l identical to h_{l-1} bit for bit (no -0.0 -> +0.0 flips)
             ht = h.copy() if wl.sigma == 0 else h + np.float32(wl.sigma) * upd
-        if pos is None:
+        if rows is None:
             x_out[c0:c1] = _store(wl, h)
             if with_target:
                 h_out[c0:c1] = _store(wl, ht)
         else:
-            idx = [t for t in range(c0, c1) if t in pos]
-            if idx:
-                loc = np.array(idx) - c0
-                dst = [pos[t] for t in idx]
-                x_out[dst] = _store(wl, h[loc])
-                if with_target:
-                    h_out[dst] = _store(wl, ht[loc])
+            sel = np.nonzero((want >= c0) & (want < c1))[0]
+            loc = want[sel] - c0
+            x_out[sel] = _store(wl, h[loc])
+            if with_target:
+                h_out[sel] = _store(wl, ht[loc])
+
+    if len(chunks) > 1 and _workers() > 1:
+        with ThreadPoolExecutor(max_workers=_workers()) as ex:
+            list(ex.map(one, chunks))
+    else:
+        for c0 in chunks:
+            one(c0)
     return LayerInputs(x=x_out, w=_store(wl, w32), select_bias=sb, logit_bias=None,
                        h_target=h_out, clusters=clusters[want] if rows is not None else clusters)
