@@ -106,6 +106,8 @@ struct Shared {
   int64_t L[kMaxR];
   int32_t part[kMaxR];
   uint64_t wgain[16], wtie[16], wcost[16];
+  uint64_t rgain[16], rtie[16], rcost[16];   // full mode: per-wave bests of the first phase
+  int64_t cmin[2];               // time budget: the lowest cost of any swap on link type 0 / 1
   int64_t N;
   int32_t bad, stop, amax, amin, top[3], ns, J;
   int64_t other;
@@ -389,6 +391,26 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   const bool frontier = bg.mode == FB_FRONTIER;
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
   const bool marks = frontier && J > 1;
+  if (a.timed && !frontier) {
+    // every candidate moves at least one expert, so it costs at least alpha + the smallest
+    // expert's transfer time on its link
+    int64_t mb = INT64_MAX;
+    for (int e = tid; e < E; e += NT) mb = sh.u.run.ebytes[e] < mb ? sh.u.run.ebytes[e] : mb;
+    for (int off = 32; off > 0; off >>= 1) {
+      const int64_t o = __shfl_xor(mb, off);
+      mb = o < mb ? o : mb;
+    }
+    if (lane == 0) sh.rgain[wave] = (uint64_t)mb;
+    __syncthreads();
+    if (tid == 0) {
+      for (int w = 1; w < NT / 64; ++w) mb = (int64_t)sh.rgain[w] < mb ? (int64_t)sh.rgain[w] : mb;
+      for (int t = 0; t < 2; ++t) {
+        const int64_t beta = a.cost.beta_bytes_per_us[t];
+        sh.cmin[t] = a.cost.alpha_ns[t] + ceil_div(mb * 1000, beta, 1.0 / (double)beta);
+      }
+    }
+    __syncthreads();
+  }
   for (int round = 0; active && round < bg.max_swaps; ++round) {
     if (marks)                        // the previous round's reads ended at its last barrier
       for (int s2 = tid; s2 < S; s2 += NT) { sh.u.run.mrow[s2] = 0; sh.u.run.mcol[s2] = 0; }
@@ -492,17 +514,114 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         }
       }
     } else {
-      for (int pair = tid; pair < R * R; pair += NT) {
-        const int ra = pair / R, rb = pair - ra * R;
-        if (!(sh.L[ra] > sh.L[rb])) continue;
-        if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) continue;
+      // Full mode, in two phases.  Phase 1 scores every pair (amax, b); the best of those
+      // candidates (they stay in the threads' bests) is the reference.  Phase 2 scores the other
+      // pairs, skipping each pair whose benefit bound divided by the lowest cost on its link falls
+      // below the reference's ratio: none of its candidates can be the round's best.  For
+      // D = L_a - L_b > 0 and any swap, M' >= max(other, ceil((L_a + L_b) / 2)) and
+      // 2d (L_b - L_a - d) <= floor(D^2 / 2), so den (M - max(other, ceil((L_a + L_b) / 2))) +
+      // num floor(D^2 / 2) bounds the benefit.
+      // Work units are (rank pair, slot p of the first rank), interleaved over the threads so that
+      // skipped pairs spread evenly; what does not depend on the second rank's slot q is taken once
+      // per unit.
+      uint64_t ref_g = 0, ref_c = 1;
+      auto unit = [&](int ra, int rb, int p) {
+        const int64_t La = sh.L[ra], Lb = sh.L[rb];
+        if (!(La > Lb)) return;
+        const int sa = ra * S + p;
+        if (sh.mslot[sa]) return;
+        if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) return;
         int64_t other = INT64_MIN;
         for (int u = 0; u < 3; ++u) {
           const int tr = sh.top[u];
           if (tr >= 0 && tr != ra && tr != rb) { other = sh.L[tr]; break; }
         }
-        for (int p = 0; p < S; ++p)
-          for (int q = 0; q < S; ++q) consider(ra, rb, p, q, other);
+        {
+          const int64_t D = La - Lb;
+          const int64_t half = (La + Lb + 1) >> 1;
+          const int64_t mlo = other > half ? other : half;
+          const int64_t ub = g_den * (M - mlo) + g_num * ((D * D) >> 1);
+          if (ub <= 0) return;                       // no positive benefit on this pair
+          if (ref_g != 0) {
+            const int64_t cmin = a.timed ? sh.cmin[sh.node[ra] == sh.node[rb] ? 0 : 1] : 1;
+            if ((unsigned __int128)ub * ref_c < (unsigned __int128)ref_g * (uint64_t)cmin) return;
+          }
+        }
+        const int i = sh.item[sa];
+        const int64_t li = sh.sload[sa];
+        const int ei = i >= V ? -1 : J == 1 ? i : expert_of(i, E, inv_e);
+        // time budget: the pair's link, and what the candidate's cost may be at most
+        int64_t alpha = 0, beta = 1, cap_ns = 0, bi = 0;
+        double inv_beta = 1.0;
+        bool link_scan = false;
+        if (a.timed) {
+          const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
+          alpha = a.cost.alpha_ns[t];
+          beta = a.cost.beta_bytes_per_us[t];
+          inv_beta = 1.0 / (double)beta;
+          cap_ns = sh.rank_left[ra] < sh.rank_left[rb] ? sh.rank_left[ra] : sh.rank_left[rb];
+          if (alpha > cap_ns) return;              // no swap on this link fits any more
+          link_scan = a.cost.link_budget_ns < a.cost.rank_budget_ns;
+          bi = ei >= 0 ? sh.u.run.ebytes[ei] : 0;
+        }
+        const int64_t spread0 = Lb - La;
+        for (int q = 0; q < S; ++q) {
+          const int sb = rb * S + q;
+          const int j = sh.item[sb];
+          if (sh.mslot[sb] || (i >= V && j >= V)) continue;
+          if (J > 1 && ((i < V && holds(rb, i)) || (j < V && holds(ra, j)))) continue;
+          const int64_t d = (int64_t)sh.sload[sb] - li;
+          const int64_t la = La + d, lb = Lb - d;
+          int64_t m2 = la > lb ? la : lb;
+          if (other > m2) m2 = other;
+          const int64_t gain = g_den * (M - m2) + (g_num ? g_num * (2 * d * (spread0 - d)) : 0);
+          if (gain <= 0) continue;
+          const uint64_t tk = tie_key(ra, rb, i, j);
+          if (a.timed) {
+            const int ej = j >= V ? -1 : J == 1 ? j : expert_of(j, E, inv_e);
+            const int64_t bytes = bi + (ej >= 0 ? sh.u.run.ebytes[ej] : 0);
+            const int64_t c = alpha + ceil_div(bytes * 1000, beta, inv_beta);
+            if (c > cap_ns) continue;
+            if (link_scan && !swap_fits(a, sh, ra, rb, c)) continue;
+            if (ratio_better((uint64_t)gain, (uint64_t)c, tk, bgain, bcost, btie)) {
+              bgain = (uint64_t)gain; bcost = (uint64_t)c; btie = tk;
+            }
+          } else if ((uint64_t)gain > bgain || ((uint64_t)gain == bgain && tk < btie)) {
+            bgain = (uint64_t)gain; btie = tk;
+          }
+        }
+      };
+      // phase 1: the pairs (amax, b)
+      for (int un = tid; un < R * S; un += NT) {
+        const int rb = un / S;
+        unit(amax, rb, un - rb * S);
+      }
+      {
+        uint64_t rg = bgain, rc = bcost, rt = btie;
+        for (int off = 32; off > 0; off >>= 1) {
+          const uint64_t og = __shfl_xor(rg, off), oc = __shfl_xor(rc, off), ot = __shfl_xor(rt, off);
+          const bool better = a.timed ? ratio_better(og, oc, ot, rg, rc, rt)
+                                      : (og > rg || (og == rg && og != 0 && ot < rt));
+          if (better) { rg = og; rc = oc; rt = ot; }
+        }
+        if (lane == 0) { sh.rgain[wave] = rg; sh.rcost[wave] = rc; sh.rtie[wave] = rt; }
+        __syncthreads();
+        rg = sh.rgain[0]; rc = sh.rcost[0]; rt = sh.rtie[0];
+        for (int w = 1; w < NT / 64; ++w) {
+          const bool better = a.timed ? ratio_better(sh.rgain[w], sh.rcost[w], sh.rtie[w], rg, rc, rt)
+                                      : (sh.rgain[w] > rg || (sh.rgain[w] == rg && rg != 0 && sh.rtie[w] < rt));
+          if (better) { rg = sh.rgain[w]; rc = sh.rcost[w]; rt = sh.rtie[w]; }
+        }
+        ref_g = rg;
+        ref_c = a.timed ? rc : 1;
+      }
+      // phase 2: every other pair
+      const int units = R * R * S;
+      for (int un = tid; un < units; un += NT) {
+        const int pair = un / S, p = un - pair * S;
+        const int ra = pair / R;
+        if (ra == amax) continue;
+        unit(ra, pair - ra * R, p);
       }
     }
     uint64_t g, t, cst = 1;
