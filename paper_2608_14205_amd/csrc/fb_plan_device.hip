@@ -43,6 +43,8 @@ constexpr int kRankBits = 11;                 // R <= 1024 < 2^11
 constexpr int kItemBits = 21;                 // item ids < V + R * S <= 2^21 (checked)
 constexpr int kSmallItemBits = 13;            // ... < E + R * S <= 8192 without replicas
 constexpr int64_t kLoadCap = (int64_t)1 << 43;  // loads <= 4096 experts * (2^31 - 1) < 2^43
+constexpr int kMaxSurvivors = 8192;           // full mode: work units listed per round (more are
+                                              // evaluated where their bound test ran)
 
 template <int CTRL>
 __device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
@@ -100,6 +102,10 @@ struct Shared {
       // frontier rounds with replicas: slot p of amax (row) or q of amin (column) holds a replica
       // of an expert that the other rank also holds
       uint8_t mrow[kMaxRS], mcol[kMaxRS];
+      // full mode: the smallest and largest load among each rank's items that have not moved
+      // (smin > smax when every item has moved), and the work units left after the bound test
+      int32_t smin[kMaxR], smax[kMaxR];
+      int32_t surv[kMaxSurvivors];
     } run;
   } u;
   int32_t wsum[16];
@@ -108,6 +114,7 @@ struct Shared {
   uint64_t wgain[16], wtie[16], wcost[16];
   uint64_t rgain[16], rtie[16], rcost[16];   // full mode: per-wave bests of the first phase
   int64_t cmin[2];               // time budget: the lowest cost of any swap on link type 0 / 1
+  int32_t nsurv;                 // full mode: work units that passed this round's bound test
   int64_t N;
   int32_t bad, stop, amax, amin, top[3], ns, J;
   int64_t other;
@@ -450,6 +457,19 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         sh.stop = (sh.L[amax] - sh.L[amin] <= bg.tau) ? 1 : 0;
       }
     }
+    if (!frontier) {
+      for (int r = tid; r < R; r += NT) {
+        int32_t lo = INT32_MAX, hi = INT32_MIN;
+        for (int q = 0; q < S; ++q) {
+          if (sh.mslot[r * S + q]) continue;
+          const int32_t l = sh.sload[r * S + q];
+          lo = l < lo ? l : lo;
+          hi = l > hi ? l : hi;
+        }
+        sh.u.run.smin[r] = lo;
+        sh.u.run.smax[r] = hi;
+      }
+    }
     __syncthreads();
     if (sh.stop) break;
 
@@ -516,39 +536,53 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
     } else {
       // Full mode, in two phases.  Phase 1 scores every pair (amax, b); the best of those
       // candidates (they stay in the threads' bests) is the reference.  Phase 2 scores the other
-      // pairs, skipping each pair whose benefit bound divided by the lowest cost on its link falls
-      // below the reference's ratio: none of its candidates can be the round's best.  For
-      // D = L_a - L_b > 0 and any swap, M' >= max(other, ceil((L_a + L_b) / 2)) and
-      // 2d (L_b - L_a - d) <= floor(D^2 / 2), so den (M - max(other, ceil((L_a + L_b) / 2))) +
-      // num floor(D^2 / 2) bounds the benefit.
+      // pairs, skipping each work unit whose benefit bound divided by the lowest cost on its link
+      // falls below the reference's ratio: none of its candidates can be the round's best.  The
+      // bound of a unit (pair, slot p) is the benefit at the best load difference d = l_j - l_i
+      // that rank b's unmoved items allow.
       // Work units are (rank pair, slot p of the first rank), interleaved over the threads so that
       // skipped pairs spread evenly; what does not depend on the second rank's slot q is taken once
       // per unit.
       uint64_t ref_g = 0, ref_c = 1;
-      auto unit = [&](int ra, int rb, int p) {
+      // unit(..., false) runs the checks and the bound and tells whether the unit can hold the
+      // round's best; unit(..., true, q0, qs) also scores its candidates q = q0, q0 + qs, ... (a
+      // unit's candidates may be shared among several threads)
+      auto unit = [&](int ra, int rb, int p, bool eval, int q0 = 0, int qs = 1) -> bool {
         const int64_t La = sh.L[ra], Lb = sh.L[rb];
-        if (!(La > Lb)) return;
+        if (!(La > Lb)) return false;
         const int sa = ra * S + p;
-        if (sh.mslot[sa]) return;
-        if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) return;
+        if (sh.mslot[sa]) return false;
+        if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) return false;
         int64_t other = INT64_MIN;
         for (int u = 0; u < 3; ++u) {
           const int tr = sh.top[u];
           if (tr >= 0 && tr != ra && tr != rb) { other = sh.L[tr]; break; }
         }
-        {
-          const int64_t D = La - Lb;
-          const int64_t half = (La + Lb + 1) >> 1;
-          const int64_t mlo = other > half ? other : half;
-          const int64_t ub = g_den * (M - mlo) + g_num * ((D * D) >> 1);
-          if (ub <= 0) return;                       // no positive benefit on this pair
-          if (ref_g != 0) {
-            const int64_t cmin = a.timed ? sh.cmin[sh.node[ra] == sh.node[rb] ? 0 : 1] : 1;
-            if ((unsigned __int128)ub * ref_c < (unsigned __int128)ref_g * (uint64_t)cmin) return;
-          }
-        }
         const int i = sh.item[sa];
         const int64_t li = sh.sload[sa];
+        {
+          // d = l_j - l_i lies in [smin_b - l_i, smax_b - l_i]; the benefit is concave in d with
+          // its real maximum at d = -D/2 (both terms peak there), so over the integers of that
+          // range it is largest at the floor or the ceiling of the clipped optimum
+          const int64_t dlo = (int64_t)sh.u.run.smin[rb] - li, dhi = (int64_t)sh.u.run.smax[rb] - li;
+          if (dlo > dhi) return false;                     // every item of rank b has moved
+          const int64_t D = La - Lb;
+          auto bound_at = [&](int64_t d) -> int64_t {
+            d = d < dlo ? dlo : d > dhi ? dhi : d;
+            const int64_t la = La + d, lb = Lb - d;
+            int64_t m2 = la > lb ? la : lb;
+            if (other > m2) m2 = other;
+            return g_den * (M - m2) + g_num * (2 * d * (-D - d));
+          };
+          const int64_t dfl = -((D + 1) >> 1), dce = -(D >> 1);   // floor and ceiling of -D/2
+          const int64_t b1 = bound_at(dfl), b2 = bound_at(dce);
+          const int64_t ub = b1 > b2 ? b1 : b2;
+          if (ub <= 0) return false;                       // no positive benefit in this unit
+          if (ref_g != 0) {
+            const int64_t cmin = a.timed ? sh.cmin[sh.node[ra] == sh.node[rb] ? 0 : 1] : 1;
+            if ((unsigned __int128)ub * ref_c < (unsigned __int128)ref_g * (uint64_t)cmin) return false;
+          }
+        }
         const int ei = i >= V ? -1 : J == 1 ? i : expert_of(i, E, inv_e);
         // time budget: the pair's link, and what the candidate's cost may be at most
         int64_t alpha = 0, beta = 1, cap_ns = 0, bi = 0;
@@ -560,12 +594,13 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
           beta = a.cost.beta_bytes_per_us[t];
           inv_beta = 1.0 / (double)beta;
           cap_ns = sh.rank_left[ra] < sh.rank_left[rb] ? sh.rank_left[ra] : sh.rank_left[rb];
-          if (alpha > cap_ns) return;              // no swap on this link fits any more
+          if (sh.cmin[t] > cap_ns) return false;         // no swap on this link fits any more
           link_scan = a.cost.link_budget_ns < a.cost.rank_budget_ns;
           bi = ei >= 0 ? sh.u.run.ebytes[ei] : 0;
         }
+        if (!eval) return true;
         const int64_t spread0 = Lb - La;
-        for (int q = 0; q < S; ++q) {
+        for (int q = q0; q < S; q += qs) {
           const int sb = rb * S + q;
           const int j = sh.item[sb];
           if (sh.mslot[sb] || (i >= V && j >= V)) continue;
@@ -590,12 +625,17 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
             bgain = (uint64_t)gain; btie = tk;
           }
         }
+        return true;
       };
-      // phase 1: the pairs (amax, b)
-      for (int un = tid; un < R * S; un += NT) {
-        const int rb = un / S;
-        unit(amax, rb, un - rb * S);
+      // phase 1: the pairs (amax, b), each unit's candidates shared by up to S threads
+      {
+        const int qp = NT / (R * S) < 1 ? 1 : NT / (R * S) > S ? S : NT / (R * S);
+        for (int w = tid; w < R * S * qp; w += NT) {
+          const int un = w / qp, rb = un / S;
+          unit(amax, rb, un - rb * S, true, w - un * qp, qp);
+        }
       }
+      if (tid == 0) sh.nsurv = 0;
       {
         uint64_t rg = bgain, rc = bcost, rt = btie;
         for (int off = 32; off > 0; off >>= 1) {
@@ -615,13 +655,62 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         ref_g = rg;
         ref_c = a.timed ? rc : 1;
       }
-      // phase 2: every other pair
-      const int units = R * R * S;
-      for (int un = tid; un < units; un += NT) {
+      // phase 2: a bound test per pair, over every d = l_j - l_i its unmoved items allow, lists the
+      // units of the pairs that pass; the listed units (each with its own, tighter bound test) are
+      // then scored spread over all threads, so that a wave's lanes are not left idle behind the
+      // few pairs that survive
+      for (int pair = tid; pair < R * R; pair += NT) {
+        const int ra = pair / R, rb = pair - ra * R;
+        if (ra == amax) continue;
+        const int64_t La = sh.L[ra], Lb = sh.L[rb];
+        if (!(La > Lb)) continue;
+        if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) continue;
+        const int t = a.timed ? (sh.node[ra] == sh.node[rb] ? 0 : 1) : 0;
+        if (a.timed) {
+          const int64_t cap_ns = sh.rank_left[ra] < sh.rank_left[rb] ? sh.rank_left[ra] : sh.rank_left[rb];
+          if (sh.cmin[t] > cap_ns) continue;
+        }
+        const int64_t ia = sh.u.run.smin[ra], xa = sh.u.run.smax[ra];
+        const int64_t ib = sh.u.run.smin[rb], xb = sh.u.run.smax[rb];
+        if (ia > xa || ib > xb) continue;            // every item of a rank has moved
+        int64_t other = INT64_MIN;
+        for (int u = 0; u < 3; ++u) {
+          const int tr = sh.top[u];
+          if (tr >= 0 && tr != ra && tr != rb) { other = sh.L[tr]; break; }
+        }
+        const int64_t dlo = ib - xa, dhi = xb - ia, D = La - Lb;
+        auto bound_at = [&](int64_t d) -> int64_t {
+          d = d < dlo ? dlo : d > dhi ? dhi : d;
+          const int64_t la = La + d, lb = Lb - d;
+          int64_t m2 = la > lb ? la : lb;
+          if (other > m2) m2 = other;
+          return g_den * (M - m2) + g_num * (2 * d * (-D - d));
+        };
+        const int64_t b1 = bound_at(-((D + 1) >> 1)), b2 = bound_at(-(D >> 1));
+        const int64_t ub = b1 > b2 ? b1 : b2;
+        if (ub <= 0) continue;
+        if (ref_g != 0) {
+          const int64_t cmin = a.timed ? sh.cmin[t] : 1;
+          if ((unsigned __int128)ub * ref_c < (unsigned __int128)ref_g * (uint64_t)cmin) continue;
+        }
+        const int at = atomicAdd(&sh.nsurv, S);
+        if (at + S <= kMaxSurvivors) {
+          for (int p = 0; p < S; ++p) sh.u.run.surv[at + p] = pair * S + p;
+        } else {
+          for (int p = 0; p < S; ++p) unit(ra, rb, p, true);
+        }
+      }
+      __syncthreads();
+      // (a pair whose units did not fit was scored where it was tested; the list holds whole
+      // pairs, so its length is the largest multiple of S not beyond the capacity)
+      const int ns2 = sh.nsurv <= kMaxSurvivors ? sh.nsurv : (kMaxSurvivors / S) * S;
+      const int qp2 = ns2 == 0 ? 1 : NT / ns2 < 1 ? 1 : NT / ns2 > S ? S : NT / ns2;
+      for (int w = tid; w < ns2 * qp2; w += NT) {
+        const int k = w / qp2;
+        const int un = sh.u.run.surv[k];
         const int pair = un / S, p = un - pair * S;
         const int ra = pair / R;
-        if (ra == amax) continue;
-        unit(ra, pair - ra * R, p);
+        unit(ra, pair - ra * R, p, true, w - k * qp2, qp2);
       }
     }
     uint64_t g, t, cst = 1;
