@@ -375,9 +375,12 @@ def main():
 
     # the predictor kernel alone: K launches back to back right after the timed steps, bracketed by
     # events on its stream (a marker between every launch would add several microseconds of its
-    # own to each bracketed launch)
+    # own to each bracketed launch).  Three launches go first so that the start marker is reached
+    # with the following launches already queued: the GPU never waits for the host in between.
     k_start = torch.cuda.Event(enable_timing=True)
     k_end = torch.cuda.Event(enable_timing=True)
+    for i in range(3):
+        pred.predict_load(xs[i % nbuf], wp, scoring, e2r_t, wl.R, select_bias=sb, out=out)
     k_start.record(stream)
     for i in range(K):
         pred.predict_load(xs[i % nbuf], wp, scoring, e2r_t, wl.R, select_bias=sb, out=out)
