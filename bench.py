@@ -286,6 +286,8 @@ def main():
     # take up to 1.5x the steady-state time), and the CPU leg leaves it idle for seconds: before the
     # warm-up steps, steps run for at least this long (not counted as warm-up or timed steps).
     ap.add_argument("--settle-ms", type=float, default=300.0)
+    ap.add_argument("--streams", type=int, default=2,
+                    help="independent batches in flight during the timed steps (1 = one stream)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     # The bench line is the DeepSeek-V3-shaped batch.  The other input shapes can be timed the same
@@ -335,6 +337,35 @@ def main():
         pred.predict_load(xs[i % nbuf], router, scoring, e2r_t, wl.R, select_bias=sb, out=out)
         fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
 
+    # The timed steps keep `streams` independent batches in flight: step i runs on stream
+    # i mod streams with that stream's own workspace, outputs and plan, so one batch's planning and
+    # tail overlap the next batch's prediction.  Every step still predicts and plans its own batch.
+    lanes = []
+    for j in range(args.streams):
+        s_j = stream if args.streams == 1 else torch.cuda.Stream(dev)
+        o_j = fb.Prediction(torch.empty(wl.E, dtype=torch.int32, device=dev),
+                            torch.empty(wl.R, dtype=torch.int32, device=dev),
+                            torch.empty(1, dtype=torch.float64, device=dev))
+        lanes.append((s_j, fb.Predictor(dev, stream=s_j), o_j,
+                      fb.plan_swaps_device(o_j.counts, slots_t, budget, stream=s_j)))
+
+    def steps(first, n):
+        if args.streams > 1:
+            ev = torch.cuda.Event()
+            ev.record(stream)
+            for s_j, _, _, _ in lanes:
+                s_j.wait_event(ev)
+        for i in range(first, first + n):
+            s_j, p_j, o_j, pl_j = lanes[i % args.streams]
+            p_j.predict_load(xs[i % nbuf], wp, scoring, e2r_t, wl.R, select_bias=sb, out=o_j,
+                             stream=s_j)
+            fb.plan_swaps_device(o_j.counts, slots_t, budget, out=pl_j, stream=s_j)
+        if args.streams > 1:
+            for s_j, _, _, _ in lanes:
+                e = torch.cuda.Event()
+                e.record(s_j)
+                stream.wait_event(e)
+
     # the timed layer once with its selections, for the check against the oracle in the CPU leg
     dbg = pred.predict_load(x0, wp, scoring, e2r_t, wl.R, select_bias=sb, return_topk=True)
     torch.cuda.synchronize()
@@ -353,12 +384,10 @@ def main():
     t0 = time.perf_counter()
     n_settle = 0
     while (time.perf_counter() - t0) * 1e3 < args.settle_ms:
-        for i in range(20):
-            step(n_settle + i, wp)
+        steps(n_settle, 20)
         n_settle += 20
         torch.cuda.synchronize()
-    for i in range(args.warmup):
-        step(i, wp)
+    steps(0, args.warmup)
     torch.cuda.synchronize()
 
     # the timed steps
@@ -367,11 +396,26 @@ def main():
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record(stream)
-    for i in range(K):
-        step(i, wp)
+    steps(0, K)
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
+    # every batch's result: the same counts and plan as the checked run
+    for _, _, o_j, pl_j in lanes:
+        assert np.array_equal(o_j.counts.cpu().numpy().astype(np.int64), gpu_counts), \
+            "a timed step disagrees with the checked run"
+        assert len(pl_j.to_host().swaps) <= wl.budget
+
+    # the same K steps on one stream, one batch after the other (for reference)
+    o_start = torch.cuda.Event(enable_timing=True)
+    o_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    o_start.record(stream)
+    for i in range(K):
+        step(i, wp)
+    o_end.record(stream)
+    torch.cuda.synchronize()
+    one_stream_ms = o_start.elapsed_time(o_end) / K
 
     # the predictor kernel alone: K launches back to back right after the timed steps, bracketed by
     # events on its stream (a marker between every launch would add several microseconds of its
@@ -460,9 +504,12 @@ def main():
                                 if wl.n_group > 1 else "")),
                    "ranks": wl.R, "slots_per_rank": wl.S, "swap_budget": wl.budget,
                    "split_mode": split_mode,
-                   "step": "fb_predict_load_packed + fb_plan_swaps_device, one stream",
+                   "step": "fb_predict_load_packed + fb_plan_swaps_device on one batch; "
+                           f"{args.streams} batches in flight on {args.streams} streams",
                    "router_packing": "once, before timing (fb_pack_router_weight)"},
         "clock_settle": {"ms": args.settle_ms, "steps": n_settle},
+        "streams": args.streams,
+        "ms_per_step_one_stream": one_stream_ms,
         "ms_per_step_repacking_router": unpacked_ms,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,
