@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define FB_ABI_VERSION 3
+#define FB_ABI_VERSION 4
 
 /* Status codes. */
 #define FB_OK 0
@@ -264,13 +264,15 @@ size_t fb_predict_split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t
  * fb_predict_load on h_{l-1} and on the actual router input H_l with topk_idx / logits requested,
  * then compare. All three calls are stream-ordered and deterministic. */
 
-/* Top-k hit count: hits = sum over tokens of |predicted set intersect actual set|; the hit rate is
- * hits / (T * k).
+/* Top-k hit count and hit rate: hits = sum over tokens of |predicted set intersect actual set|,
+ * hit rate = hits / (T * k) (the fraction of the final top-k assignments the early pass recovers;
+ * 1.0 for T = 0).
  *   topk_pred, topk_actual  device int32[T * k], rows of k distinct expert ids in [0, 256).
  *   hits                    device int64 out (overwritten).
+ *   hit_rate                device double out (overwritten), or NULL.
  * FB_EINVAL for null pointers, T < 0 or k < 1; FB_EUNSUPPORTED for k > FB_MAX_TOPK. */
 int fb_topk_hits(const int32_t* topk_pred, const int32_t* topk_actual, int64_t T, int32_t k,
-                 int64_t* hits, void* stream);
+                 int64_t* hits, double* hit_rate, void* stream);
 
 /* Bytes of device workspace fb_row_cosine_mean needs. */
 size_t fb_cosine_workspace_bytes(void);

@@ -16,7 +16,7 @@ FB_OK, FB_EINVAL, FB_EUNSUPPORTED, FB_EDEVICE, FB_ENOSPC = 0, -1, -2, -3, -4
 FB_BF16, FB_F32 = 0, 1
 FB_SOFTMAX, FB_SIGMOID = 0, 1
 FB_FRONTIER, FB_FULL = 0, 1
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 
 class fb_scoring(ctypes.Structure):
@@ -80,7 +80,7 @@ SIGNATURES = {
                                                   ctypes.POINTER(fb_cost_model), _VP, _VP, _VP,
                                                   _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "fb_swap_budget_from_cost": (_I64, [_D, _D, _D, _D, _I64]),
-    "fb_topk_hits": (ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
+    "fb_topk_hits": (ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP, _VP]),
     "fb_cosine_workspace_bytes": (_SZ, []),
     "fb_row_cosine_mean": (ctypes.c_int, [_VP, _VP, _I64, _I32, _I64, _I64, _I32, _VP, _VP, _SZ, _VP]),
     "fb_fold_rank_loads": (ctypes.c_int, [_VP, _I32, _VP, _I32, _VP, _VP, _VP]),

@@ -507,19 +507,22 @@ def row_cosine_mean(a: torch.Tensor, b: torch.Tensor,
 
 
 def topk_hits(topk_pred: torch.Tensor, topk_actual: torch.Tensor,
-              stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-    """fb_topk_hits: sum over tokens of the predicted and actual sets' intersection size (device int64)."""
+              stream: Optional[torch.cuda.Stream] = None,
+              with_rate: bool = False):
+    """fb_topk_hits: sum over tokens of the predicted and actual sets' intersection size (device
+    int64); with_rate=True also returns the device-computed hit rate hits / (T k) (float64)."""
     if topk_pred.shape != topk_actual.shape or topk_pred.dim() != 2:
         raise ValueError("top-k tables must both be T x k")
     for t in (topk_pred, topk_actual):
         if t.dtype != torch.int32 or not t.is_contiguous():
             raise ValueError("top-k tables must be contiguous int32")
     out = torch.empty(1, dtype=torch.int64, device=topk_pred.device)
+    rate = torch.empty(1, dtype=torch.float64, device=topk_pred.device) if with_rate else None
     with torch.cuda.device(topk_pred.device):
         L.check(L.lib().fb_topk_hits(_ptr(topk_pred), _ptr(topk_actual), topk_pred.shape[0],
-                                     topk_pred.shape[1], _ptr(out),
+                                     topk_pred.shape[1], _ptr(out), _ptr(rate),
                                      _stream_handle(topk_pred.device, stream)), "fb_topk_hits")
-    return out
+    return (out, rate) if with_rate else out
 
 
 def fold_rank_loads(counts: torch.Tensor, expert_to_rank: torch.Tensor, R: int,
@@ -565,10 +568,8 @@ def prediction_quality(pred: Prediction, actual: Prediction, hidden_prev: Option
     carry topk (and logits for the logit cosine)."""
     if pred.topk is None or actual.topk is None:
         raise ValueError("both passes need return_topk=True")
-    hits = topk_hits(pred.topk, actual.topk)
+    hits, rate = topk_hits(pred.topk, actual.topk, with_rate=True)
     lc = row_cosine_mean(pred.logits, actual.logits) if pred.logits is not None and actual.logits is not None else None
     hc = row_cosine_mean(hidden_prev, hidden_target) if hidden_prev is not None and hidden_target is not None else None
-    T, k = pred.topk.shape
-    h = int(hits.item())
-    return Quality(h, h / float(T * k) if T else 1.0, None if lc is None else float(lc.item()),
+    return Quality(int(hits.item()), float(rate.item()), None if lc is None else float(lc.item()),
                    None if hc is None else float(hc.item()))

@@ -387,13 +387,13 @@ int fb_plan_swaps_timed_device(const int32_t* counts, int32_t E, const int32_t* 
 size_t fb_cosine_workspace_bytes(void) { return fb::cosine_workspace_bytes(); }
 
 int fb_topk_hits(const int32_t* topk_pred, const int32_t* topk_actual, int64_t T, int32_t k,
-                 int64_t* hits, void* stream) {
+                 int64_t* hits, double* hit_rate, void* stream) {
   if (!hits || T < 0 || k < 1) return FB_EINVAL;
   if (T > 0 && (!topk_pred || !topk_actual)) return FB_EINVAL;
   if (k > FB_MAX_TOPK) return FB_EUNSUPPORTED;
   const int dc = fb::check_device();
   if (dc != FB_OK) return dc;
-  return fb::launch_hits(topk_pred, topk_actual, T, k, hits, stream);
+  return fb::launch_hits(topk_pred, topk_actual, T, k, hits, hit_rate, stream);
 }
 
 int fb_row_cosine_mean(const void* a, const void* b, int64_t rows, int32_t cols, int64_t ld_a,

@@ -87,7 +87,8 @@ int launch_plan_device(const PlanDeviceLaunch& a);
 // Prediction-quality diagnostics (fb_quality.hip).
 constexpr int kCosineBlocks = 1024;           // grid of the row-cosine kernel (4 waves each)
 size_t cosine_workspace_bytes();
-int launch_hits(const int32_t* pred, const int32_t* act, int64_t T, int32_t k, int64_t* hits, void* stream);
+int launch_hits(const int32_t* pred, const int32_t* act, int64_t T, int32_t k, int64_t* hits,
+                double* rate, void* stream);
 int launch_cosine(const void* a, const void* b, int64_t rows, int32_t cols, int64_t lda, int64_t ldb,
                   int32_t dtype, double* out, void* workspace, void* stream);
 int launch_fold(const int32_t* counts, int32_t E, const int32_t* e2r, int32_t R, int32_t* rank_loads,

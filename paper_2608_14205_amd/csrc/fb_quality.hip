@@ -64,6 +64,11 @@ __global__ __launch_bounds__(kQThreads) void hits_kernel(const int32_t* __restri
 
 __global__ void zero_u64_kernel(unsigned long long* p) { *p = 0ull; }
 
+// hit rate = hits / (T * k), 1.0 for an empty batch
+__global__ void rate_kernel(const unsigned long long* hits, int64_t slots, double* rate) {
+  *rate = slots > 0 ? (double)*hits / (double)slots : 1.0;
+}
+
 // One wave per row at a time; 16-byte loads; products and sums in double.  Each wave writes the sum
 // of the cosines of the rows it handled to partial[wave id].
 template <bool BF16>
@@ -165,7 +170,8 @@ __global__ __launch_bounds__(kQThreads) void fold_kernel(const int32_t* __restri
 
 size_t cosine_workspace_bytes() { return (size_t)kCosineBlocks * kQWaves * sizeof(double); }
 
-int launch_hits(const int32_t* pred, const int32_t* act, int64_t T, int32_t k, int64_t* hits, void* stream) {
+int launch_hits(const int32_t* pred, const int32_t* act, int64_t T, int32_t k, int64_t* hits,
+                double* rate, void* stream) {
   (void)hipGetLastError();
   hipStream_t st = static_cast<hipStream_t>(stream);
   auto* h = reinterpret_cast<unsigned long long*>(hits);
@@ -174,6 +180,7 @@ int launch_hits(const int32_t* pred, const int32_t* act, int64_t T, int32_t k, i
     const int64_t blocks = (T + kQThreads - 1) / kQThreads;
     hipLaunchKernelGGL(hits_kernel, dim3((unsigned)blocks), dim3(kQThreads), 0, st, pred, act, T, k, h);
   }
+  if (rate) hipLaunchKernelGGL(rate_kernel, dim3(1), dim3(1), 0, st, h, T * (int64_t)k, rate);
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
 }
 

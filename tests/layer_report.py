@@ -94,7 +94,7 @@ def main():
                               torch.empty_like(p_out.max_mean))
         pred.predict_load(h, wp, scoring, e2r_d, wl.R, select_bias=sb, out=a_out, return_topk=True,
                           return_logits=True)
-        hits = fb.topk_hits(p_out.topk, a_out.topk)
+        hits, hit_rate = fb.topk_hits(p_out.topk, a_out.topk, with_rate=True)
         hcos = fb.row_cosine_mean(x, h)
         lcos = fb.row_cosine_mean(p_out.logits, a_out.logits)
         torch.cuda.synchronize()
@@ -124,7 +124,7 @@ def main():
                           "differing_on_gpu_logits": st["mismatch_on_gpu_logits"],
                           "eval_exempt": st["eval_exempt"], "counts_l1": l1,
                           "max_rel_logit_err": st["max_rel_err"]},
-               "quality": {"hit_rate": int(hits.item()) / float(wl.T * wl.k),
+               "quality": {"hit_rate": float(hit_rate.item()), "hits": int(hits.item()),
                            "hidden_cosine": float(hcos.item()), "logit_cosine": float(lcos.item())},
                "plans": []}
         counts_d = torch.from_numpy(counts.astype(np.int32)).to(dev)

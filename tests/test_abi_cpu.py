@@ -55,7 +55,7 @@ def test_struct_layouts_match_header():
 
 def test_version_and_status_strings():
     lib = fb.lib()
-    assert lib.fb_abi_version() == 3
+    assert lib.fb_abi_version() == 4
     for code in (0, -1, -2, -3, -4):
         assert L.status_string(code).startswith("FB_")
     assert "unknown" in L.status_string(7)
@@ -393,11 +393,11 @@ def test_unpacked_predict_needs_room_for_the_packed_weight():
 def test_diagnostics_validation_without_gpu():
     lib = fb.lib()
     h = 0x5000
-    assert lib.fb_topk_hits(0x1000, 0x2000, -1, 8, h, None) == L.FB_EINVAL
-    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 0, h, None) == L.FB_EINVAL
-    assert lib.fb_topk_hits(None, 0x2000, 4, 8, h, None) == L.FB_EINVAL
-    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 8, None, None) == L.FB_EINVAL
-    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 33, h, None) == L.FB_EUNSUPPORTED
+    assert lib.fb_topk_hits(0x1000, 0x2000, -1, 8, h, None, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 0, h, None, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(None, 0x2000, 4, 8, h, None, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 8, None, None, None) == L.FB_EINVAL
+    assert lib.fb_topk_hits(0x1000, 0x2000, 4, 33, h, None, None) == L.FB_EUNSUPPORTED
     ws = lib.fb_cosine_workspace_bytes()
     assert ws >= 8
     def cos(**o):

@@ -78,13 +78,17 @@ def test_identical_passes_are_perfect():
 def test_hits_edge_cases():
     _say("[quality] hit edge cases")
     empty = torch.empty((0, 4), dtype=torch.int32, device="cuda")
-    assert int(fb.topk_hits(empty, empty).item()) == 0
+    h0, r0 = fb.topk_hits(empty, empty, with_rate=True)
+    assert int(h0.item()) == 0 and float(r0.item()) == 1.0
     g = np.random.default_rng(7)
     T, k = 777, 32
     tp = np.stack([g.permutation(256)[:k] for _ in range(T)]).astype(np.int32)
     ta = np.stack([g.permutation(256)[:k] for _ in range(T)]).astype(np.int32)
-    got = int(fb.topk_hits(torch.from_numpy(tp).cuda(), torch.from_numpy(ta).cuda()).item())
-    assert got == sum(len(set(r.tolist()) & set(s.tolist())) for r, s in zip(tp, ta))
+    hits, rate = fb.topk_hits(torch.from_numpy(tp).cuda(), torch.from_numpy(ta).cuda(), with_rate=True)
+    ref = sum(len(set(r.tolist()) & set(s.tolist())) for r, s in zip(tp, ta))
+    assert int(hits.item()) == ref
+    # the oracle's hit rate on the same lists (Sec. "Metrics")
+    assert float(rate.item()) == OP.hit_rate(tp, ta)
 
 
 @pytest.mark.parametrize("rows,cols,dtype", [(1, 8, "bf16"), (3, 4, "f32"), (5000, 7168, "bf16"),
