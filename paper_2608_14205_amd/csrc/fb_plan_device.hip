@@ -45,6 +45,12 @@ constexpr int kSmallItemBits = 13;            // ... < E + R * S <= 8192 without
 constexpr int64_t kLoadCap = (int64_t)1 << 43;  // loads <= 4096 experts * (2^31 - 1) < 2^43
 constexpr int kMaxSurvivors = 8192;           // full mode: work units listed per round (more are
                                               // evaluated where their bound test ran)
+// Tables of at most kSmallRS slots and kSmallR ranks run in a workgroup that holds a fraction of the
+// LDS (about 24 KB in frontier mode, 57 KB in full mode, against 153 KB for the largest tables), so
+// that it can start on a CU beside another kernel's workgroups, for instance attention's while the
+// plan is made on a side stream, instead of waiting for a whole CU to drain.
+constexpr int kSmallRS = 512;
+constexpr int kSmallR = 64;
 
 template <int CTRL>
 __device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
@@ -89,28 +95,32 @@ __device__ __forceinline__ uint64_t tie_key(int a, int b, int i, int j) {
          ((uint64_t)i << kItemBits) | (uint64_t)j;
 }
 
-struct Shared {
-  int32_t item[kMaxRS];          // slot -> item id (slot value, or V + slot for an empty slot)
-  int32_t sload[kMaxRS];         // slot -> load (token share) of its item
-  uint8_t mslot[kMaxRS];         // slot -> its item has moved
+// LDS of plan_general for tables of at most CRS slots and CR ranks; SURV work units listed per
+// full-mode round.  E <= R * S <= CRS, so the per-expert arrays fit the slot capacity.
+template <int CRS, int CR, int SURV>
+struct SharedT {
+  static constexpr int kSurv = SURV;
+  int32_t item[CRS];             // slot -> item id (slot value, or V + slot for an empty slot)
+  int32_t sload[CRS];            // slot -> load (token share) of its item
+  uint8_t mslot[CRS];            // slot -> its item has moved
   union {
     struct {                     // placement check
-      int32_t cnt[kMaxRS], ej[kMaxRS], reps[kMaxRS], base[kMaxRS], flag[kMaxRS];
+      int32_t cnt[CRS], ej[CRS], reps[CRS], base[CRS], flag[CRS];
     } chk;
     struct {                     // after the check
-      int64_t ebytes[kMaxRS];    // expert sizes (time budget)
+      int64_t ebytes[CRS];       // expert sizes (time budget)
       // frontier rounds with replicas: slot p of amax (row) or q of amin (column) holds a replica
       // of an expert that the other rank also holds
-      uint8_t mrow[kMaxRS], mcol[kMaxRS];
+      uint8_t mrow[CRS], mcol[CRS];
       // full mode: the smallest and largest load among each rank's items that have not moved
       // (smin > smax when every item has moved), and the work units left after the bound test
-      int32_t smin[kMaxR], smax[kMaxR];
-      int32_t surv[kMaxSurvivors];
+      int32_t smin[CR], smax[CR];
+      int32_t surv[SURV];
     } run;
   } u;
   int32_t wsum[16];
-  int64_t L[kMaxR];
-  int32_t part[kMaxR];
+  int64_t L[CR];
+  int32_t part[CR];
   uint64_t wgain[16], wtie[16], wcost[16];
   uint64_t rgain[16], rtie[16], rcost[16];   // full mode: per-wave bests of the first phase
   int64_t cmin[2];               // time budget: the lowest cost of any swap on link type 0 / 1
@@ -120,8 +130,8 @@ struct Shared {
   int64_t other;
   // time budget: what is left of every rank's budget, rank nodes, and the accepted swaps' links
   // and costs (the link budgets are charged by scanning them)
-  int64_t rank_left[kMaxR];
-  int32_t node[kMaxR];
+  int64_t rank_left[CR];
+  int32_t node[CR];
   int32_t acc_pair[kMaxTimedSwaps];   // a * kMaxR + b, a < b
   int64_t acc_cost[kMaxTimedSwaps];
 };
@@ -252,7 +262,8 @@ __device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t beta, double in
 
 // Eq. 9 in whole nanoseconds for a swap moving expert ei off rank ra and expert ej off rank rb
 // (-1: an empty slot, which transfers nothing).
-__device__ __forceinline__ int64_t swap_cost(const PlanDeviceLaunch& a, const Shared& sh, int ra,
+template <class SH>
+__device__ __forceinline__ int64_t swap_cost(const PlanDeviceLaunch& a, const SH& sh, int ra,
                                              int rb, int ei, int ej) {
   const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
   const int64_t bytes = (ei >= 0 ? sh.u.run.ebytes[ei] : 0) + (ej >= 0 ? sh.u.run.ebytes[ej] : 0);
@@ -261,7 +272,8 @@ __device__ __forceinline__ int64_t swap_cost(const PlanDeviceLaunch& a, const Sh
 }
 
 // Does a swap of cost c between ranks ra and rb fit the remaining rank and link budgets?
-__device__ __forceinline__ bool swap_fits(const PlanDeviceLaunch& a, const Shared& sh, int ra,
+template <class SH>
+__device__ __forceinline__ bool swap_fits(const PlanDeviceLaunch& a, const SH& sh, int ra,
                                           int rb, int64_t c) {
   if (c > sh.rank_left[ra] || c > sh.rank_left[rb]) return false;
   // every swap on a link also charges both of its ranks, so a link budget at least the rank
@@ -289,9 +301,15 @@ __device__ __forceinline__ bool ratio_better(uint64_t g1, uint64_t c1, uint64_t 
   return t1 < t2;
 }
 
-template <int NT>
+// NT threads (256: frontier mode, 1024: full mode); SMALL: tables of at most kSmallRS slots and
+// kSmallR ranks
+template <int NT, bool SMALL>
 __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
-  __shared__ Shared sh;
+  constexpr int CRS = SMALL ? kSmallRS : kMaxRS;
+  constexpr int CR = SMALL ? kSmallR : kMaxR;
+  // the survivor list serves full mode only
+  __shared__ SharedT<CRS, CR, NT == 1024 ? kMaxSurvivors : 64> sh;
+  constexpr int kSurv = decltype(sh)::kSurv;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -306,7 +324,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   // space is free
   for (int c = tid; c < RS; c += NT) sh.item[c] = a.slot_expert[c];
   for (int e = tid; e < E; e += NT) { sh.u.chk.cnt[e] = a.counts[e]; sh.u.chk.reps[e] = 0; }
-  constexpr int kEB = (kMaxRS + NT - 1) / NT;
+  constexpr int kEB = (CRS + NT - 1) / NT;
   int64_t eb[kEB];
 #pragma unroll
   for (int u = 0; u < kEB; ++u) {
@@ -694,7 +712,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
           if ((unsigned __int128)ub * ref_c < (unsigned __int128)ref_g * (uint64_t)cmin) continue;
         }
         const int at = atomicAdd(&sh.nsurv, S);
-        if (at + S <= kMaxSurvivors) {
+        if (at + S <= kSurv) {
           for (int p = 0; p < S; ++p) sh.u.run.surv[at + p] = pair * S + p;
         } else {
           for (int p = 0; p < S; ++p) unit(ra, rb, p, true);
@@ -703,7 +721,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       __syncthreads();
       // (a pair whose units did not fit was scored where it was tested; the list holds whole
       // pairs, so its length is the largest multiple of S not beyond the capacity)
-      const int ns2 = sh.nsurv <= kMaxSurvivors ? sh.nsurv : (kMaxSurvivors / S) * S;
+      const int ns2 = sh.nsurv <= kSurv ? sh.nsurv : (kSurv / S) * S;
       const int qp2 = ns2 == 0 ? 1 : NT / ns2 < 1 ? 1 : NT / ns2 > S ? S : NT / ns2;
       for (int w = tid; w < ns2 * qp2; w += NT) {
         const int k = w / qp2;
@@ -921,14 +939,22 @@ __device__ __forceinline__ int rounds_small(const PlanDeviceLaunch& a, uint2* sl
   return ns;
 }
 
+// Slot capacity of the one-wave planner: R <= 64 * RPL ranks of S <= 8 (CPL 1) or S <= 11 (CPL 2)
+// slots, so its LDS follows the launch shape (16.6 KB for 64 ranks of 8 slots) and the workgroup can
+// start beside other kernels' workgroups on a CU.
+constexpr int wave_cap(int RPL, int CPL) {
+  return 64 * RPL * (CPL == 1 ? 8 : 11) < kMaxRS ? 64 * RPL * (CPL == 1 ? 8 : 11) : kMaxRS;
+}
+
 // RPL: ranks per lane (R <= 64 * RPL); rank r lives in lane r % 64, register r / 64.
 // CPL: candidates per lane, 1 for S * S <= 64, 2 for S * S <= 128.
 template <int RPL, int CPL>
 __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) {
-  __shared__ int32_t vals[kMaxRS], cnt[kMaxRS], ej[kMaxRS];     // the input tables
-  __shared__ int32_t reps[kMaxRS], base[kMaxRS], flag[kMaxRS];   // placement check
-  __shared__ uint2 slot[kMaxRS];     // x: item id | moved flag, y: the item's load (token share)
-  __shared__ int32_t part[kMaxR];
+  constexpr int CAP = wave_cap(RPL, CPL);   // >= R * S >= E
+  __shared__ int32_t vals[CAP], cnt[CAP], ej[CAP];     // the input tables
+  __shared__ int32_t reps[CAP], base[CAP], flag[CAP];   // placement check
+  __shared__ uint2 slot[CAP];        // x: item id | moved flag, y: the item's load (token share)
+  __shared__ int32_t part[64 * RPL];
   __shared__ int32_t s_bad, s_J;
   const int lane = threadIdx.x;
   const int E = a.E, R = a.R, S = a.S, RS = R * S;
@@ -1140,6 +1166,9 @@ int launch_plan_device(const PlanDeviceLaunch& a) {
   (void)hipGetLastError();
   hipStream_t st = static_cast<hipStream_t>(a.stream);
   if (!a.timed && a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 128) {
+    // the routing below keeps R * S within the chosen kernel's slot capacity
+    const int rpl = a.R <= 64 ? 1 : a.R <= 128 ? 2 : a.R <= 256 ? 4 : 16;
+    if ((int64_t)a.R * a.S > wave_cap(rpl, (int64_t)a.S * a.S <= 64 ? 1 : 2)) return FB_EUNSUPPORTED;
     if ((int64_t)a.S * a.S <= 64) {
       if (a.R <= 64) hipLaunchKernelGGL((plan_frontier_wave<1, 1>), dim3(1), dim3(64), 0, st, a);
       else if (a.R <= 128) hipLaunchKernelGGL((plan_frontier_wave<2, 1>), dim3(1), dim3(64), 0, st, a);
@@ -1152,10 +1181,16 @@ int launch_plan_device(const PlanDeviceLaunch& a) {
       else hipLaunchKernelGGL((plan_frontier_wave<16, 2>), dim3(1), dim3(64), 0, st, a);
     }
   }
-  else if (a.budget.mode == FB_FRONTIER)
-    hipLaunchKernelGGL(plan_general<256>, dim3(1), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL(plan_general<1024>, dim3(1), dim3(1024), 0, st, a);
+  else {
+    const bool small = (int64_t)a.R * a.S <= kSmallRS && a.R <= kSmallR;
+    if (a.budget.mode == FB_FRONTIER) {
+      if (small) hipLaunchKernelGGL((plan_general<256, true>), dim3(1), dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((plan_general<256, false>), dim3(1), dim3(256), 0, st, a);
+    } else {
+      if (small) hipLaunchKernelGGL((plan_general<1024, true>), dim3(1), dim3(1024), 0, st, a);
+      else hipLaunchKernelGGL((plan_general<1024, false>), dim3(1), dim3(1024), 0, st, a);
+    }
+  }
   return hipGetLastError() == hipSuccess ? FB_OK : FB_EDEVICE;
 }
 
