@@ -40,7 +40,11 @@ size_t split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype, int
 // launch leaves both at zero.
 constexpr size_t kWsAccOffset = 0;
 constexpr size_t kWsTicketOffset = 1024;
+// split mode: one arrival counter per tile, so the tile's last split finishes it
+constexpr size_t kWsTileTicketOffset = 1088;
+constexpr int kMaxSplitTiles = 128;
 constexpr size_t kWsBytes = 2048;
+static_assert(kWsTileTicketOffset + 4 * kMaxSplitTiles <= kWsBytes, "tile tickets fit the header");
 
 // Scratch of fb_predict_load_packed_noalloc: a workspace header, then room for the split mode's
 // partial logits of the largest batch that runs split on 256 CUs (at most 128 tiles, 4 splits, 64

@@ -92,6 +92,7 @@ struct Params {
   double* max_mean;
   int32_t* ws_acc;
   uint32_t* ws_ticket;
+  uint32_t* ws_tile;   // split mode: arrivals per tile (kSplit)
   int32_t* topk_idx;
   float* logits;
   uint32_t nblocks;
@@ -470,10 +471,10 @@ __device__ __forceinline__ void contract(f32x16 (&acc)[FE][FT], const Params& p,
 }
 
 // BM_: tokens per workgroup (the configuration's own, or half of it when that fills the chip better)
-// MODE: kFused contracts the whole row and finishes the tile; kPartial (split mode, grid tiles x
-// ks) contracts one of ks stage ranges and stores its partial logits; kFinish (split mode, grid
-// tiles) sums a tile's partial logits in split order and finishes the tile.
-constexpr int kFused = 0, kPartial = 1, kFinish = 2;
+// MODE: kFused contracts the whole row and finishes the tile; kSplit (split mode, grid tiles x ks)
+// contracts one of ks stage ranges and stores its partial logits, and the tile's last split to
+// arrive sums the tile's partials in split order and finishes the tile.
+constexpr int kFused = 0, kSplit = 1;
 template <bool BF16, int EPAD, int BM_, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   using Cfg = TileCfg<EPAD>;
@@ -516,7 +517,7 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int we = wave % WE;
   const int wt = wave / WE;
-  const int tile = MODE == kPartial ? (int)(blockIdx.x / (uint32_t)p.ks) : (int)blockIdx.x;
+  const int tile = MODE == kSplit ? (int)(blockIdx.x / (uint32_t)p.ks) : (int)blockIdx.x;
   const int64_t row0 = (int64_t)tile * BM;
   const int E = p.E;
   constexpr int NACC = FE * FT * 16;               // accumulator registers per thread
@@ -536,21 +537,9 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  if constexpr (MODE == kFinish) {
-    // the tile's logits: its partial sums added in split order (the same order on every run)
-    const float* src = p.partial + (size_t)tile * p.ks * NACC * kThreads + tid;
-    for (int ks = 0; ks < p.ks; ++ks) {
-#pragma unroll
-      for (int a = 0; a < FE; ++a)
-#pragma unroll
-        for (int b = 0; b < FT; ++b)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            acc[a][b][r] += src[((size_t)ks * NACC + (a * FT + b) * 16 + r) * kThreads];
-    }
-  } else {
+  {
     Params q = p;
-    if constexpr (MODE == kPartial) {
+    if constexpr (MODE == kSplit) {
       const int ks = (int)(blockIdx.x % (uint32_t)p.ks);
       const int chunk = (p.st_total + p.ks - 1) / p.ks;
       q.st_base = ks * chunk;
@@ -558,15 +547,43 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     }
     if (row0 < p.T && q.nstages > 0)
       contract<BF16, EPAD, FE, FT, NS, BM, TW>(acc, q, row0, wave, we, wt, lane, smem);
-    if constexpr (MODE == kPartial) {
+    if constexpr (MODE == kSplit) {
+      // The partial goes out with device-scope stores, which are visible to every XCD once
+      // performed; each thread waits for its own, and the barrier orders them all before the
+      // arrival count.  The last split to arrive reads the partials back with device-scope loads
+      // (so not from a stale line of its own L2) and adds them in split order.
       float* dst = p.partial + ((size_t)blockIdx.x * NACC) * kThreads + tid;
 #pragma unroll
       for (int a = 0; a < FE; ++a)
 #pragma unroll
         for (int b = 0; b < FT; ++b)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) dst[(size_t)((a * FT + b) * 16 + r) * kThreads] = acc[a][b][r];
-      return;
+          for (int r = 0; r < 16; ++r)
+            __hip_atomic_store(&dst[(size_t)((a * FT + b) * 16 + r) * kThreads], acc[a][b][r],
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
+      __syncthreads();
+      if (tid == 0) s_flag = atomicAdd(&p.ws_tile[tile], 1u) == (uint32_t)(p.ks - 1) ? 1 : 0;
+      __syncthreads();
+      if (s_flag != 1) return;
+      if (tid == 0) atomicExch(&p.ws_tile[tile], 0u);   // left zeroed for the next call
+      const float* src = p.partial + (size_t)tile * p.ks * NACC * kThreads + tid;
+#pragma unroll
+      for (int a = 0; a < FE; ++a)
+#pragma unroll
+        for (int b = 0; b < FT; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+      for (int ks = 0; ks < p.ks; ++ks) {
+#pragma unroll
+        for (int a = 0; a < FE; ++a)
+#pragma unroll
+          for (int b = 0; b < FT; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              acc[a][b][r] += __hip_atomic_load(&src[((size_t)ks * NACC + (a * FT + b) * 16 + r) * kThreads],
+                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
   lds_barrier();
@@ -1057,7 +1074,8 @@ int epad_of(int32_t E) {
 // hidden rows and each streams a share of the router weight.
 int split_count(int64_t T, int BM, int st_total, int num_cus) {
   const int64_t tiles = (T + BM - 1) / BM;
-  if (T <= 0 || tiles * 2 > num_cus) return 1;
+  // split mode: at most half of the CUs hold tiles, and each tile has an arrival counter
+  if (T <= 0 || tiles * 2 > num_cus || tiles > kMaxSplitTiles) return 1;
   int64_t ks = num_cus / tiles;
   if (ks > 4) ks = 4;
   if (ks > st_total / 4) ks = st_total / 4;
@@ -1120,6 +1138,7 @@ int launch_cfg_bm(const PredictLaunch& a) {
   p.max_mean = a.max_mean;
   p.ws_acc = reinterpret_cast<int32_t*>(static_cast<char*>(a.workspace) + kWsAccOffset);
   p.ws_ticket = reinterpret_cast<uint32_t*>(static_cast<char*>(a.workspace) + kWsTicketOffset);
+  p.ws_tile = reinterpret_cast<uint32_t*>(static_cast<char*>(a.workspace) + kWsTileTicketOffset);
   p.topk_idx = a.topk_idx;
   p.logits = a.logits;
   const int64_t tiles = (a.T + BM - 1) / BM;
@@ -1132,10 +1151,8 @@ int launch_cfg_bm(const PredictLaunch& a) {
   hipStream_t st = static_cast<hipStream_t>(a.stream);
   if (p.ks > 1 && a.partial != nullptr &&
       a.partial_bytes >= (size_t)tiles * p.ks * BM * EPAD * sizeof(float)) {
-    hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM, kPartial>), dim3(p.nblocks * p.ks),
+    hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM, kSplit>), dim3(p.nblocks * p.ks),
                        dim3(kThreads), 0, st, p);
-    hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM, kFinish>), dim3(p.nblocks), dim3(kThreads),
-                       0, st, p);
   } else {
     p.ks = 1;
     hipLaunchKernelGGL((predict_kernel<BF16, EPAD, BM, kFused>), dim3(p.nblocks), dim3(kThreads),
