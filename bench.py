@@ -255,6 +255,74 @@ def _time_ms(torch, stream, fn, K):
     return a.elapsed_time(b) / K
 
 
+def _smi_sample():
+    """Socket power (amd-smi) and shader clock (rocm-smi) of GPU 0; read-only queries."""
+    import subprocess
+    out = {}
+    try:
+        r = subprocess.run(["amd-smi", "metric", "--power", "--json"], capture_output=True,
+                           text=True, timeout=20)
+        out["socket_power_w"] = json.loads(r.stdout)["gpu_data"][0]["power"]["socket_power"]["value"]
+    except Exception:
+        pass
+    try:
+        r = subprocess.run(["rocm-smi", "-c", "--json"], capture_output=True, text=True, timeout=20)
+        card = next(iter(json.loads(r.stdout).values()))
+        out["sclk_mhz"] = int(card["sclk clock speed:"].strip("()Mhz"))
+    except Exception:
+        pass
+    return out
+
+
+def measure_power(torch, xs, nbuf, run_pred, wt, stream, seconds):
+    """Board power and shader clock while the predictor runs back to back on the benchmark's hidden
+    states, on all-zero hidden states of the same shape, and while hipBLASLt runs the plain router
+    GEMM on the benchmark's hidden states: evidence for what bounds the kernel (the chip's power
+    limit versus its own design).  Each phase runs for `seconds`; sampling starts after one second."""
+    import statistics
+    import threading
+    zeros = [torch.zeros_like(xs[0]) for _ in range(2)]
+    phases = [("predictor", lambda i: run_pred(xs[i % nbuf])),
+              ("predictor_all_zero_hidden", lambda i: run_pred(zeros[i % 2])),
+              ("hipblaslt_router_gemm", lambda i: torch.matmul(xs[i % nbuf], wt))]
+    res = {"idle": _smi_sample()}
+    for name, fn in phases:
+        stop = threading.Event()
+        samples = []
+
+        def poll():
+            time.sleep(1.0)
+            while not stop.is_set():
+                samples.append(_smi_sample())
+
+        th = threading.Thread(target=poll)
+        th.start()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        n = n0 = 0
+        started = False
+        while time.perf_counter() - t0 < seconds:
+            if not started and time.perf_counter() - t0 > 1.0:
+                a.record(stream)
+                n0, started = n, True
+            for i in range(20):
+                fn(n + i)
+            n += 20
+            torch.cuda.synchronize()
+        b.record(stream)
+        torch.cuda.synchronize()
+        stop.set()
+        th.join()
+        pw = [x["socket_power_w"] for x in samples if "socket_power_w" in x]
+        ck = [x["sclk_mhz"] for x in samples if "sclk_mhz" in x]
+        res[name] = {"us_per_launch": a.elapsed_time(b) / max(1, n - n0) * 1e3,
+                     "socket_power_w_median": statistics.median(pw) if pw else None,
+                     "sclk_mhz_median": statistics.median(ck) if ck else None,
+                     "samples": len(samples)}
+    return res
+
+
 def measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t, slots_t, sb, pred,
                    out, stream):
     """The rest of the hot path's entry points on the same workload, each timed back to back:
@@ -330,6 +398,10 @@ def main():
                     help="independent batches in flight during the timed steps (1 = one stream)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    # instead of the bench line: board power and shader clock while the predictor runs on the
+    # benchmark's hidden states and on all-zero ones, and while hipBLASLt runs the router GEMM
+    ap.add_argument("--power", action="store_true")
+    ap.add_argument("--power-seconds", type=float, default=5.0)
     # The bench line is the DeepSeek-V3-shaped batch.  The other input shapes can be timed the same
     # way for context (same step, roofline fields without counter traffic, no extras or CPU leg).
     ap.add_argument("--workload", default="deepseek-v3",
@@ -376,6 +448,16 @@ def main():
     def step(i, router):
         pred.predict_load(xs[i % nbuf], router, scoring, e2r_t, wl.R, select_bias=sb, out=out)
         fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
+
+    if args.power:
+        res = measure_power(torch, xs, nbuf,
+                            lambda x: pred.predict_load(x, wp, scoring, e2r_t, wl.R, select_bias=sb,
+                                                        out=out),
+                            w.t(), stream, args.power_seconds)
+        print(json.dumps({"power_probe": res, "workload": args.workload,
+                          "what": "amd-smi socket power and rocm-smi shader clock, medians of the "
+                                  "samples taken while each load ran back to back"}))
+        return
 
     # The timed steps keep `streams` independent batches in flight: step i runs on stream
     # i mod streams with that stream's own workspace, outputs and plan, so one batch's planning and
