@@ -291,8 +291,10 @@ def test_pack_layout_and_packed_predict(E, H, dtype):
                                     ("dsv3", 300), ("dsv3", 1100)])
 def test_split_mode_parity(name, T):
     """Packed batches too small to occupy the GPU run in split mode (partial logits of stage ranges
-    on several workgroups, added in split order by a second kernel): oracle parity, repeats that
-    are bit-identical, and the fused path's selections where both match the oracle on every token."""
+    on several workgroups, added in split order by the tile's last split to arrive): oracle parity,
+    repeats that are bit-identical, the workspace header (accumulators, ticket and the per-tile
+    arrival counters) left at zero, and the fused path's selections where both match the oracle on
+    every token."""
     wl, e2r = _case(name, T)
     dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     need = fb.predict_split_workspace_bytes(T, wl.E, wl.H, dt)
@@ -308,6 +310,7 @@ def test_split_mode_parity(name, T):
     for key in ("counts", "rank_loads", "topk"):
         assert np.array_equal(a[key], b[key]), key
     assert np.array_equal(a["logits"].view(np.uint32), b["logits"].view(np.uint32))
+    assert not pred.workspace[:2048].cpu().numpy().any()
     fused = run_gpu(li, wl, e2r, predictor=fb.Predictor(split=False), packed=True)
     fstats = check_prediction(fused, li, wl, e2r, label=f"fused {name}/T={T}")
     if stats["mismatch"] == 0 and fstats["mismatch"] == 0:
