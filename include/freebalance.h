@@ -149,9 +149,10 @@ const char* fb_status_string(int status);
  * multiple of 256 bytes.  0 if E, H or dtype is invalid or E > FB_MAX_EXPERTS. */
 size_t fb_router_packed_bytes(int32_t E, int32_t H, int32_t dtype);
 
-/* Bytes of device workspace fb_predict_load needs: 2048 bytes of accumulators plus room for the
- * router weight it packs on every call (fb_router_packed_bytes).  fb_predict_load_packed needs only
- * the first 2048 bytes.  0 for invalid arguments as in fb_router_packed_bytes. */
+/* Bytes of device workspace fb_predict_load needs: 2048 bytes of accumulators and completion
+ * counters plus room for the router weight it packs on every call (fb_router_packed_bytes).
+ * fb_predict_load_packed needs only the first 2048 bytes.  0 for invalid arguments as in
+ * fb_router_packed_bytes. */
 size_t fb_predict_workspace_bytes(int32_t E, int32_t H, int32_t dtype);
 
 /* Prepare a predictor workspace: zero-fills its first 2048 bytes with a kernel on `stream` (no
@@ -222,8 +223,9 @@ int fb_predict_load(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
  *                        too small to occupy the GPU runs in split mode: the hidden dimension of
  *                        every tile is split over several workgroups whose partial logits (kept
  *                        in the workspace past its first 2048 bytes) are added in a fixed order
- *                        by a second kernel.  Results are then deterministic and within the
- *                        float32 summation-order tolerance of the fused path's.
+ *                        by the tile's last workgroup to arrive, still in one launch.  Results
+ *                        are then deterministic and within the float32 summation-order
+ *                        tolerance of the fused path's.
  * Every other argument, and every error, as in fb_predict_load. */
 int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
                            int32_t dtype, const void* router_packed, size_t router_packed_bytes,
@@ -236,7 +238,7 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
 /* fb_predict_load_packed for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument, no allocation.  The
  * library keeps a fixed scratch array in device memory instead, FB_NOALLOC_SCRATCH_BYTES per device
- * (2048 bytes of accumulators and completion ticket, then 32 MiB for split-mode partial logits),
+ * (2048 bytes of accumulators and completion counters, then 32 MiB for split-mode partial logits),
  * held by every device the call runs on until the process ends.  The first call on a device looks
  * up that device's copy and zeroes its header with a fill kernel on `stream`; every completed call
  * leaves the header zeroed again.  All calls on one device share the array: calls that overlap
