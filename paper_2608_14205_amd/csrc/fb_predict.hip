@@ -551,7 +551,9 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
       // The partial goes out with device-scope stores, which are visible to every XCD once
       // performed; each thread waits for its own, and the barrier orders them all before the
       // arrival count.  The last split to arrive reads the partials back with device-scope loads
-      // (so not from a stale line of its own L2) and adds them in split order.
+      // (so not from a stale line of its own L2) and adds them in split order.  The loads of one
+      // 16-register block go out before any of them is used, so that a tile with many registers
+      // keeps them in flight together instead of waiting for each.
       float* dst = p.partial + ((size_t)blockIdx.x * NACC) * kThreads + tid;
 #pragma unroll
       for (int a = 0; a < FE; ++a)
@@ -578,11 +580,15 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
 #pragma unroll
         for (int a = 0; a < FE; ++a)
 #pragma unroll
-          for (int b = 0; b < FT; ++b)
+          for (int b = 0; b < FT; ++b) {
+            f32x16 t;
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-              acc[a][b][r] += __hip_atomic_load(&src[((size_t)ks * NACC + (a * FT + b) * 16 + r) * kThreads],
-                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              t[r] = __hip_atomic_load(&src[((size_t)ks * NACC + (a * FT + b) * 16 + r) * kThreads],
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[a][b][r] += t[r];
+          }
       }
     }
   }
