@@ -216,16 +216,25 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
         t = alone(attn)
         per_type[name] = {"t_attn_ms": t, "tflops": flops / (t * 1e-3) / 1e12, **spend(t)}
         del attn
-    # the overlap itself, on one sequence of the full stand-in
+    # the overlap itself, on one sequence of the full stand-in: each repetition times the attention
+    # alone and with the early pass enqueued after it and before it, in a rotating order, and keeps
+    # the differences to the run alone, which cancels the slow drift of the clocks between
+    # repetitions
     attn, _ = attention_standin(torch, dev, seqs=1)
     run_once(attn, True, True)
-    ta, tb, tc = [], [], []
-    for _ in range(7):
-        ta.append(run_once(attn, True, False))
-        tb.append(run_once(attn, True, True))
-        tc.append(run_once(attn, True, True, pp_first=True))
+    reps = 15
+    ta, d_after, d_first = [], [], []
+    for i in range(reps):
+        kinds = ["alone", "after", "first"]
+        kinds = kinds[i % 3:] + kinds[:i % 3]
+        t = {}
+        for k in kinds:
+            t[k] = run_once(attn, True, k != "alone", pp_first=(k == "first"))
+        ta.append(t["alone"])
+        d_after.append(t["after"] - t["alone"])
+        d_first.append(t["first"] - t["alone"])
     med = lambda v: sorted(v)[len(v) // 2]
-    t_attn1, t_after, t_before = med(ta), med(tb), med(tc)
+    quart = lambda v: [sorted(v)[len(v) // 4], sorted(v)[(3 * len(v)) // 4]]
     full = per_type["full"]
     return {"attention_standin": "4 sequences x 8192 tokens x 128 heads x 128 dims: S = QK^T and "
                                  "O = SV as bf16 batched GEMMs (hipBLASLt via torch.bmm), main stream; "
@@ -235,11 +244,15 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
             "B_l_rule": "max(0, T_attn - delta), delta = predict + plan time",
             "B_l_ns": full["B_l_ns"], "timed_plan_swaps": full["timed_plan_swaps"],
             "overlap_one_sequence": {
-                "t_attn_ms": t_attn1, "t_both_pass_after_ms": t_after, "t_both_pass_first_ms": t_before,
-                "hidden_fraction_pass_after": (t_attn1 + t_pp - t_after) / t_pp,
-                "hidden_fraction_pass_first": (t_attn1 + t_pp - t_before) / t_pp,
-                "what": "medians of 7 alternating runs; hidden fraction = (t_attn + t_pass - t_both) / t_pass"}}
-
+                "t_attn_ms": med(ta),
+                "added_ms_pass_after": med(d_after), "added_ms_pass_after_quartiles": quart(d_after),
+                "added_ms_pass_first": med(d_first), "added_ms_pass_first_quartiles": quart(d_first),
+                "hidden_fraction_pass_after": 1.0 - med(d_after) / t_pp,
+                "hidden_fraction_pass_first": 1.0 - med(d_first) / t_pp,
+                "what": f"{reps} repetitions, each timing the attention alone and with the early pass "
+                        "enqueued after and before it (rotating order); added = that repetition's "
+                        "difference to the attention alone, median and quartiles; hidden fraction = "
+                        "1 - added / t_predict_plan"}}
 
 def _time_ms(torch, stream, fn, K):
     """Average duration of K back-to-back calls of fn, bracketed by events on the stream."""
@@ -277,14 +290,18 @@ def _smi_sample():
 def measure_power(torch, xs, nbuf, run_pred, wt, stream, seconds):
     """Board power and shader clock while the predictor runs back to back on the benchmark's hidden
     states, on all-zero hidden states of the same shape, and while hipBLASLt runs the plain router
-    GEMM on the benchmark's hidden states: evidence for what bounds the kernel (the chip's power
-    limit versus its own design).  Each phase runs for `seconds`; sampling starts after one second."""
+    GEMM on the benchmark's hidden states and the one-sequence attention stand-in of the overlap
+    measurement: evidence for what bounds the kernel (the chip's power limit versus its own design)
+    and for how much of the early pass attention can hide.  Each phase runs for `seconds`; sampling
+    starts after one second."""
     import statistics
     import threading
     zeros = [torch.zeros_like(xs[0]) for _ in range(2)]
+    attn, _ = attention_standin(torch, xs[0].device, seqs=1)
     phases = [("predictor", lambda i: run_pred(xs[i % nbuf])),
               ("predictor_all_zero_hidden", lambda i: run_pred(zeros[i % 2])),
-              ("hipblaslt_router_gemm", lambda i: torch.matmul(xs[i % nbuf], wt))]
+              ("hipblaslt_router_gemm", lambda i: torch.matmul(xs[i % nbuf], wt)),
+              ("attention_standin_one_sequence", lambda i: attn(stream))]
     res = {"idle": _smi_sample()}
     for name, fn in phases:
         stop = threading.Event()
