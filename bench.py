@@ -1,8 +1,8 @@
 """Benchmark of the residual workload predictor + swap planner on one MI355X.
 
-A step is one pass of the whole hot path over one batch: the fused predictor kernel (router GEMM,
-scoring, top-k, histogram, rank fold, max/mean) followed by the device swap planner, back to back on
-one stream.  The workload is the DeepSeek-V3-shaped prefill batch: T=32768 tokens, H=7168, E=256
+A step is one pass of the whole hot path over one batch, one fb_predict_plan_packed call: the fused
+predictor kernel (router GEMM, scoring, top-k, histogram, rank fold, max/mean) whose last workgroup
+then makes the swap plan of the counts.  The workload is the DeepSeek-V3-shaped prefill batch: T=32768 tokens, H=7168, E=256
 routed experts, sigmoid scoring with a per-expert selection bias, group-limited top-8 (8 groups,
 4 kept, group score = sum of the top-2), 32 ranks x 8 slots, swap cap 8.  Inputs are seeded
 synthetic data resident in HBM before timing starts; hidden-state buffers rotate so every step reads
@@ -169,13 +169,18 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
     main = torch.cuda.current_stream(dev)
     side = torch.cuda.Stream(dev)
     pred = fb.Predictor(dev, stream=side)
-    out = pred.predict_load(x, wp, scoring, e2r_t, wl.R, select_bias=sb, stream=side)
-    plan = fb.plan_swaps_device(out.counts, slots_t, budget, stream=side)
+    out, plan = pred.predict_plan(x, wp, scoring, e2r_t, slots_t, budget, select_bias=sb,
+                                  stream=side)
     torch.cuda.synchronize()
+    lat = []                          # the early pass's own latency in the last run_once
 
     def early_pass():
-        pred.predict_load(x, wp, scoring, e2r_t, wl.R, select_bias=sb, out=out, stream=side)
-        fb.plan_swaps_device(out.counts, slots_t, budget, out=plan, stream=side)
+        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        p0.record(side)
+        pred.predict_plan(x, wp, scoring, e2r_t, slots_t, budget, select_bias=sb, out=out,
+                          plan=plan, stream=side)
+        p1.record(side)
+        lat[:] = [(p0, p1)]
 
     def run_once(attn, use_attn, use_pp, pp_first=False):
         st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -223,13 +228,15 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
     attn, _ = attention_standin(torch, dev, seqs=1)
     run_once(attn, True, True)
     reps = 15
-    ta, d_after, d_first = [], [], []
+    ta, d_after, d_first, l_after, l_first = [], [], [], [], []
     for i in range(reps):
         kinds = ["alone", "after", "first"]
         kinds = kinds[i % 3:] + kinds[:i % 3]
         t = {}
         for k in kinds:
             t[k] = run_once(attn, True, k != "alone", pp_first=(k == "first"))
+            if k != "alone":
+                (l_after if k == "after" else l_first).append(lat[0][0].elapsed_time(lat[0][1]))
         ta.append(t["alone"])
         d_after.append(t["after"] - t["alone"])
         d_first.append(t["first"] - t["alone"])
@@ -249,10 +256,13 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
                 "added_ms_pass_first": med(d_first), "added_ms_pass_first_quartiles": quart(d_first),
                 "hidden_fraction_pass_after": 1.0 - med(d_after) / t_pp,
                 "hidden_fraction_pass_first": 1.0 - med(d_first) / t_pp,
+                "early_pass_latency_ms_pass_after": med(l_after),
+                "early_pass_latency_ms_pass_first": med(l_first),
                 "what": f"{reps} repetitions, each timing the attention alone and with the early pass "
-                        "enqueued after and before it (rotating order); added = that repetition's "
-                        "difference to the attention alone, median and quartiles; hidden fraction = "
-                        "1 - added / t_predict_plan"}}
+                        "(fb_predict_plan_packed) enqueued after and before it (rotating order); "
+                        "added = that repetition's difference to the attention alone, median and "
+                        "quartiles; hidden fraction = 1 - added / t_predict_plan; early-pass "
+                        "latency = its own start-to-end on the side stream beside the attention"}}
 
 def _time_ms(torch, stream, fn, K):
     """Average duration of K back-to-back calls of fn, bracketed by events on the stream."""
@@ -463,8 +473,12 @@ def main():
     plan = fb.plan_swaps_device(out.counts, slots_t, budget)   # allocates the plan buffers once
 
     def step(i, router):
-        pred.predict_load(xs[i % nbuf], router, scoring, e2r_t, wl.R, select_bias=sb, out=out)
-        fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
+        if isinstance(router, fb.PackedRouter):
+            pred.predict_plan(xs[i % nbuf], router, scoring, e2r_t, slots_t, budget, select_bias=sb,
+                              out=out, plan=plan)
+        else:
+            pred.predict_load(xs[i % nbuf], router, scoring, e2r_t, wl.R, select_bias=sb, out=out)
+            fb.plan_swaps_device(out.counts, slots_t, budget, out=plan)
 
     if args.power:
         res = measure_power(torch, xs, nbuf,
@@ -496,9 +510,8 @@ def main():
                 s_j.wait_event(ev)
         for i in range(first, first + n):
             s_j, p_j, o_j, pl_j = lanes[i % args.streams]
-            p_j.predict_load(xs[i % nbuf], wp, scoring, e2r_t, wl.R, select_bias=sb, out=o_j,
-                             stream=s_j)
-            fb.plan_swaps_device(o_j.counts, slots_t, budget, out=pl_j, stream=s_j)
+            p_j.predict_plan(xs[i % nbuf], wp, scoring, e2r_t, slots_t, budget, select_bias=sb,
+                             out=o_j, plan=pl_j, stream=s_j)
         if args.streams > 1:
             for s_j, _, _, _ in lanes:
                 e = torch.cuda.Event()
@@ -643,7 +656,8 @@ def main():
                                 if wl.n_group > 1 else "")),
                    "ranks": wl.R, "slots_per_rank": wl.S, "swap_budget": wl.budget,
                    "split_mode": split_mode,
-                   "step": "fb_predict_load_packed + fb_plan_swaps_device on one batch; "
+                   "step": "fb_predict_plan_packed on one batch (the prediction, then the swap "
+                           "plan in its last workgroup); "
                            f"{args.streams} batches in flight on {args.streams} streams",
                    "router_packing": "once, before timing (fb_pack_router_weight)"},
         "clock_settle": {"ms": args.settle_ms, "steps": n_settle},

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define FB_ABI_VERSION 4
+#define FB_ABI_VERSION 5
 
 /* Status codes. */
 #define FB_OK 0
@@ -234,6 +234,29 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
                            int32_t* counts, int32_t* rank_loads, double* max_mean,
                            void* workspace, size_t workspace_bytes, int32_t* topk_idx,
                            float* logits, void* stream);
+
+/* The whole early pass of one layer in one call: fb_predict_load_packed, then the swap plan of the
+ * predicted counts as fb_plan_swaps_device would make it (Alg. 1, Eq. 6-8), stream-ordered with no
+ * host round trip.  For a swap-count budget in frontier mode on at most 64 ranks with S * S <= 128
+ * (the DeepSeek-V3-shaped 32 x 8 placement, for instance) the plan is made inside the predictor's
+ * last workgroup, right after the counts are complete, so that no separate kernel has to wait for
+ * a free compute unit when the call runs beside other work (attention on another stream); any
+ * other plan runs as its own kernel on the same stream.  Results are identical to the two calls.
+ *   hidden ... workspace_bytes   as in fb_predict_load_packed (no debug outputs).
+ *   counts                       device int32[E] out: the predicted counts, then the planner's
+ *                                input.
+ *   slot_expert ... status       as in fb_plan_swaps_device (device arrays; budget a host struct
+ *                                read during the call), with this call's E and R.
+ * Errors: every argument error of either call, checked on the host before anything runs. */
+int fb_predict_plan_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                           int32_t dtype, const void* router_packed, size_t router_packed_bytes,
+                           int32_t E, const float* logit_bias, const float* select_bias,
+                           const fb_scoring* scoring, const int32_t* expert_to_rank, int32_t R,
+                           int32_t* counts, int32_t* rank_loads, double* max_mean,
+                           void* workspace, size_t workspace_bytes, const int32_t* slot_expert,
+                           int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
+                           int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                           int64_t* new_rank_loads, int32_t* status, void* stream);
 
 /* fb_predict_load_packed for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument, no allocation.  The

@@ -280,6 +280,69 @@ class Predictor:
         L.check(st, "fb_predict_load_packed" if packed else "fb_predict_load")
         return out
 
+    def predict_plan(self, hidden: torch.Tensor, router: PackedRouter, scoring: Scoring,
+                     expert_to_rank: torch.Tensor, slots: torch.Tensor, budget: Budget, *,
+                     logit_bias=None, select_bias=None, out: Optional[Prediction] = None,
+                     plan: Optional[DevicePlan] = None,
+                     stream: Optional[torch.cuda.Stream] = None):
+        """fb_predict_plan_packed: the prediction and the swap plan of its counts in one call
+        (the plan inside the predictor's last workgroup where the one-wave planner serves it).
+        slots is the int32[R, S] placement; returns (Prediction, DevicePlan)."""
+        if not isinstance(router, PackedRouter):
+            raise ValueError("predict_plan takes a packed router (pack_router_weight)")
+        if hidden.dim() != 2 or (hidden.numel() > 0 and hidden.stride(1) != 1):
+            raise ValueError("hidden must be T x H with rows contiguous in H")
+        if slots.dtype != torch.int32 or slots.dim() != 2 or not slots.is_contiguous():
+            raise ValueError("slots must be a contiguous int32[R, S] tensor")
+        T, H = hidden.shape
+        E = router.E
+        if router.H != H or router.dtype != hidden.dtype:
+            raise ValueError("packed router was built for another H or dtype")
+        R, S = slots.shape
+        for t in (hidden, expert_to_rank, slots, logit_bias, select_bias, router.data):
+            if t is not None and t.device != self.device:
+                raise ValueError("all tensors must live on the predictor's device")
+        if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
+            raise ValueError("expert_to_rank must be int32[E]")
+        for b in (logit_bias, select_bias):
+            if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
+                raise ValueError("biases must be contiguous float32[E]")
+        code = _dtype_code(hidden)
+        lib = L.lib()
+        if self.split:
+            with torch.cuda.device(self.device):
+                need = int(lib.fb_predict_split_workspace_bytes(T, E, H, code))
+            if need > 0:
+                self._reserve(need, stream)
+        else:
+            self._reserve(2048, stream)
+        dev = self.device
+        if out is None:
+            out = Prediction(torch.empty(E, dtype=torch.int32, device=dev),
+                             torch.empty(R, dtype=torch.int32, device=dev),
+                             torch.empty(1, dtype=torch.float64, device=dev))
+        if plan is None:
+            plan = DevicePlan(torch.empty(max(budget.max_swaps, 1) * SWAP_BYTES, dtype=torch.uint8,
+                                          device=dev),
+                              torch.empty(1, dtype=torch.int32, device=dev),
+                              torch.empty((R, S), dtype=torch.int32, device=dev),
+                              torch.empty(E, dtype=torch.int32, device=dev),
+                              torch.empty(R, dtype=torch.int64, device=dev),
+                              torch.empty(1, dtype=torch.int32, device=dev))
+        sc = scoring.to_c()
+        bg = budget.to_c()
+        ld = hidden.stride(0) if T > 0 else H
+        with torch.cuda.device(dev):
+            st = lib.fb_predict_plan_packed(
+                _ptr(hidden), T, H, ld, code, _ptr(router.data), router.data.numel(), E,
+                _ptr(logit_bias), _ptr(select_bias), ctypes.byref(sc), _ptr(expert_to_rank), R,
+                _ptr(out.counts), _ptr(out.rank_loads), _ptr(out.max_mean), _ptr(self.workspace),
+                self.workspace.numel(), slots.data_ptr(), S, ctypes.byref(bg), plan.swaps.data_ptr(),
+                plan.n_swaps.data_ptr(), plan.slots.data_ptr(), plan.expert_to_rank.data_ptr(),
+                plan.rank_loads.data_ptr(), plan.status.data_ptr(), _stream_handle(dev, stream))
+        L.check(st, "fb_predict_plan_packed")
+        return out, plan
+
 
 def predict_load_packed_noalloc(hidden: torch.Tensor, router: PackedRouter, scoring: Scoring,
                                 expert_to_rank: torch.Tensor, R: int, out: Prediction, *,

@@ -199,6 +199,53 @@ fb::PredictLaunch make_launch(const void* hidden, int64_t T, int32_t H, int64_t 
   a.num_cus = fb::device_cu_count();
   a.partial = nullptr;
   a.partial_bytes = 0;
+  a.plan = nullptr;
+  return a;
+}
+
+// Arguments of the swap-count device planner (all but the counts): FB_OK or the status to return.
+int check_plan_device(int32_t E, const int32_t* slot_expert, int32_t R, int32_t S,
+                      const fb_budget* budget, const fb_swap* swaps, const int32_t* n_swaps,
+                      const int32_t* new_slot_expert, const int32_t* new_expert_to_rank,
+                      const int64_t* new_rank_loads, const int32_t* status) {
+  if (!slot_expert || !budget || !n_swaps || !new_slot_expert || !new_expert_to_rank ||
+      !new_rank_loads || !status)
+    return FB_EINVAL;
+  if (E < 1 || R < 1 || S < 1) return FB_EINVAL;
+  if (R > FB_MAX_RANKS || (int64_t)R * S > FB_MAX_SLOTS_TOTAL) return FB_EUNSUPPORTED;
+  if (E > R * S) return FB_EINVAL;
+  const fb_budget bg = *budget;
+  if (bg.max_swaps < 0 || bg.per_rank_cap < 0 || bg.tau < 0 || bg.gamma_num < 0 || bg.gamma_den < 0)
+    return FB_EINVAL;
+  if (bg.mode != FB_FRONTIER && bg.mode != FB_FULL) return FB_EINVAL;
+  if (bg.max_swaps > 0 && !swaps) return FB_EINVAL;
+  return FB_OK;
+}
+
+fb::PlanDeviceLaunch make_plan_launch(const int32_t* counts, int32_t E, const int32_t* slot_expert,
+                                      int32_t R, int32_t S, const fb_budget& bg, fb_swap* swaps,
+                                      int32_t* n_swaps, int32_t* new_slot_expert,
+                                      int32_t* new_expert_to_rank, int64_t* new_rank_loads,
+                                      int32_t* status, void* stream) {
+  fb::PlanDeviceLaunch a;
+  a.counts = counts;
+  a.E = E;
+  a.slot_expert = slot_expert;
+  a.R = R;
+  a.S = S;
+  a.budget = bg;
+  a.swaps = swaps;
+  a.n_swaps = n_swaps;
+  a.new_slot_expert = new_slot_expert;
+  a.new_expert_to_rank = new_expert_to_rank;
+  a.new_rank_loads = new_rank_loads;
+  a.status = status;
+  a.stream = stream;
+  a.timed = 0;
+  a.cost = fb_cost_model{};
+  a.rank_node = nullptr;
+  a.expert_bytes = nullptr;
+  a.swap_cost_ns = nullptr;
   return a;
 }
 
@@ -257,6 +304,46 @@ int fb_predict_load_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
   return fb::launch_predict(a);
 }
 
+int fb_predict_plan_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                           int32_t dtype, const void* router_packed, size_t router_packed_bytes,
+                           int32_t E, const float* logit_bias, const float* select_bias,
+                           const fb_scoring* scoring, const int32_t* expert_to_rank, int32_t R,
+                           int32_t* counts, int32_t* rank_loads, double* max_mean,
+                           void* workspace, size_t workspace_bytes, const int32_t* slot_expert,
+                           int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
+                           int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                           int64_t* new_rank_loads, int32_t* status, void* stream) {
+  if (!router_packed) return FB_EINVAL;
+  const int vc = check_predict(hidden, T, H, ld_hidden, dtype, E, select_bias, scoring,
+                               expert_to_rank, R, counts, rank_loads, max_mean, workspace,
+                               workspace_bytes, fb::kWsBytes);
+  if (vc != FB_OK) return vc;
+  const int pc = check_plan_device(E, slot_expert, R, S, budget, swaps, n_swaps, new_slot_expert,
+                                   new_expert_to_rank, new_rank_loads, status);
+  if (pc != FB_OK) return pc;
+  if (!aligned16(router_packed)) return FB_EUNSUPPORTED;
+  if (router_packed_bytes < fb::router_packed_bytes(E, H, dtype)) return FB_ENOSPC;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  fb::PredictLaunch a = make_launch(hidden, T, H, ld_hidden, dtype, router_packed, E, logit_bias,
+                                    select_bias, scoring, expert_to_rank, R, counts, rank_loads,
+                                    max_mean, workspace, nullptr, nullptr, stream);
+  const size_t sb = fb::split_workspace_bytes(T, E, H, dtype, a.num_cus);
+  if (sb > 0 && workspace_bytes >= fb::kWsBytes + sb) {
+    a.partial = reinterpret_cast<float*>(static_cast<char*>(workspace) + fb::kWsBytes);
+    a.partial_bytes = workspace_bytes - fb::kWsBytes;
+  }
+  const fb::PlanDeviceLaunch p = make_plan_launch(counts, E, slot_expert, R, S, *budget, swaps,
+                                                  n_swaps, new_slot_expert, new_expert_to_rank,
+                                                  new_rank_loads, status, stream);
+  // the one-wave planner runs in the predictor's last workgroup; any other plan follows as a
+  // kernel of its own on the same stream
+  if (fb::plan_fusable(p)) a.plan = &p;
+  const int lc = fb::launch_predict(a);
+  if (lc != FB_OK || a.plan != nullptr) return lc;
+  return fb::launch_plan_device(p);
+}
+
 int fb_predict_load_packed_noalloc(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
                                    int32_t dtype, const void* router_packed,
                                    size_t router_packed_bytes, int32_t E, const float* logit_bias,
@@ -300,38 +387,15 @@ int fb_plan_swaps_device(const int32_t* counts, int32_t E, const int32_t* slot_e
                          int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
                          int32_t* new_slot_expert, int32_t* new_expert_to_rank,
                          int64_t* new_rank_loads, int32_t* status, void* stream) {
-  if (!counts || !slot_expert || !budget || !n_swaps || !new_slot_expert || !new_expert_to_rank ||
-      !new_rank_loads || !status)
-    return FB_EINVAL;
-  if (E < 1 || R < 1 || S < 1) return FB_EINVAL;
-  if (R > FB_MAX_RANKS || (int64_t)R * S > FB_MAX_SLOTS_TOTAL) return FB_EUNSUPPORTED;
-  if (E > R * S) return FB_EINVAL;
-  const fb_budget bg = *budget;
-  if (bg.max_swaps < 0 || bg.per_rank_cap < 0 || bg.tau < 0 || bg.gamma_num < 0 || bg.gamma_den < 0)
-    return FB_EINVAL;
-  if (bg.mode != FB_FRONTIER && bg.mode != FB_FULL) return FB_EINVAL;
-  if (bg.max_swaps > 0 && !swaps) return FB_EINVAL;
+  if (!counts) return FB_EINVAL;
+  const int vc = check_plan_device(E, slot_expert, R, S, budget, swaps, n_swaps, new_slot_expert,
+                                   new_expert_to_rank, new_rank_loads, status);
+  if (vc != FB_OK) return vc;
   const int dc = fb::check_device();
   if (dc != FB_OK) return dc;
-  fb::PlanDeviceLaunch a;
-  a.counts = counts;
-  a.E = E;
-  a.slot_expert = slot_expert;
-  a.R = R;
-  a.S = S;
-  a.budget = bg;
-  a.swaps = swaps;
-  a.n_swaps = n_swaps;
-  a.new_slot_expert = new_slot_expert;
-  a.new_expert_to_rank = new_expert_to_rank;
-  a.new_rank_loads = new_rank_loads;
-  a.status = status;
-  a.stream = stream;
-  a.timed = 0;
-  a.rank_node = nullptr;
-  a.expert_bytes = nullptr;
-  a.swap_cost_ns = nullptr;
-  return fb::launch_plan_device(a);
+  return fb::launch_plan_device(make_plan_launch(counts, E, slot_expert, R, S, *budget, swaps,
+                                                 n_swaps, new_slot_expert, new_expert_to_rank,
+                                                 new_rank_loads, status, stream));
 }
 
 int fb_plan_swaps_timed_device(const int32_t* counts, int32_t E, const int32_t* slot_expert,

@@ -9,6 +9,8 @@
 namespace fb {
 
 // Arguments of one fused predictor launch, validated by the ABI layer.
+struct PlanDeviceLaunch;
+
 struct PredictLaunch {
   const void* hidden;
   int64_t T;
@@ -32,6 +34,9 @@ struct PredictLaunch {
   int32_t num_cus;    // compute units of the device (tile-height choice)
   float* partial;     // split mode: partial-logit buffer in the workspace, or NULL
   size_t partial_bytes;
+  // the swap plan of the counts, made in the predictor's last workgroup (frontier mode, swap-count
+  // budget, R <= 64, S * S <= 128; see plan_fusable), or NULL
+  const PlanDeviceLaunch* plan;
 };
 // Bytes of partial logits the split mode needs for a batch (0: that batch runs fused).
 size_t split_workspace_bytes(int64_t T, int32_t E, int32_t H, int32_t dtype, int num_cus);
@@ -87,6 +92,11 @@ struct PlanDeviceLaunch {
 constexpr int kMaxTimedSwaps = 1024;           // swap cap of the device planner under a time budget
 constexpr int64_t kCostLimit = (int64_t)1 << 40;  // alpha, beta and expert sizes
 int launch_plan_device(const PlanDeviceLaunch& a);
+// Whether the one-wave planner serves this plan, so that it can run inside the predictor's last
+// workgroup: a swap-count budget in frontier mode, R <= 64 and S * S <= 128.
+inline bool plan_fusable(const PlanDeviceLaunch& a) {
+  return !a.timed && a.budget.mode == FB_FRONTIER && a.R <= 64 && (int64_t)a.S * a.S <= 128;
+}
 
 // Prediction-quality diagnostics (fb_quality.hip).
 constexpr int kCosineBlocks = 1024;           // grid of the row-cosine kernel (4 waves each)

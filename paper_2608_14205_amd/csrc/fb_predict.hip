@@ -37,6 +37,7 @@
 #include <type_traits>
 
 #include "fb_internal.h"
+#include "fb_plan_wave.h"
 
 namespace fb {
 namespace {
@@ -101,6 +102,8 @@ struct Params {
   int32_t st_total;    // stages of a whole row
   int32_t ks;          // splits of the stage range (split mode); 1 otherwise
   float* partial;      // split mode: partial logits, [tile][split][register][thread]
+  int32_t plan_cpl;    // 0: no plan; 1 or 2: the one-wave planner's candidates per lane
+  PlanDeviceLaunch plan;   // the swap plan of the counts, made by the last workgroup
 };
 
 // Workgroup barrier that orders LDS only; outstanding global loads stay in flight across it.
@@ -1064,6 +1067,17 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
     *p.max_mean = s_flag ? -1.0 : ratio;
     atomicExch(p.ws_ticket, 0u);
   }
+  if (p.plan_cpl != 0) {
+    // The swap plan of the counts just written (Alg. 1, frontier mode): the one-wave planner in
+    // this workgroup's first wave, in LDS the selection no longer needs.  The barrier publishes
+    // every wave's counts; the other waves are done.
+    static_assert(SMEM >= plan_wave_lds_bytes(wave_cap(1, 2), 1), "the planner's LDS fits");
+    __syncthreads();
+    if (wave != 0) return;
+    const PlanWaveLds l = plan_wave_lds(smem, wave_cap(1, 2), 1);
+    if (p.plan_cpl == 1) plan_wave_body<1, 1>(p.plan, l);
+    else plan_wave_body<1, 2>(p.plan, l);
+  }
 }
 
 __global__ void zero_kernel(uint32_t* p, size_t n) {
@@ -1154,6 +1168,11 @@ int launch_cfg_bm(const PredictLaunch& a) {
   p.st_base = 0;
   p.ks = split_count(a.T, BM, p.st_total, a.num_cus);
   p.partial = a.partial;
+  p.plan_cpl = 0;
+  if (a.plan != nullptr) {
+    p.plan = *a.plan;
+    p.plan_cpl = (int64_t)a.plan->S * a.plan->S <= 64 ? 1 : 2;
+  }
   hipStream_t st = static_cast<hipStream_t>(a.stream);
   if (p.ks > 1 && a.partial != nullptr &&
       a.partial_bytes >= (size_t)tiles * p.ks * BM * EPAD * sizeof(float)) {

@@ -36,7 +36,8 @@ def test_header_declares_the_boundary():
                             "fb_topk_hits", "fb_cosine_workspace_bytes", "fb_row_cosine_mean",
                             "fb_fold_rank_loads", "fb_plan_swaps_timed",
                             "fb_plan_swaps_timed_device", "fb_predict_split_workspace_bytes",
-                            "fb_fold_slot_loads", "fb_predict_load_packed_noalloc"])
+                            "fb_fold_slot_loads", "fb_predict_load_packed_noalloc",
+                            "fb_predict_plan_packed"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -55,7 +56,7 @@ def test_struct_layouts_match_header():
 
 def test_version_and_status_strings():
     lib = fb.lib()
-    assert lib.fb_abi_version() == 4
+    assert lib.fb_abi_version() == 5
     for code in (0, -1, -2, -3, -4):
         assert L.status_string(code).startswith("FB_")
     assert "unknown" in L.status_string(7)
@@ -384,6 +385,45 @@ def _predict_noalloc_call(**over):
 def test_predict_noalloc_validation_without_gpu(over, code):
     """Arguments are checked before the scratch is looked up or anything is launched."""
     assert _predict_noalloc_call(**over) == code
+
+
+def _predict_plan_call(**over):
+    """fb_predict_plan_packed with fake (never dereferenced) pointers."""
+    a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, wp=0x2000, wpb=8192, E=16, lb=None,
+             sb=None, sc=fb.Scoring("softmax", 2).to_c(), e2r=0x3000, R=4, counts=0x4000,
+             rl=0x5000, mm=0x6000, ws=0x7000, wsb=2048, slots=0x8000, S=4,
+             bg=fb.Budget(4).to_c(), swaps=0x9000, ns=0xa000, nslots=0xb000, ne2r=0xc000,
+             nrl=0xd000, status=0xe000, stream=None)
+    a.update(over)
+    sc, bg = a["sc"], a["bg"]
+    return fb.lib().fb_predict_plan_packed(
+        a["hidden"], a["T"], a["H"], a["ld"], a["dtype"], a["wp"], a["wpb"], a["E"], a["lb"],
+        a["sb"], ctypes.byref(sc) if sc is not None else None, a["e2r"], a["R"], a["counts"],
+        a["rl"], a["mm"], a["ws"], a["wsb"], a["slots"], a["S"],
+        ctypes.byref(bg) if bg is not None else None, a["swaps"], a["ns"], a["nslots"], a["ne2r"],
+        a["nrl"], a["status"], a["stream"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(wp=None), L.FB_EINVAL),
+    (dict(wp=0x2008), L.FB_EUNSUPPORTED),
+    (dict(wpb=8191), L.FB_ENOSPC),
+    (dict(counts=None), L.FB_EINVAL),
+    (dict(wsb=2047), L.FB_ENOSPC),
+    (dict(T=-2), L.FB_EINVAL),
+    (dict(H=48), L.FB_EUNSUPPORTED),
+    (dict(slots=None), L.FB_EINVAL),
+    (dict(bg=None), L.FB_EINVAL),
+    (dict(S=0), L.FB_EINVAL),
+    (dict(S=3), L.FB_EINVAL),                     # E = 16 > R * S = 12
+    (dict(status=None), L.FB_EINVAL),
+    (dict(nrl=None), L.FB_EINVAL),
+    (dict(swaps=None), L.FB_EINVAL),              # a budget of 4 needs room for the swaps
+    (dict(bg=fb.Budget(4, mode="full").to_c(), R=2000, e2r=0x3000), L.FB_EUNSUPPORTED),
+])
+def test_predict_plan_validation_without_gpu(over, code):
+    """Both calls' arguments are checked on the host before anything runs."""
+    assert _predict_plan_call(**over) == code
 
 
 def test_unpacked_predict_needs_room_for_the_packed_weight():
