@@ -70,6 +70,44 @@ def test_graph_replay_matches_eager():
     assert not pred.workspace[:2048].any().item()
 
 
+def test_graph_replay_of_the_one_call_early_pass():
+    """fb_predict_plan_packed (prediction and plan in one kernel) captured as one graph node."""
+    _say("[graph] capture predict_plan")
+    wl, slots, e2r, x, w, sb = _setup(T=6000, layer=2)
+    e2r_t = torch.from_numpy(e2r).cuda()
+    slots_t = torch.from_numpy(slots).cuda()
+    wp = fb.pack_router_weight(w)
+    sc, bg = scoring_of(wl), fb.Budget(wl.budget)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        pred = fb.Predictor(stream=side)
+        out, plan = pred.predict_plan(x, wp, sc, e2r_t, slots_t, bg, select_bias=sb)
+    side.synchronize()
+    eager = (out.counts.clone(), out.rank_loads.clone(), out.max_mean.clone(), _plan_tuple(plan))
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        pred.predict_plan(x, wp, sc, e2r_t, slots_t, bg, select_bias=sb, out=out, plan=plan)
+    torch.cuda.synchronize()
+
+    x2 = to_device(make_layer(wl, 3).x, wl.dtype)   # eager work on other data between replays
+    for rep in range(4):
+        out.counts.fill_(-7)
+        plan.n_swaps.fill_(-7)
+        plan.slots.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.counts, eager[0]), f"replay {rep}: counts"
+        assert torch.equal(out.rank_loads, eager[1])
+        assert torch.equal(out.max_mean, eager[2])
+        pt = _plan_tuple(plan)
+        assert pt[0] == eager[3][0] and np.array_equal(pt[1], eager[3][1]) and np.array_equal(pt[2], eager[3][2])
+        other = fb.predict_load(x2, w, sc, e2r_t, wl.R, select_bias=sb)
+        torch.cuda.synchronize()
+        assert int(other.counts.sum().item()) == x2.shape[0] * wl.k
+    assert not pred.workspace[:2048].any().item()
+
+
 def test_side_stream_next_to_other_work():
     """The predictor on its own stream while a dense bf16 GEMM runs on another (the early pass shares
     the GPU with other layer work): both results stay correct.  The timings are printed."""
