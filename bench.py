@@ -353,25 +353,33 @@ def measure_power(torch, xs, nbuf, run_pred, wt, stream, seconds):
 def measure_extras(args, fb, torch, wl, xs, nbuf, wp, w, scoring, budget, e2r_t, slots_t, sb, pred,
                    out, stream):
     """The rest of the hot path's entry points on the same workload, each timed back to back:
-    the predict -> plan step replayed from a HIP graph, the prediction-quality diagnostics (row
-    cosine of two hidden-state batches, top-k hits, rank fold), the time-budgeted planner and the
-    fold and plan of a replicated placement."""
+    the step replayed from a HIP graph (one node, and predict -> plan as two), the
+    prediction-quality diagnostics (row cosine of two hidden-state batches, top-k hits, rank fold),
+    the time-budgeted planner and the fold and plan of a replicated placement."""
     K = max(10, args.steps // 4)
     res = {}
-    # predict -> plan captured once per hidden-state buffer, replayed in rotation
+    # the step (fb_predict_plan_packed, one node) captured once per hidden-state buffer, replayed
+    # in rotation; and predict -> plan as two nodes
     try:
         side = torch.cuda.Stream()
         plan_g = fb.plan_swaps_device(out.counts, slots_t, budget)
-        graphs = []
+        graphs, graphs2 = [], []
         with torch.cuda.stream(side):
             for i in range(nbuf):
                 g = torch.cuda.CUDAGraph()
                 with torch.cuda.graph(g, stream=side):
+                    pred.predict_plan(xs[i], wp, scoring, e2r_t, slots_t, budget, select_bias=sb,
+                                      out=out, plan=plan_g)
+                graphs.append(g)
+                g2 = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g2, stream=side):
                     pred.predict_load(xs[i], wp, scoring, e2r_t, wl.R, select_bias=sb, out=out)
                     fb.plan_swaps_device(out.counts, slots_t, budget, out=plan_g)
-                graphs.append(g)
+                graphs2.append(g2)
         torch.cuda.synchronize()
         res["graph_ms_per_step"] = _time_ms(torch, stream, lambda i: graphs[i % nbuf].replay(), K)
+        res["graph_two_nodes_ms_per_step"] = _time_ms(torch, stream,
+                                                      lambda i: graphs2[i % nbuf].replay(), K)
     except Exception as ex:  # graph capture is context, never a reason to lose the bench line
         res["graph_ms_per_step"] = None
         res["graph_error"] = str(ex)[:200]
