@@ -47,6 +47,13 @@ constexpr int kMaxSurvivors = 8192;           // full mode: work units listed pe
 constexpr int kSmallRS = 512;
 constexpr int kSmallR = 64;
 
+// Full mode on tables of at most kSmallR ranks and S <= kFrontS slots per rank: every unordered rank
+// pair keeps the candidates that no other candidate of the pair dominates (at most kFrontCap of
+// them; kFrontAll when more, and then all of the pair's candidates are scored).
+constexpr int kFrontS = 8;
+constexpr int kFrontCap = 8;
+constexpr uint8_t kFrontAll = 255;
+
 // Tie order after the benefit: (src rank, dst rank, item i, item j) ascending, as one integer.
 __device__ __forceinline__ uint64_t tie_key(int a, int b, int i, int j) {
   return ((uint64_t)a << (kRankBits + 2 * kItemBits)) | ((uint64_t)b << (2 * kItemBits)) |
@@ -54,10 +61,17 @@ __device__ __forceinline__ uint64_t tie_key(int a, int b, int i, int j) {
 }
 
 // LDS of plan_general for tables of at most CRS slots and CR ranks; SURV work units listed per
-// full-mode round.  E <= R * S <= CRS, so the per-expert arrays fit the slot capacity.
-template <int CRS, int CR, int SURV>
+// full-mode round; NPAIR rank pairs with a stored frontier.  E <= R * S <= CRS, so the per-expert
+// arrays fit the slot capacity.
+template <int CRS, int CR, int SURV, int NPAIR>
 struct SharedT {
   static constexpr int kSurv = SURV;
+  // full mode with stored frontiers: per unordered pair (index b (b - 1) / 2 + a for a < b) the
+  // number of stored candidates (or kFrontAll) and each one's slot pair p * S + q, with p on the
+  // more loaded rank of the pair when the frontier was built
+  uint8_t fr_n[NPAIR];
+  uint8_t fr_pt[NPAIR][kFrontCap];
+  int32_t last[2];               // ranks of the swap accepted in the previous round
   int32_t item[CRS];             // slot -> item id (slot value, or V + slot for an empty slot)
   int32_t sload[CRS];            // slot -> load (token share) of its item
   uint8_t mslot[CRS];            // slot -> its item has moved
@@ -130,6 +144,39 @@ __device__ __forceinline__ bool swap_fits(const PlanDeviceLaunch& a, const SH& s
   return c <= a.cost.link_budget_ns - used;
 }
 
+// What a rank pair's candidates share under a time budget: the link's alpha and beta, and the most
+// a candidate may cost (what is left of both ranks' budgets and of the pair's link budget).
+struct PairCost {
+  int64_t alpha, beta, cap_ns;
+  double inv_beta;
+};
+
+// One step of a lexicographic minimum of (u, c, t) with payload x, with the lane that DPP control
+// CTRL names (every lane of the wave takes part).
+template <int CTRL>
+__device__ __forceinline__ void lex_min_step(uint64_t& u, uint64_t& c, uint64_t& t, int& x) {
+  const uint64_t u2 = dpp_u64<CTRL>(u), c2 = dpp_u64<CTRL>(c), t2 = dpp_u64<CTRL>(t);
+  const int x2 = __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+  if (u2 < u || (u2 == u && (c2 < c || (c2 == c && t2 < t)))) { u = u2; c = c2; t = t2; x = x2; }
+}
+
+// Lexicographic minimum over each group of 8 lanes (8g .. 8g + 7); every lane of a group ends with
+// it.  Lane exchanges: lane ^ 1, lane ^ 2, then the mirror within the 8 lanes (lane i and 7 - i).
+__device__ __forceinline__ void seg_min8(uint64_t& u, uint64_t& c, uint64_t& t, int& x) {
+  lex_min_step<0xB1>(u, c, t, x);    // quad_perm [1,0,3,2]
+  lex_min_step<0x4E>(u, c, t, x);    // quad_perm [2,3,0,1]
+  lex_min_step<0x141>(u, c, t, x);   // row_half_mirror
+}
+
+// Unordered rank pair k = y (y - 1) / 2 + x, x < y.
+__device__ __forceinline__ void pair_of(int k, int& x, int& y) {
+  int b = (int)((1.0f + sqrtf(8.0f * (float)k + 1.0f)) * 0.5f);
+  while (b * (b - 1) / 2 > k) --b;
+  while ((b + 1) * b / 2 <= k) ++b;
+  y = b;
+  x = k - b * (b - 1) / 2;
+}
+
 // (gain, cost, tie) ordering of the time-budgeted planner; gain 0 means "no candidate".
 __device__ __forceinline__ bool ratio_better(uint64_t g1, uint64_t c1, uint64_t t1, uint64_t g2,
                                              uint64_t c2, uint64_t t2) {
@@ -146,14 +193,40 @@ __device__ __forceinline__ bool ratio_better(uint64_t g1, uint64_t c1, uint64_t 
   return t1 < t2;
 }
 
+// One step of the time-budgeted reduction (the better (gain, cost, tie) by ratio_better) with the
+// lane that DPP control CTRL names.
+template <int CTRL>
+__device__ __forceinline__ void ratio_step(uint64_t& g, uint64_t& c, uint64_t& t) {
+  const uint64_t g2 = dpp_u64<CTRL>(g), c2 = dpp_u64<CTRL>(c), t2 = dpp_u64<CTRL>(t);
+  if (ratio_better(g2, c2, t2, g, c, t)) { g = g2; c = c2; t = t2; }
+}
+
+// Best (gain, cost, tie) of the wave by ratio_better (every lane takes part; uniform result): each
+// row of 16 lanes by DPP (lane ^ 1, lane ^ 2, the mirror within 8 lanes, the mirror within 16),
+// then the four rows.
+__device__ __forceinline__ void wave_best_ratio(uint64_t& g, uint64_t& c, uint64_t& t) {
+  ratio_step<0xB1>(g, c, t);
+  ratio_step<0x4E>(g, c, t);
+  ratio_step<0x141>(g, c, t);
+  ratio_step<0x140>(g, c, t);
+  uint64_t bg = readlane_u64(g, 0), bc = readlane_u64(c, 0), bt = readlane_u64(t, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    const uint64_t og = readlane_u64(g, 16 * r), oc = readlane_u64(c, 16 * r), ot = readlane_u64(t, 16 * r);
+    if (ratio_better(og, oc, ot, bg, bc, bt)) { bg = og; bc = oc; bt = ot; }
+  }
+  g = bg; c = bc; t = bt;
+}
+
 // NT threads (256: frontier mode, 1024: full mode); SMALL: tables of at most kSmallRS slots and
 // kSmallR ranks
 template <int NT, bool SMALL>
 __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   constexpr int CRS = SMALL ? kSmallRS : kMaxRS;
   constexpr int CR = SMALL ? kSmallR : kMaxR;
-  // the survivor list serves full mode only
-  __shared__ SharedT<CRS, CR, NT == 1024 ? kMaxSurvivors : 64> sh;
+  // the survivor list serves full mode only, the stored frontiers full mode on small tables
+  constexpr bool kFront = SMALL && NT == 1024;
+  __shared__ SharedT<CRS, CR, NT == 1024 ? kMaxSurvivors : 64, kFront ? CR * (CR - 1) / 2 : 1> sh;
   constexpr int kSurv = decltype(sh)::kSurv;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -261,6 +334,9 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
   const bool frontier = bg.mode == FB_FRONTIER;
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
   const bool marks = frontier && J > 1;
+  // full mode with stored frontiers (gamma > 0; with gamma = 0 the benefit stops falling with the
+  // load difference once the pair is below the largest load outside it, and the frontiers grow)
+  const bool front = kFront && !frontier && S <= kFrontS && g_num > 0;
   if (a.timed && !frontier) {
     // every candidate moves at least one expert, so it costs at least alpha + the smallest
     // expert's transfer time on its link
@@ -320,7 +396,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         sh.stop = (sh.L[amax] - sh.L[amin] <= bg.tau) ? 1 : 0;
       }
     }
-    if (!frontier) {
+    if (!frontier && !front) {
       for (int r = tid; r < R; r += NT) {
         int32_t lo = INT32_MAX, hi = INT32_MIN;
         for (int q = 0; q < S; ++q) {
@@ -333,11 +409,15 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         sh.u.run.smax[r] = hi;
       }
     }
-    __syncthreads();
-    if (sh.stop) break;
+    // (with stored frontiers the rebuild below needs none of wave 0's results, so the first
+    // barrier after it publishes them)
+    if (!front) {
+      __syncthreads();
+      if (sh.stop) break;
+    }
 
     // ---- candidates ----------------------------------------------------------------------------
-    const int amax = sh.amax, amin = sh.amin;
+    const int amax = front ? 0 : sh.amax, amin = front ? 0 : sh.amin;
     if (marks) {
       // candidate (p, q) would put a replica beside another replica of its expert, or exchange two
       // replicas of one expert, exactly when row p or column q of the pair's same-expert matrix
@@ -394,6 +474,206 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         for (int idx = tid; idx < S * S; idx += NT) {
           const int p = idx / S;
           consider(amax, amin, p, idx - p * S, other);
+        }
+      }
+    } else if (front) {
+      if constexpr (kFront) {
+        // Full mode with stored frontiers (gamma > 0).  In a pair (ra, rb) with D = L_ra - L_rb > 0, a
+        // candidate with load difference d = l_j - l_i leaves the two ranks at their mean +- (D +
+        // 2d) / 2, so with u = |D + 2d| its benefit is den (M - max(o, (L_ra + L_rb + u) / 2)) +
+        // num (D^2 - u^2) / 2, o the largest load outside the pair: it falls strictly as u grows,
+        // whatever M and o are.  A candidate (u, C, tk) therefore cannot be the round's best while
+        // its pair holds another admissible one with u' <= u, C' <= C and (u', C', tk')
+        // lexicographically smaller.  What is left of a pair is a staircase: the lexicographically
+        // smallest (u, C, tk), then the smallest among the candidates that cost less than it, and so
+        // on (one candidate without a time budget).  Only a swap on a rank of the pair changes
+        // what decides it (the pair's loads, items, moved flags, swap counts, rank and link
+        // budgets), so each round rebuilds the staircases of the pairs that hold a rank of the
+        // previous swap (every pair in the first round) and scores the stored candidates of every
+        // pair.
+        auto pair_setup = [&](int x, int y, int& ra, int& rb, PairCost& pc) -> bool {
+          const int64_t Lx = sh.L[x], Ly = sh.L[y];
+          if (Lx == Ly) return false;
+          ra = Lx > Ly ? x : y;
+          rb = Lx > Ly ? y : x;
+          if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) return false;
+          pc.alpha = 0; pc.beta = 1; pc.cap_ns = 0; pc.inv_beta = 1.0;
+          if (a.timed) {
+            const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
+            pc.cap_ns = sh.rank_left[ra] < sh.rank_left[rb] ? sh.rank_left[ra] : sh.rank_left[rb];
+            // a link budget at least the rank budget never binds (every swap on the link also
+            // charges both ranks); else what the pair's accepted swaps left of it
+            if (a.cost.link_budget_ns < a.cost.rank_budget_ns) {
+              const int key = ra < rb ? ra * kMaxR + rb : rb * kMaxR + ra;
+              int64_t left = a.cost.link_budget_ns;
+              for (int s2 = 0; s2 < sh.ns; ++s2) left -= sh.acc_pair[s2] == key ? sh.acc_cost[s2] : 0;
+              pc.cap_ns = left < pc.cap_ns ? left : pc.cap_ns;
+            }
+            if (sh.cmin[t] > pc.cap_ns) return false;      // no swap on this link fits any more
+            pc.alpha = a.cost.alpha_ns[t];
+            pc.beta = a.cost.beta_bytes_per_us[t];
+            pc.inv_beta = 1.0 / (double)pc.beta;
+          }
+          return true;
+        };
+        // admissibility (every test but the benefit's sign) and the keys u, C, tk of candidate
+        // (p, q) of the pair (ra, rb)
+        auto cand = [&](int ra, int rb, int p, int q, const PairCost& pc, int64_t D, uint64_t& u,
+                        uint64_t& c, uint64_t& tk, int64_t& d) -> bool {
+          const int sa = ra * S + p, sb = rb * S + q;
+          const int i = sh.item[sa], j = sh.item[sb];
+          if (sh.mslot[sa] || sh.mslot[sb] || (i >= V && j >= V)) return false;
+          if (J > 1 && ((i < V && holds(rb, i)) || (j < V && holds(ra, j)))) return false;
+          d = (int64_t)sh.sload[sb] - (int64_t)sh.sload[sa];
+          const int64_t x = D + 2 * d;
+          u = (uint64_t)(x < 0 ? -x : x);
+          c = 1;
+          if (a.timed) {
+            const int ei = i >= V ? -1 : J == 1 ? i : expert_of(i, E, inv_e);
+            const int ej = j >= V ? -1 : J == 1 ? j : expert_of(j, E, inv_e);
+            const int64_t bytes = (ei >= 0 ? sh.u.run.ebytes[ei] : 0) + (ej >= 0 ? sh.u.run.ebytes[ej] : 0);
+            const int64_t cc = pc.alpha + ceil_div(bytes * 1000, pc.beta, pc.inv_beta);
+            if (cc > pc.cap_ns) return false;
+            c = (uint64_t)cc;
+          }
+          tk = tie_key(ra, rb, i, j);
+          return true;
+        };
+        // rebuild, one pair per 8 lanes: lane p holds the candidates (p, q) of slot p of the more
+        // loaded rank, and each pass stores the group's lexicographically smallest (u, C, tk) among
+        // the candidates that cost less than the one stored before.  Groups go to waves 1, 2, ...
+        // first: wave 0 finds the extremes meanwhile.
+        const bool all = round == 0;
+        const int nd = all ? R * (R - 1) / 2 : 2 * R - 3;
+        const int la0 = sh.last[0], lb0 = sh.last[1];
+        const int p = lane & 7;
+        const int wv = wave == 0 ? NT / 64 - 1 : wave - 1;
+        for (int w0 = wv * 8; w0 < nd; w0 += NT / 8) {
+          const int w = w0 + (lane >> 3);
+          const bool pv = w < nd;
+          const int wq = pv ? w : 0;
+          int x, y;
+          if (all) {
+            pair_of(wq, x, y);
+          } else {
+            int r0 = la0, o;
+            if (wq < R - 1) {
+              o = wq < la0 ? wq : wq + 1;          // every rank but la0
+            } else {
+              r0 = lb0;                            // every rank but la0 and lb0
+              o = wq - (R - 1);
+              const int lo = la0 < lb0 ? la0 : lb0, hi = la0 < lb0 ? lb0 : la0;
+              if (o >= lo) ++o;
+              if (o >= hi) ++o;
+            }
+            x = r0 < o ? r0 : o;
+            y = r0 < o ? o : r0;
+          }
+          const int k = y * (y - 1) / 2 + x;
+          int ra = 0, rb = 0;
+          PairCost pc;
+          const bool live = pv && pair_setup(x, y, ra, rb, pc);
+          const int64_t D = live ? sh.L[ra] - sh.L[rb] : 0;
+          // slot p of ra, and the S slots of rb, each read once (indices clamped into the rank)
+          const int sa = ra * S + (p < S ? p : S - 1);
+          const int ia = sh.item[sa];
+          const int64_t lia = sh.sload[sa];
+          const bool aok = live && p < S && !sh.mslot[sa] &&
+                           !(J > 1 && ia < V && holds(rb, ia));
+          // the cost of each admissible candidate (1 without a time budget; ~0 for the others), in
+          // registers for the passes, which read the destination slots again
+          uint64_t kc[kFrontS];
+          int64_t ba = 0;
+          if (a.timed && aok && ia < V) ba = sh.u.run.ebytes[J == 1 ? ia : expert_of(ia, E, inv_e)];
+#pragma unroll
+          for (int q = 0; q < kFrontS; ++q) {
+            const int sb = rb * S + (q < S ? q : S - 1);
+            const int j = sh.item[sb];
+            bool ok = aok && q < S && !sh.mslot[sb] && !(ia >= V && j >= V) &&
+                      !(J > 1 && j < V && holds(ra, j));
+            uint64_t c = 1;
+            if (ok && a.timed) {
+              const int64_t bytes = ba + (j < V ? sh.u.run.ebytes[J == 1 ? j : expert_of(j, E, inv_e)] : 0);
+              const int64_t cc = pc.alpha + ceil_div(bytes * 1000, pc.beta, pc.inv_beta);
+              ok = cc <= pc.cap_ns;
+              c = (uint64_t)cc;
+            }
+            kc[q] = ok ? c : ~0ull;
+          }
+          uint64_t climit = ~0ull;
+          int n = 0;
+          bool done = !live;
+          for (;;) {
+            uint64_t bu = ~0ull, bc = ~0ull, bt = ~0ull;   // tie keys of R <= 64 ranks are below ~0
+            int bpq = 0;
+            if (!done) {
+#pragma unroll
+              for (int q = 0; q < kFrontS; ++q) {
+                const uint64_t c = kc[q];
+                if (c >= climit) continue;
+                const int64_t xd = D + 2 * ((int64_t)sh.sload[rb * S + q] - lia);
+                const uint64_t u = (uint64_t)(xd < 0 ? -xd : xd);
+                const uint64_t tk = tie_key(ra, rb, ia, sh.item[rb * S + q]);
+                if (u < bu || (u == bu && (c < bc || (c == bc && tk < bt)))) {
+                  bu = u; bc = c; bt = tk; bpq = p * S + q;
+                }
+              }
+            }
+            seg_min8(bu, bc, bt, bpq);
+            if (!done) {
+              if (bt == ~0ull) {
+                done = true;
+              } else if (n == kFrontCap) {
+                n = kFrontAll;
+                done = true;
+              } else {
+                if (p == 0) sh.fr_pt[k][n] = (uint8_t)bpq;
+                ++n;
+                climit = bc;
+                done = !a.timed;
+              }
+            }
+            if (__ballot(!done) == 0) break;
+          }
+          if (pv && p == 0) sh.fr_n[k] = (uint8_t)n;
+        }
+        __syncthreads();                         // the frontiers and wave 0's extremes
+        if (sh.stop) break;
+        const int64_t Mf = sh.L[sh.amax];
+        // score the stored candidates of every pair, one pair per thread
+        for (int k = tid; k < R * (R - 1) / 2; k += NT) {
+          const int n = sh.fr_n[k];
+          if (n == 0) continue;
+          int x, y, ra, rb;
+          pair_of(k, x, y);
+          PairCost pc;
+          if (!pair_setup(x, y, ra, rb, pc)) continue;
+          int64_t other = INT64_MIN;
+          for (int t3 = 0; t3 < 3; ++t3) {
+            const int tr = sh.top[t3];
+            if (tr >= 0 && tr != ra && tr != rb) { other = sh.L[tr]; break; }
+          }
+          const int64_t La = sh.L[ra], Lb = sh.L[rb];
+          const int cnt = n == kFrontAll ? S * S : n;
+          for (int m = 0; m < cnt; ++m) {
+            const int pq = n == kFrontAll ? m : sh.fr_pt[k][m];
+            const int p = pq / S;
+            uint64_t u, c, tk;
+            int64_t d;
+            if (!cand(ra, rb, p, pq - p * S, pc, La - Lb, u, c, tk, d)) continue;
+            const int64_t la = La + d, lb = Lb - d;
+            int64_t m2 = la > lb ? la : lb;
+            if (other > m2) m2 = other;
+            const int64_t gain = g_den * (Mf - m2) + g_num * (2 * d * (Lb - La - d));
+            if (gain <= 0) continue;
+            if (a.timed) {
+              if (ratio_better((uint64_t)gain, c, tk, bgain, bcost, btie)) {
+                bgain = (uint64_t)gain; bcost = c; btie = tk;
+              }
+            } else if ((uint64_t)gain > bgain || ((uint64_t)gain == bgain && tk < btie)) {
+              bgain = (uint64_t)gain; btie = tk;
+            }
+          }
         }
       }
     } else {
@@ -577,68 +857,70 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
       }
     }
     uint64_t g, t, cst = 1;
+    // the best candidate of every wave, then of the waves' bests (lane w reads wave w's): by
+    // benefit / cost under a time budget, else by benefit; then by tie key
+    constexpr int NW = NT / 64;
     if (a.timed) {
-      // best of the wave by benefit / cost, then tie key: butterfly over the lanes
       uint64_t wg = bgain, wc = bcost, wt = btie;
-      for (int off = 32; off > 0; off >>= 1) {
-        const uint64_t og = __shfl_xor(wg, off), oc = __shfl_xor(wc, off), ot = __shfl_xor(wt, off);
-        if (ratio_better(og, oc, ot, wg, wc, wt)) { wg = og; wc = oc; wt = ot; }
-      }
+      wave_best_ratio(wg, wc, wt);
       if (lane == 0) { sh.wgain[wave] = wg; sh.wtie[wave] = wt; sh.wcost[wave] = wc; }
       __syncthreads();
-      g = sh.wgain[0]; t = sh.wtie[0]; cst = sh.wcost[0];
-      for (int w = 1; w < NT / 64; ++w)
-        if (ratio_better(sh.wgain[w], sh.wcost[w], sh.wtie[w], g, cst, t)) {
-          g = sh.wgain[w]; t = sh.wtie[w]; cst = sh.wcost[w];
-        }
+      g = lane < NW ? sh.wgain[lane] : 0;
+      cst = lane < NW ? sh.wcost[lane] : 1;
+      t = lane < NW ? sh.wtie[lane] : ~0ull;
+      wave_best_ratio(g, cst, t);
     } else {
-      // best of the wave: largest gain, then smallest tie key
       const uint64_t wg = wave_max_u64(bgain);
       const uint64_t wt = ~wave_max_u64((wg != 0 && bgain == wg) ? ~btie : 0ull);
       g = wg; t = wt;
       if (NT > 64) {
         if (lane == 0) { sh.wgain[wave] = wg; sh.wtie[wave] = wt; }
         __syncthreads();
-        g = sh.wgain[0]; t = sh.wtie[0];
-        for (int w = 1; w < NT / 64; ++w) {
-          const uint64_t og = sh.wgain[w], ot = sh.wtie[w];
-          if (og > g || (og == g && og != 0 && ot < t)) { g = og; t = ot; }
-        }
+        const uint64_t og = lane < NW ? sh.wgain[lane] : 0;
+        const uint64_t ot = lane < NW ? sh.wtie[lane] : ~0ull;
+        g = wave_max_u64(og);
+        t = ~wave_max_u64((g != 0 && og == g) ? ~ot : 0ull);
       }
     }
     if (g == 0) break;                          // no admissible candidate with positive benefit
-    if (tid == 0) {
+    if (wave == 0) {
       const int ca = (int)(t >> (kRankBits + 2 * kItemBits)) & ((1 << kRankBits) - 1);
       const int cb = (int)(t >> (2 * kItemBits)) & ((1 << kRankBits) - 1);
       const int ci = (int)(t >> kItemBits) & ((1 << kItemBits) - 1);
       const int cj = (int)t & ((1 << kItemBits) - 1);
       int sa = ca * S, sb = cb * S;               // the winning items' slots (ids are unique)
-      for (int s = 0; s < S; ++s) {
-        if (sh.item[ca * S + s] == ci) sa = ca * S + s;
-        if (sh.item[cb * S + s] == cj) sb = cb * S + s;
+      for (int s0 = 0; s0 < S; s0 += 64) {
+        const int s = s0 + lane;
+        const uint64_t ha = __ballot(s < S && sh.item[ca * S + s] == ci);
+        const uint64_t hb = __ballot(s < S && sh.item[cb * S + s] == cj);
+        if (ha) sa = ca * S + s0 + __ffsll((unsigned long long)ha) - 1;
+        if (hb) sb = cb * S + s0 + __ffsll((unsigned long long)hb) - 1;
       }
-      const int32_t li = sh.sload[sa], lj = sh.sload[sb];
-      const int64_t d = (int64_t)lj - (int64_t)li;
-      sh.item[sa] = cj; sh.sload[sa] = lj;
-      sh.item[sb] = ci; sh.sload[sb] = li;
-      sh.L[ca] += d;
-      sh.L[cb] -= d;
-      sh.mslot[sa] = 1; sh.mslot[sb] = 1;
-      ++sh.part[ca]; ++sh.part[cb];
-      fb_swap sw;
-      sw.src_rank = ca; sw.dst_rank = cb; sw.src_slot = sa - ca * S; sw.dst_slot = sb - cb * S;
-      sw.expert_src = ci < V ? ci : -1;
-      sw.expert_dst = cj < V ? cj : -1;
-      sw.gain = (int64_t)g;
-      a.swaps[sh.ns] = sw;
-      if (a.timed) {
-        sh.rank_left[ca] -= (int64_t)cst;
-        sh.rank_left[cb] -= (int64_t)cst;
-        sh.acc_pair[sh.ns] = ca < cb ? ca * kMaxR + cb : cb * kMaxR + ca;
-        sh.acc_cost[sh.ns] = (int64_t)cst;
-        if (a.swap_cost_ns) a.swap_cost_ns[sh.ns] = (int64_t)cst;
+      if (lane == 0) {
+        const int32_t li = sh.sload[sa], lj = sh.sload[sb];
+        const int64_t d = (int64_t)lj - (int64_t)li;
+        sh.item[sa] = cj; sh.sload[sa] = lj;
+        sh.item[sb] = ci; sh.sload[sb] = li;
+        sh.L[ca] += d;
+        sh.L[cb] -= d;
+        sh.mslot[sa] = 1; sh.mslot[sb] = 1;
+        ++sh.part[ca]; ++sh.part[cb];
+        if constexpr (kFront) { sh.last[0] = ca; sh.last[1] = cb; }
+        fb_swap sw;
+        sw.src_rank = ca; sw.dst_rank = cb; sw.src_slot = sa - ca * S; sw.dst_slot = sb - cb * S;
+        sw.expert_src = ci < V ? ci : -1;
+        sw.expert_dst = cj < V ? cj : -1;
+        sw.gain = (int64_t)g;
+        a.swaps[sh.ns] = sw;
+        if (a.timed) {
+          sh.rank_left[ca] -= (int64_t)cst;
+          sh.rank_left[cb] -= (int64_t)cst;
+          sh.acc_pair[sh.ns] = ca < cb ? ca * kMaxR + cb : cb * kMaxR + ca;
+          sh.acc_cost[sh.ns] = (int64_t)cst;
+          if (a.swap_cost_ns) a.swap_cost_ns[sh.ns] = (int64_t)cst;
+        }
+        sh.ns = sh.ns + 1;
       }
-      sh.ns = sh.ns + 1;
     }
     __syncthreads();
   }

@@ -254,3 +254,28 @@ def test_device_planner_seeded_fuzz():
         _same(_dev(counts, slots, bg), host)
         n += 1
     assert n > 900
+
+
+@pytest.mark.parametrize("max_swaps", [1, 6])
+def test_full_mode_pair_with_a_long_staircase(max_swaps):
+    """Full mode under a time budget on two ranks of 8 slots whose candidates form a staircase of 9
+    (load difference growing while the cost falls): more than the 8 the device planner stores per
+    rank pair, so it scores all of the pair's candidates.  Device = host = oracle."""
+    from oracle.cost import CostModel as OCost
+    print(f"[plan] long staircase, {max_swaps} swaps", flush=True)
+    # rank 0: experts 0-7 with 100 + 10 p tokens and (p + 1) KB; rank 1: experts 8-11 with no
+    # tokens and 5 KB, experts 12-15 with one token and no bytes.  With beta = 1000 B/us a candidate
+    # (p, q) costs alpha + its bytes in ns, and u = |D + 2 (l_q - l_p)| orders the candidates by p;
+    # the one-token partners cost 5000 ns less at u + 2, so every slot p adds a point
+    counts = np.array([100 + 10 * p for p in range(8)] + [0] * 4 + [1] * 4, np.int32)
+    slots = np.arange(16, dtype=np.int32).reshape(2, 8)
+    sizes = [1000 * (p + 1) for p in range(8)] + [5000] * 4 + [0] * 4
+    cm = OCost([0, 0], sizes, (3, 3), (1000, 1000), 10 ** 9)
+    bg = fb.Budget(max_swaps, mode="full")
+    host = fb.plan_swaps_timed(counts, slots, bg, fb.CostModel(*cm))
+    dev = _dev_timed(counts, slots, bg, fb.CostModel(*cm))
+    _same(dev, host)
+    assert dev.costs == host.costs
+    ref = OP.plan_swaps(counts, slots, max_swaps, mode="full", cost=cm)
+    _same(dev, ref)
+    assert len(dev.swaps) >= 1
