@@ -144,6 +144,12 @@ __device__ __forceinline__ bool swap_fits(const PlanDeviceLaunch& a, const SH& s
   return c <= a.cost.link_budget_ns - used;
 }
 
+// A compile-time flag for generic lambdas.
+template <bool B>
+struct Flag {
+  static constexpr bool value = B;
+};
+
 // What a rank pair's candidates share under a time budget: the link's alpha and beta, and the most
 // a candidate may cost (what is left of both ranks' budgets and of the pair's link budget).
 struct PairCost {
@@ -491,14 +497,20 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         // budgets), so each round rebuilds the staircases of the pairs that hold a rank of the
         // previous swap (every pair in the first round) and scores the stored candidates of every
         // pair.
-        auto pair_setup = [&](int x, int y, int& ra, int& rb, PairCost& pc) -> bool {
+        // Flags REP (a replicated placement) and TIMED (a time budget) are compile-time, so the
+        // plain count-budget round is straight-line code.
+        // The pair {x, y}: its orientation (ra the more loaded rank), D = L_ra - L_rb, and what its
+        // candidates may cost; false when none of them can be admissible.
+        auto pair_setup = [&](auto TIMED, int x, int y, int& ra, int& rb, int64_t& D,
+                              PairCost& pc) -> bool {
           const int64_t Lx = sh.L[x], Ly = sh.L[y];
           if (Lx == Ly) return false;
           ra = Lx > Ly ? x : y;
           rb = Lx > Ly ? y : x;
+          D = Lx > Ly ? Lx - Ly : Ly - Lx;
           if (capped && (sh.part[ra] >= bg.per_rank_cap || sh.part[rb] >= bg.per_rank_cap)) return false;
           pc.alpha = 0; pc.beta = 1; pc.cap_ns = 0; pc.inv_beta = 1.0;
-          if (a.timed) {
+          if constexpr (decltype(TIMED)::value) {
             const int t = sh.node[ra] == sh.node[rb] ? 0 : 1;
             pc.cap_ns = sh.rank_left[ra] < sh.rank_left[rb] ? sh.rank_left[ra] : sh.rank_left[rb];
             // a link budget at least the rank budget never binds (every swap on the link also
@@ -516,165 +528,204 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
           }
           return true;
         };
-        // admissibility (every test but the benefit's sign) and the keys u, C, tk of candidate
-        // (p, q) of the pair (ra, rb)
-        auto cand = [&](int ra, int rb, int p, int q, const PairCost& pc, int64_t D, uint64_t& u,
-                        uint64_t& c, uint64_t& tk, int64_t& d) -> bool {
+        // the expert of item it (below V) and its transfer size
+        auto item_bytes = [&](auto REP, int it) -> int64_t {
+          if (it >= V) return 0;
+          return sh.u.run.ebytes[decltype(REP)::value ? expert_of(it, E, inv_e) : it];
+        };
+        // candidate (p, q) of the pair (ra, rb): every admissibility test but the benefit's sign;
+        // its cost c (1 without a time budget) and its load difference d
+        auto cand = [&](auto REP, auto TIMED, int ra, int rb, int p, int q, const PairCost& pc,
+                        uint64_t& c, int64_t& d, int& i, int& j) -> bool {
           const int sa = ra * S + p, sb = rb * S + q;
-          const int i = sh.item[sa], j = sh.item[sb];
+          i = sh.item[sa];
+          j = sh.item[sb];
           if (sh.mslot[sa] || sh.mslot[sb] || (i >= V && j >= V)) return false;
-          if (J > 1 && ((i < V && holds(rb, i)) || (j < V && holds(ra, j)))) return false;
+          if constexpr (decltype(REP)::value)
+            if ((i < V && holds(rb, i)) || (j < V && holds(ra, j))) return false;
           d = (int64_t)sh.sload[sb] - (int64_t)sh.sload[sa];
-          const int64_t x = D + 2 * d;
-          u = (uint64_t)(x < 0 ? -x : x);
           c = 1;
-          if (a.timed) {
-            const int ei = i >= V ? -1 : J == 1 ? i : expert_of(i, E, inv_e);
-            const int ej = j >= V ? -1 : J == 1 ? j : expert_of(j, E, inv_e);
-            const int64_t bytes = (ei >= 0 ? sh.u.run.ebytes[ei] : 0) + (ej >= 0 ? sh.u.run.ebytes[ej] : 0);
-            const int64_t cc = pc.alpha + ceil_div(bytes * 1000, pc.beta, pc.inv_beta);
+          if constexpr (decltype(TIMED)::value) {
+            const int64_t cc = pc.alpha + ceil_div((item_bytes(REP, i) + item_bytes(REP, j)) * 1000,
+                                                   pc.beta, pc.inv_beta);
             if (cc > pc.cap_ns) return false;
             c = (uint64_t)cc;
           }
-          tk = tie_key(ra, rb, i, j);
           return true;
         };
         // rebuild, one pair per 8 lanes: lane p holds the candidates (p, q) of slot p of the more
         // loaded rank, and each pass stores the group's lexicographically smallest (u, C, tk) among
         // the candidates that cost less than the one stored before.  Groups go to waves 1, 2, ...
         // first: wave 0 finds the extremes meanwhile.
-        const bool all = round == 0;
-        const int nd = all ? R * (R - 1) / 2 : 2 * R - 3;
-        const int la0 = sh.last[0], lb0 = sh.last[1];
-        const int p = lane & 7;
-        const int wv = wave == 0 ? NT / 64 - 1 : wave - 1;
-        for (int w0 = wv * 8; w0 < nd; w0 += NT / 8) {
-          const int w = w0 + (lane >> 3);
-          const bool pv = w < nd;
-          const int wq = pv ? w : 0;
-          int x, y;
-          if (all) {
-            pair_of(wq, x, y);
-          } else {
-            int r0 = la0, o;
-            if (wq < R - 1) {
-              o = wq < la0 ? wq : wq + 1;          // every rank but la0
+        auto build = [&](auto REP, auto TIMED) {
+          constexpr bool rep = decltype(REP)::value, timed = decltype(TIMED)::value;
+          const bool all = round == 0;
+          const int nd = all ? R * (R - 1) / 2 : 2 * R - 3;
+          const int la0 = sh.last[0], lb0 = sh.last[1];
+          const int p = lane & 7;
+          const int wv = wave == 0 ? NT / 64 - 1 : wave - 1;
+          for (int w0 = wv * 8; w0 < nd; w0 += NT / 8) {
+            const int w = w0 + (lane >> 3);
+            const bool pv = w < nd;
+            const int wq = pv ? w : 0;
+            int x, y;
+            if (all) {
+              pair_of(wq, x, y);
             } else {
-              r0 = lb0;                            // every rank but la0 and lb0
-              o = wq - (R - 1);
-              const int lo = la0 < lb0 ? la0 : lb0, hi = la0 < lb0 ? lb0 : la0;
-              if (o >= lo) ++o;
-              if (o >= hi) ++o;
+              int r0 = la0, o;
+              if (wq < R - 1) {
+                o = wq < la0 ? wq : wq + 1;        // every rank but la0
+              } else {
+                r0 = lb0;                          // every rank but la0 and lb0
+                o = wq - (R - 1);
+                const int lo = la0 < lb0 ? la0 : lb0, hi = la0 < lb0 ? lb0 : la0;
+                if (o >= lo) ++o;
+                if (o >= hi) ++o;
+              }
+              x = r0 < o ? r0 : o;
+              y = r0 < o ? o : r0;
             }
-            x = r0 < o ? r0 : o;
-            y = r0 < o ? o : r0;
-          }
-          const int k = y * (y - 1) / 2 + x;
-          int ra = 0, rb = 0;
-          PairCost pc;
-          const bool live = pv && pair_setup(x, y, ra, rb, pc);
-          const int64_t D = live ? sh.L[ra] - sh.L[rb] : 0;
-          // slot p of ra, and the S slots of rb, each read once (indices clamped into the rank)
-          const int sa = ra * S + (p < S ? p : S - 1);
-          const int ia = sh.item[sa];
-          const int64_t lia = sh.sload[sa];
-          const bool aok = live && p < S && !sh.mslot[sa] &&
-                           !(J > 1 && ia < V && holds(rb, ia));
-          // the cost of each admissible candidate (1 without a time budget; ~0 for the others), in
-          // registers for the passes, which read the destination slots again
-          uint64_t kc[kFrontS];
-          int64_t ba = 0;
-          if (a.timed && aok && ia < V) ba = sh.u.run.ebytes[J == 1 ? ia : expert_of(ia, E, inv_e)];
+            const int k = y * (y - 1) / 2 + x;
+            int ra = 0, rb = 0;
+            int64_t D = 0;
+            PairCost pc;
+            const bool live = pv && pair_setup(TIMED, x, y, ra, rb, D, pc);
+            // slot p of ra, and the S slots of rb (indices clamped into the rank)
+            const int sa = ra * S + (p < S ? p : S - 1), sb0 = rb * S;
+            const int ia = sh.item[sa];
+            const int64_t lia = sh.sload[sa];
+            bool aok = live && p < S && !sh.mslot[sa];
+            if constexpr (rep) aok = aok && !(ia < V && holds(rb, ia));
+            const int64_t ba = timed ? item_bytes(REP, ia) : 0;
+            // the destination slots are read in batches (one LDS wait each): without a time budget
+            // items, loads and moved flags once; with one, items and flags, then the sizes, and the
+            // items and loads again in every pass (the costs stay in registers)
+            int jv[kFrontS], lv[kFrontS];
+            bool mv[kFrontS];
 #pragma unroll
-          for (int q = 0; q < kFrontS; ++q) {
-            const int sb = rb * S + (q < S ? q : S - 1);
-            const int j = sh.item[sb];
-            bool ok = aok && q < S && !sh.mslot[sb] && !(ia >= V && j >= V) &&
-                      !(J > 1 && j < V && holds(ra, j));
-            uint64_t c = 1;
-            if (ok && a.timed) {
-              const int64_t bytes = ba + (j < V ? sh.u.run.ebytes[J == 1 ? j : expert_of(j, E, inv_e)] : 0);
-              const int64_t cc = pc.alpha + ceil_div(bytes * 1000, pc.beta, pc.inv_beta);
-              ok = cc <= pc.cap_ns;
-              c = (uint64_t)cc;
+            for (int q = 0; q < kFrontS; ++q) {
+              const int sb = sb0 + (q < S ? q : S - 1);
+              jv[q] = sh.item[sb];
+              mv[q] = sh.mslot[sb] != 0;
+              if constexpr (!timed) lv[q] = sh.sload[sb];
             }
-            kc[q] = ok ? c : ~0ull;
-          }
-          uint64_t climit = ~0ull;
-          int n = 0;
-          bool done = !live;
-          for (;;) {
-            uint64_t bu = ~0ull, bc = ~0ull, bt = ~0ull;   // tie keys of R <= 64 ranks are below ~0
-            int bpq = 0;
-            if (!done) {
+            uint32_t okm = 0;                    // bit q: candidate (p, q) is admissible
+#pragma unroll
+            for (int q = 0; q < kFrontS; ++q) {
+              bool ok = aok && q < S && !mv[q] && !(ia >= V && jv[q] >= V);
+              if constexpr (rep) ok = ok && !(jv[q] < V && holds(ra, jv[q]));
+              okm |= ok ? 1u << q : 0u;
+            }
+            uint64_t kc[kFrontS];                // costs (time budget)
+            if constexpr (timed) {
+              int64_t bv[kFrontS];
+#pragma unroll
+              for (int q = 0; q < kFrontS; ++q) bv[q] = item_bytes(REP, jv[q]);
 #pragma unroll
               for (int q = 0; q < kFrontS; ++q) {
-                const uint64_t c = kc[q];
-                if (c >= climit) continue;
-                const int64_t xd = D + 2 * ((int64_t)sh.sload[rb * S + q] - lia);
-                const uint64_t u = (uint64_t)(xd < 0 ? -xd : xd);
-                const uint64_t tk = tie_key(ra, rb, ia, sh.item[rb * S + q]);
-                if (u < bu || (u == bu && (c < bc || (c == bc && tk < bt)))) {
-                  bu = u; bc = c; bt = tk; bpq = p * S + q;
+                const int64_t cc = pc.alpha + ceil_div((ba + bv[q]) * 1000, pc.beta, pc.inv_beta);
+                if (cc > pc.cap_ns) okm &= ~(1u << q);
+                kc[q] = (uint64_t)cc;
+              }
+            }
+            uint64_t climit = ~0ull;
+            int n = 0;
+            bool done = !live;
+            for (;;) {
+              uint64_t bu = ~0ull, bc = ~0ull, bt = ~0ull;   // tie keys of R <= 64 ranks are below ~0
+              int bpq = 0;
+              if (!done) {
+                if constexpr (timed) {
+#pragma unroll
+                  for (int q = 0; q < kFrontS; ++q) {
+                    const int sb = sb0 + (q < S ? q : S - 1);
+                    jv[q] = sh.item[sb];
+                    lv[q] = sh.sload[sb];
+                  }
+                }
+#pragma unroll
+                for (int q = 0; q < kFrontS; ++q) {
+                  const uint64_t c = timed ? kc[q] : 1;
+                  const bool in = ((okm >> q) & 1) && c < climit;
+                  const int64_t xd = D + 2 * ((int64_t)lv[q] - lia);
+                  const uint64_t u = (uint64_t)(xd < 0 ? -xd : xd);
+                  const uint64_t tk = tie_key(ra, rb, ia, jv[q]);
+                  if (in && (u < bu || (u == bu && (c < bc || (c == bc && tk < bt))))) {
+                    bu = u; bc = c; bt = tk; bpq = p * S + q;
+                  }
                 }
               }
+              seg_min8(bu, bc, bt, bpq);
+              if (!done) {
+                if (bt == ~0ull) {
+                  done = true;
+                } else if (n == kFrontCap) {
+                  n = kFrontAll;
+                  done = true;
+                } else {
+                  if (p == 0) sh.fr_pt[k][n] = (uint8_t)bpq;
+                  ++n;
+                  climit = bc;
+                  done = !timed;
+                }
+              }
+              if (__ballot(!done) == 0) break;
             }
-            seg_min8(bu, bc, bt, bpq);
-            if (!done) {
-              if (bt == ~0ull) {
-                done = true;
-              } else if (n == kFrontCap) {
-                n = kFrontAll;
-                done = true;
-              } else {
-                if (p == 0) sh.fr_pt[k][n] = (uint8_t)bpq;
-                ++n;
-                climit = bc;
-                done = !a.timed;
+            if (pv && p == 0) sh.fr_n[k] = (uint8_t)n;
+          }
+        };
+        // score the stored candidates of every pair, one pair per thread
+        auto score = [&](auto REP, auto TIMED, int64_t Mf) {
+          for (int k = tid; k < R * (R - 1) / 2; k += NT) {
+            const int n = sh.fr_n[k];
+            if (n == 0) continue;
+            int x, y, ra, rb;
+            int64_t D;
+            pair_of(k, x, y);
+            PairCost pc;
+            if (!pair_setup(TIMED, x, y, ra, rb, D, pc)) continue;
+            int64_t other = INT64_MIN;
+            for (int t3 = 0; t3 < 3; ++t3) {
+              const int tr = sh.top[t3];
+              if (tr >= 0 && tr != ra && tr != rb) { other = sh.L[tr]; break; }
+            }
+            const int64_t La = sh.L[ra], Lb = sh.L[rb];
+            const int cnt = n == kFrontAll ? S * S : n;
+            for (int m = 0; m < cnt; ++m) {
+              const int pq = n == kFrontAll ? m : sh.fr_pt[k][m];
+              const int p = pq / S;
+              uint64_t c;
+              int64_t d;
+              int i, j;
+              if (!cand(REP, TIMED, ra, rb, p, pq - p * S, pc, c, d, i, j)) continue;
+              const int64_t la = La + d, lb = Lb - d;
+              int64_t m2 = la > lb ? la : lb;
+              if (other > m2) m2 = other;
+              const int64_t gain = g_den * (Mf - m2) + g_num * (2 * d * (Lb - La - d));
+              if (gain <= 0) continue;
+              const uint64_t tk = tie_key(ra, rb, i, j);
+              if constexpr (decltype(TIMED)::value) {
+                if (ratio_better((uint64_t)gain, c, tk, bgain, bcost, btie)) {
+                  bgain = (uint64_t)gain; bcost = c; btie = tk;
+                }
+              } else if ((uint64_t)gain > bgain || ((uint64_t)gain == bgain && tk < btie)) {
+                bgain = (uint64_t)gain; btie = tk;
               }
             }
-            if (__ballot(!done) == 0) break;
           }
-          if (pv && p == 0) sh.fr_n[k] = (uint8_t)n;
-        }
+        };
+        auto with_flags = [&](auto f) {
+          if (J > 1) {
+            if (a.timed) f(Flag<true>{}, Flag<true>{}); else f(Flag<true>{}, Flag<false>{});
+          } else {
+            if (a.timed) f(Flag<false>{}, Flag<true>{}); else f(Flag<false>{}, Flag<false>{});
+          }
+        };
+        with_flags(build);
         __syncthreads();                         // the frontiers and wave 0's extremes
         if (sh.stop) break;
         const int64_t Mf = sh.L[sh.amax];
-        // score the stored candidates of every pair, one pair per thread
-        for (int k = tid; k < R * (R - 1) / 2; k += NT) {
-          const int n = sh.fr_n[k];
-          if (n == 0) continue;
-          int x, y, ra, rb;
-          pair_of(k, x, y);
-          PairCost pc;
-          if (!pair_setup(x, y, ra, rb, pc)) continue;
-          int64_t other = INT64_MIN;
-          for (int t3 = 0; t3 < 3; ++t3) {
-            const int tr = sh.top[t3];
-            if (tr >= 0 && tr != ra && tr != rb) { other = sh.L[tr]; break; }
-          }
-          const int64_t La = sh.L[ra], Lb = sh.L[rb];
-          const int cnt = n == kFrontAll ? S * S : n;
-          for (int m = 0; m < cnt; ++m) {
-            const int pq = n == kFrontAll ? m : sh.fr_pt[k][m];
-            const int p = pq / S;
-            uint64_t u, c, tk;
-            int64_t d;
-            if (!cand(ra, rb, p, pq - p * S, pc, La - Lb, u, c, tk, d)) continue;
-            const int64_t la = La + d, lb = Lb - d;
-            int64_t m2 = la > lb ? la : lb;
-            if (other > m2) m2 = other;
-            const int64_t gain = g_den * (Mf - m2) + g_num * (2 * d * (Lb - La - d));
-            if (gain <= 0) continue;
-            if (a.timed) {
-              if (ratio_better((uint64_t)gain, c, tk, bgain, bcost, btie)) {
-                bgain = (uint64_t)gain; bcost = c; btie = tk;
-              }
-            } else if ((uint64_t)gain > bgain || ((uint64_t)gain == bgain && tk < btie)) {
-              bgain = (uint64_t)gain; btie = tk;
-            }
-          }
-        }
+        with_flags([&](auto REP, auto TIMED) { score(REP, TIMED, Mf); });
       }
     } else {
       // Full mode, in two phases.  Phase 1 scores every pair (amax, b); the best of those
