@@ -6,7 +6,7 @@
 // share of the admissible candidates with the exact integer benefit
 //     den * (M - M') + num * 2d (L_b - L_a - d),
 // the best candidate under (benefit desc, src rank, dst rank, item ids asc) is found with two
-// packed-key reductions, and thread 0 applies it.  State lives in LDS.
+// packed-key reductions, and wave 0 applies it.  State lives in LDS.
 //
 // The benefit fits an int64: the launcher checks den N + 4 num N^2 <= INT64_MAX once, and each
 // term and partial product is bounded by it (0 <= M' <= N, |d| <= N, |L_b - L_a - d| <= N).
@@ -17,7 +17,10 @@
 //     carry the item, its moved flag and its count so that a candidate costs one LDS round trip,
 //     and a round is a handful of wave reductions with no workgroup barrier.
 //   * plan_general<NT> for everything else (full mode, larger S, a time budget): state in LDS,
-//     threads split the candidates by rank pair, per-wave reductions combined through LDS.
+//     threads split the candidates by rank pair, per-wave reductions combined through LDS.  Full
+//     mode on up to 64 ranks of up to 8 slots with gamma > 0 keeps, per rank pair, the few
+//     candidates that can still be a round's best and rebuilds only the pairs of the previous
+//     swap; other full-mode tables score every pair under a benefit bound.
 //
 // Under a time budget (the cost form of the same section, Eq. 9-10 enforced per rank and per link)
 // every candidate also costs C = alpha + ceil(bytes * 1000 / beta) ns on its link, must fit what is
