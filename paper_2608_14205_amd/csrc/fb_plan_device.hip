@@ -631,6 +631,17 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
                 kc[q] = (uint64_t)cc;
               }
             }
+            // the group's cheapest admissible candidate: once a stored point costs that little, no
+            // candidate can cost less and the staircase is complete
+            uint64_t gmin = ~0ull;
+            if constexpr (timed) {
+#pragma unroll
+              for (int q = 0; q < kFrontS; ++q)
+                if (((okm >> q) & 1) && kc[q] < gmin) gmin = kc[q];
+              uint64_t z0 = 0, z1 = 0;
+              int zx = 0;
+              seg_min8(gmin, z0, z1, zx);
+            }
             uint64_t climit = ~0ull;
             int n = 0;
             bool done = !live;
@@ -669,7 +680,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
                   if (p == 0) sh.fr_pt[k][n] = (uint8_t)bpq;
                   ++n;
                   climit = bc;
-                  done = !timed;
+                  done = !timed || bc <= gmin;
                 }
               }
               if (__ballot(!done) == 0) break;
