@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define FB_ABI_VERSION 5
+#define FB_ABI_VERSION 6
 
 /* Status codes. */
 #define FB_OK 0
@@ -257,6 +257,31 @@ int fb_predict_plan_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
                            int32_t S, const fb_budget* budget, fb_swap* swaps, int32_t* n_swaps,
                            int32_t* new_slot_expert, int32_t* new_expert_to_rank,
                            int64_t* new_rank_loads, int32_t* status, void* stream);
+
+/* fb_predict_plan_packed under a time budget: the prediction, then the plan of its counts as
+ * fb_plan_swaps_timed_device would make it (every candidate costed by Eq. 9 on its link type and
+ * admitted against the per-rank and per-link budgets of Eq. 10, ranked by benefit / cost).  In
+ * frontier mode on at most 64 ranks with S * S <= 128 the plan is made inside the predictor's last
+ * workgroup; any other plan runs as its own kernel on the same stream.  Results are identical to
+ * fb_predict_load_packed followed by fb_plan_swaps_timed_device.
+ *   hidden ... workspace_bytes   as in fb_predict_load_packed (no debug outputs).
+ *   counts                       device int32[E] out: the predicted counts, then the planner's
+ *                                input.
+ *   slot_expert ... status       as in fb_plan_swaps_timed_device (device arrays; budget and cost
+ *                                host structs read during the call), with this call's E and R.
+ * Errors: every argument error of either call, checked on the host before anything runs. */
+int fb_predict_plan_timed_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                                 int32_t dtype, const void* router_packed,
+                                 size_t router_packed_bytes, int32_t E, const float* logit_bias,
+                                 const float* select_bias, const fb_scoring* scoring,
+                                 const int32_t* expert_to_rank, int32_t R, int32_t* counts,
+                                 int32_t* rank_loads, double* max_mean, void* workspace,
+                                 size_t workspace_bytes, const int32_t* slot_expert, int32_t S,
+                                 const fb_budget* budget, const fb_cost_model* cost,
+                                 const int32_t* rank_node, const int64_t* expert_bytes,
+                                 fb_swap* swaps, int64_t* swap_cost_ns, int32_t* n_swaps,
+                                 int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                                 int64_t* new_rank_loads, int32_t* status, void* stream);
 
 /* fb_predict_load_packed for callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation): no workspace argument, no allocation.  The

@@ -16,7 +16,7 @@ FB_OK, FB_EINVAL, FB_EUNSUPPORTED, FB_EDEVICE, FB_ENOSPC = 0, -1, -2, -3, -4
 FB_BF16, FB_F32 = 0, 1
 FB_SOFTMAX, FB_SIGMOID = 0, 1
 FB_FRONTIER, FB_FULL = 0, 1
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 
 class fb_scoring(ctypes.Structure):
@@ -69,6 +69,12 @@ SIGNATURES = {
                                               _VP, _VP, _VP, _SZ, _VP, _I32,
                                               ctypes.POINTER(fb_budget), _VP, _VP, _VP, _VP, _VP,
                                               _VP, _VP]),
+    "fb_predict_plan_timed_packed": (ctypes.c_int, [_VP, _I64, _I32, _I64, _I32, _VP, _SZ, _I32,
+                                                    _VP, _VP, ctypes.POINTER(fb_scoring), _VP, _I32,
+                                                    _VP, _VP, _VP, _VP, _SZ, _VP, _I32,
+                                                    ctypes.POINTER(fb_budget),
+                                                    ctypes.POINTER(fb_cost_model), _VP, _VP, _VP,
+                                                    _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "fb_predict_load_packed_noalloc": (ctypes.c_int, [_VP, _I64, _I32, _I64, _I32, _VP, _SZ, _I32,
                                                       _VP, _VP, ctypes.POINTER(fb_scoring), _VP,
                                                       _I32, _VP, _VP, _VP, _VP, _VP, _VP]),

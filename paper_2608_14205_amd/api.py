@@ -283,11 +283,13 @@ class Predictor:
     def predict_plan(self, hidden: torch.Tensor, router: PackedRouter, scoring: Scoring,
                      expert_to_rank: torch.Tensor, slots: torch.Tensor, budget: Budget, *,
                      logit_bias=None, select_bias=None, out: Optional[Prediction] = None,
-                     plan: Optional[DevicePlan] = None,
+                     plan: Optional[DevicePlan] = None, cost: Optional[CostModel] = None,
                      stream: Optional[torch.cuda.Stream] = None):
-        """fb_predict_plan_packed: the prediction and the swap plan of its counts in one call
-        (the plan inside the predictor's last workgroup where the one-wave planner serves it).
-        slots is the int32[R, S] placement; returns (Prediction, DevicePlan)."""
+        """fb_predict_plan_packed (fb_predict_plan_timed_packed with a cost model): the prediction
+        and the swap plan of its counts in one call (the plan inside the predictor's last workgroup
+        where the one-wave planner serves it).  slots is the int32[R, S] placement; the cost
+        model's node ids and expert sizes as in plan_swaps_timed_device.  Returns (Prediction,
+        DevicePlan)."""
         if not isinstance(router, PackedRouter):
             raise ValueError("predict_plan takes a packed router (pack_router_weight)")
         if hidden.dim() != 2 or (hidden.numel() > 0 and hidden.stride(1) != 1):
@@ -321,26 +323,39 @@ class Predictor:
             out = Prediction(torch.empty(E, dtype=torch.int32, device=dev),
                              torch.empty(R, dtype=torch.int32, device=dev),
                              torch.empty(1, dtype=torch.float64, device=dev))
+        cap = max(budget.max_swaps, 1)
         if plan is None:
-            plan = DevicePlan(torch.empty(max(budget.max_swaps, 1) * SWAP_BYTES, dtype=torch.uint8,
-                                          device=dev),
+            plan = DevicePlan(torch.empty(cap * SWAP_BYTES, dtype=torch.uint8, device=dev),
                               torch.empty(1, dtype=torch.int32, device=dev),
                               torch.empty((R, S), dtype=torch.int32, device=dev),
                               torch.empty(E, dtype=torch.int32, device=dev),
                               torch.empty(R, dtype=torch.int64, device=dev),
-                              torch.empty(1, dtype=torch.int32, device=dev))
+                              torch.empty(1, dtype=torch.int32, device=dev),
+                              None if cost is None else torch.zeros(cap, dtype=torch.int64, device=dev))
         sc = scoring.to_c()
         bg = budget.to_c()
         ld = hidden.stride(0) if T > 0 else H
-        with torch.cuda.device(dev):
-            st = lib.fb_predict_plan_packed(
-                _ptr(hidden), T, H, ld, code, _ptr(router.data), router.data.numel(), E,
+        head = (_ptr(hidden), T, H, ld, code, _ptr(router.data), router.data.numel(), E,
                 _ptr(logit_bias), _ptr(select_bias), ctypes.byref(sc), _ptr(expert_to_rank), R,
                 _ptr(out.counts), _ptr(out.rank_loads), _ptr(out.max_mean), _ptr(self.workspace),
-                self.workspace.numel(), slots.data_ptr(), S, ctypes.byref(bg), plan.swaps.data_ptr(),
-                plan.n_swaps.data_ptr(), plan.slots.data_ptr(), plan.expert_to_rank.data_ptr(),
+                self.workspace.numel(), slots.data_ptr(), S, ctypes.byref(bg))
+        tail = (plan.n_swaps.data_ptr(), plan.slots.data_ptr(), plan.expert_to_rank.data_ptr(),
                 plan.rank_loads.data_ptr(), plan.status.data_ptr(), _stream_handle(dev, stream))
-        L.check(st, "fb_predict_plan_packed")
+        if cost is None:
+            with torch.cuda.device(dev):
+                st = lib.fb_predict_plan_packed(*head, plan.swaps.data_ptr(), *tail)
+            L.check(st, "fb_predict_plan_packed")
+            return out, plan
+        nodes = torch.as_tensor(cost.rank_node, dtype=torch.int32, device=dev).contiguous()
+        nbytes = torch.as_tensor(cost.expert_bytes, dtype=torch.int64, device=dev).contiguous()
+        if nodes.numel() != R or nbytes.numel() != E:
+            raise ValueError("cost model does not match the placement")
+        cm = cost.to_c()
+        with torch.cuda.device(dev):
+            st = lib.fb_predict_plan_timed_packed(*head, ctypes.byref(cm), nodes.data_ptr(),
+                                                  nbytes.data_ptr(), plan.swaps.data_ptr(),
+                                                  _ptr(plan.costs), *tail)
+        L.check(st, "fb_predict_plan_timed_packed")
         return out, plan
 
 

@@ -249,6 +249,46 @@ fb::PlanDeviceLaunch make_plan_launch(const int32_t* counts, int32_t E, const in
   return a;
 }
 
+// The time budget of a device plan on top of the swap-count planner's arguments: FB_OK with the
+// cost model resolved (a link budget of -1 becomes the rank budget), or the status to return.
+int check_plan_timed(const fb_budget* budget, const fb_cost_model* cost, const int32_t* rank_node,
+                     const int64_t* expert_bytes, fb_cost_model* resolved) {
+  if (!cost || !rank_node || !expert_bytes) return FB_EINVAL;
+  if (budget->max_swaps > fb::kMaxTimedSwaps) return FB_EUNSUPPORTED;
+  fb_cost_model m = *cost;
+  if (m.rank_budget_ns < 0 || m.link_budget_ns < -1) return FB_EINVAL;
+  for (int t = 0; t < 2; ++t)
+    if (m.alpha_ns[t] < 1 || m.alpha_ns[t] > fb::kCostLimit || m.beta_bytes_per_us[t] < 1 ||
+        m.beta_bytes_per_us[t] > fb::kCostLimit)
+      return FB_EINVAL;
+  if (m.link_budget_ns < 0) m.link_budget_ns = m.rank_budget_ns;
+  *resolved = m;
+  return FB_OK;
+}
+
+void set_timed(fb::PlanDeviceLaunch& a, const fb_cost_model& m, const int32_t* rank_node,
+               const int64_t* expert_bytes, int64_t* swap_cost_ns) {
+  a.timed = 1;
+  a.cost = m;
+  a.rank_node = rank_node;
+  a.expert_bytes = expert_bytes;
+  a.swap_cost_ns = swap_cost_ns;
+}
+
+// The prediction, then the plan of its counts: the one-wave planner runs in the predictor's last
+// workgroup when it serves the plan; any other plan follows as a kernel of its own on the stream.
+int predict_then_plan(fb::PredictLaunch& a, const fb::PlanDeviceLaunch& p, size_t workspace_bytes) {
+  const size_t sb = fb::split_workspace_bytes(a.T, a.E, a.H, a.dtype, a.num_cus);
+  if (sb > 0 && workspace_bytes >= fb::kWsBytes + sb) {
+    a.partial = reinterpret_cast<float*>(static_cast<char*>(a.workspace) + fb::kWsBytes);
+    a.partial_bytes = workspace_bytes - fb::kWsBytes;
+  }
+  if (fb::plan_fusable(p)) a.plan = &p;
+  const int lc = fb::launch_predict(a);
+  if (lc != FB_OK || a.plan != nullptr) return lc;
+  return fb::launch_plan_device(p);
+}
+
 }  // namespace
 
 extern "C" {
@@ -328,20 +368,47 @@ int fb_predict_plan_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_
   fb::PredictLaunch a = make_launch(hidden, T, H, ld_hidden, dtype, router_packed, E, logit_bias,
                                     select_bias, scoring, expert_to_rank, R, counts, rank_loads,
                                     max_mean, workspace, nullptr, nullptr, stream);
-  const size_t sb = fb::split_workspace_bytes(T, E, H, dtype, a.num_cus);
-  if (sb > 0 && workspace_bytes >= fb::kWsBytes + sb) {
-    a.partial = reinterpret_cast<float*>(static_cast<char*>(workspace) + fb::kWsBytes);
-    a.partial_bytes = workspace_bytes - fb::kWsBytes;
-  }
   const fb::PlanDeviceLaunch p = make_plan_launch(counts, E, slot_expert, R, S, *budget, swaps,
                                                   n_swaps, new_slot_expert, new_expert_to_rank,
                                                   new_rank_loads, status, stream);
-  // the one-wave planner runs in the predictor's last workgroup; any other plan follows as a
-  // kernel of its own on the same stream
-  if (fb::plan_fusable(p)) a.plan = &p;
-  const int lc = fb::launch_predict(a);
-  if (lc != FB_OK || a.plan != nullptr) return lc;
-  return fb::launch_plan_device(p);
+  return predict_then_plan(a, p, workspace_bytes);
+}
+
+int fb_predict_plan_timed_packed(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
+                                 int32_t dtype, const void* router_packed,
+                                 size_t router_packed_bytes, int32_t E, const float* logit_bias,
+                                 const float* select_bias, const fb_scoring* scoring,
+                                 const int32_t* expert_to_rank, int32_t R, int32_t* counts,
+                                 int32_t* rank_loads, double* max_mean, void* workspace,
+                                 size_t workspace_bytes, const int32_t* slot_expert, int32_t S,
+                                 const fb_budget* budget, const fb_cost_model* cost,
+                                 const int32_t* rank_node, const int64_t* expert_bytes,
+                                 fb_swap* swaps, int64_t* swap_cost_ns, int32_t* n_swaps,
+                                 int32_t* new_slot_expert, int32_t* new_expert_to_rank,
+                                 int64_t* new_rank_loads, int32_t* status, void* stream) {
+  if (!router_packed) return FB_EINVAL;
+  const int vc = check_predict(hidden, T, H, ld_hidden, dtype, E, select_bias, scoring,
+                               expert_to_rank, R, counts, rank_loads, max_mean, workspace,
+                               workspace_bytes, fb::kWsBytes);
+  if (vc != FB_OK) return vc;
+  const int pc = check_plan_device(E, slot_expert, R, S, budget, swaps, n_swaps, new_slot_expert,
+                                   new_expert_to_rank, new_rank_loads, status);
+  if (pc != FB_OK) return pc;
+  fb_cost_model m;
+  const int tc = check_plan_timed(budget, cost, rank_node, expert_bytes, &m);
+  if (tc != FB_OK) return tc;
+  if (!aligned16(router_packed)) return FB_EUNSUPPORTED;
+  if (router_packed_bytes < fb::router_packed_bytes(E, H, dtype)) return FB_ENOSPC;
+  const int dc = fb::check_device();
+  if (dc != FB_OK) return dc;
+  fb::PredictLaunch a = make_launch(hidden, T, H, ld_hidden, dtype, router_packed, E, logit_bias,
+                                    select_bias, scoring, expert_to_rank, R, counts, rank_loads,
+                                    max_mean, workspace, nullptr, nullptr, stream);
+  fb::PlanDeviceLaunch p = make_plan_launch(counts, E, slot_expert, R, S, *budget, swaps, n_swaps,
+                                            new_slot_expert, new_expert_to_rank, new_rank_loads,
+                                            status, stream);
+  set_timed(p, m, rank_node, expert_bytes, swap_cost_ns);
+  return predict_then_plan(a, p, workspace_bytes);
 }
 
 int fb_predict_load_packed_noalloc(const void* hidden, int64_t T, int32_t H, int64_t ld_hidden,
@@ -405,46 +472,19 @@ int fb_plan_swaps_timed_device(const int32_t* counts, int32_t E, const int32_t* 
                                int32_t* n_swaps, int32_t* new_slot_expert,
                                int32_t* new_expert_to_rank, int64_t* new_rank_loads,
                                int32_t* status, void* stream) {
-  if (!counts || !slot_expert || !budget || !cost || !rank_node || !expert_bytes || !n_swaps ||
-      !new_slot_expert || !new_expert_to_rank || !new_rank_loads || !status)
-    return FB_EINVAL;
-  if (E < 1 || R < 1 || S < 1) return FB_EINVAL;
-  if (R > FB_MAX_RANKS || (int64_t)R * S > FB_MAX_SLOTS_TOTAL) return FB_EUNSUPPORTED;
-  if (E > R * S) return FB_EINVAL;
-  const fb_budget bg = *budget;
-  if (bg.max_swaps < 0 || bg.per_rank_cap < 0 || bg.tau < 0 || bg.gamma_num < 0 || bg.gamma_den < 0)
-    return FB_EINVAL;
-  if (bg.mode != FB_FRONTIER && bg.mode != FB_FULL) return FB_EINVAL;
-  if (bg.max_swaps > 0 && !swaps) return FB_EINVAL;
-  if (bg.max_swaps > fb::kMaxTimedSwaps) return FB_EUNSUPPORTED;
-  fb_cost_model m = *cost;
-  if (m.rank_budget_ns < 0 || m.link_budget_ns < -1) return FB_EINVAL;
-  for (int t = 0; t < 2; ++t)
-    if (m.alpha_ns[t] < 1 || m.alpha_ns[t] > fb::kCostLimit || m.beta_bytes_per_us[t] < 1 ||
-        m.beta_bytes_per_us[t] > fb::kCostLimit)
-      return FB_EINVAL;
-  if (m.link_budget_ns < 0) m.link_budget_ns = m.rank_budget_ns;
+  if (!counts) return FB_EINVAL;
+  const int vc = check_plan_device(E, slot_expert, R, S, budget, swaps, n_swaps, new_slot_expert,
+                                   new_expert_to_rank, new_rank_loads, status);
+  if (vc != FB_OK) return vc;
+  fb_cost_model m;
+  const int tc = check_plan_timed(budget, cost, rank_node, expert_bytes, &m);
+  if (tc != FB_OK) return tc;
   const int dc = fb::check_device();
   if (dc != FB_OK) return dc;
-  fb::PlanDeviceLaunch a;
-  a.counts = counts;
-  a.E = E;
-  a.slot_expert = slot_expert;
-  a.R = R;
-  a.S = S;
-  a.budget = bg;
-  a.swaps = swaps;
-  a.n_swaps = n_swaps;
-  a.new_slot_expert = new_slot_expert;
-  a.new_expert_to_rank = new_expert_to_rank;
-  a.new_rank_loads = new_rank_loads;
-  a.status = status;
-  a.stream = stream;
-  a.timed = 1;
-  a.cost = m;
-  a.rank_node = rank_node;
-  a.expert_bytes = expert_bytes;
-  a.swap_cost_ns = swap_cost_ns;
+  fb::PlanDeviceLaunch a = make_plan_launch(counts, E, slot_expert, R, S, *budget, swaps, n_swaps,
+                                            new_slot_expert, new_expert_to_rank, new_rank_loads,
+                                            status, stream);
+  set_timed(a, m, rank_node, expert_bytes, swap_cost_ns);
   return fb::launch_plan_device(a);
 }
 

@@ -34,8 +34,8 @@ struct PredictLaunch {
   int32_t num_cus;    // compute units of the device (tile-height choice)
   float* partial;     // split mode: partial-logit buffer in the workspace, or NULL
   size_t partial_bytes;
-  // the swap plan of the counts, made in the predictor's last workgroup (frontier mode, swap-count
-  // budget, R <= 64, S * S <= 128; see plan_fusable), or NULL
+  // the swap plan of the counts, made in the predictor's last workgroup (frontier mode, R <= 64,
+  // S * S <= 128; see plan_fusable), or NULL
   const PlanDeviceLaunch* plan;
 };
 // Bytes of partial logits the split mode needs for a batch (0: that batch runs fused).
@@ -92,10 +92,11 @@ struct PlanDeviceLaunch {
 constexpr int kMaxTimedSwaps = 1024;           // swap cap of the device planner under a time budget
 constexpr int64_t kCostLimit = (int64_t)1 << 40;  // alpha, beta and expert sizes
 int launch_plan_device(const PlanDeviceLaunch& a);
-// Whether the one-wave planner serves this plan, so that it can run inside the predictor's last
-// workgroup: a swap-count budget in frontier mode, R <= 64 and S * S <= 128.
+// Whether the one-wave planner serves this plan with one rank per lane, so that it can run inside
+// the predictor's last workgroup: frontier mode (swap-count or time budget), R <= 64 and
+// S * S <= 128.
 inline bool plan_fusable(const PlanDeviceLaunch& a) {
-  return !a.timed && a.budget.mode == FB_FRONTIER && a.R <= 64 && (int64_t)a.S * a.S <= 128;
+  return a.budget.mode == FB_FRONTIER && a.R <= 64 && (int64_t)a.S * a.S <= 128;
 }
 
 // Prediction-quality diagnostics (fb_quality.hip).

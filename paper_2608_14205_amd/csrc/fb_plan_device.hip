@@ -12,11 +12,12 @@
 // term and partial product is bounded by it (0 <= M' <= N, |d| <= N, |L_b - L_a - d| <= N).
 //
 // Two kernels:
-//   * plan_frontier_wave, one wave, for frontier mode with S * S <= 128 (the common case).  Rank
-//     loads live in registers (ranks lane + 64 m), each lane owns one or two candidates (p, q), slot entries
-//     carry the item, its moved flag and its count so that a candidate costs one LDS round trip,
-//     and a round is a handful of wave reductions with no workgroup barrier.
-//   * plan_general<NT> for everything else (full mode, larger S, a time budget): state in LDS,
+//   * plan_frontier_wave, one wave, for frontier mode with S * S <= 128 (the common case; under a
+//     time budget up to 64 ranks).  Rank loads live in registers (ranks lane + 64 m), each lane
+//     owns one or two candidates (p, q), slot entries carry the item, its moved flag and its count
+//     so that a candidate costs one LDS round trip, and a round is a handful of wave reductions
+//     with no workgroup barrier.
+//   * plan_general<NT> for everything else (full mode, larger S, a time budget on more ranks): state in LDS,
 //     threads split the candidates by rank pair, per-wave reductions combined through LDS.  Full
 //     mode on up to 64 ranks of up to 8 slots with gamma > 0 keeps, per rank pair, the few
 //     candidates that can still be a round's best and rebuilds only the pairs of the previous
@@ -111,17 +112,6 @@ struct SharedT {
   int64_t acc_cost[kMaxTimedSwaps];
 };
 
-// ceil(num / beta) for 0 <= num < 2^52 and 1 <= beta <= 2^40, exactly: a double-precision
-// quotient is within one of the truncated one (its relative error is below 2^-51), and one
-// integer correction step settles it.
-__device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t beta, double inv_beta) {
-  int64_t q = (int64_t)((double)num * inv_beta);
-  int64_t r = num - q * beta;
-  if (r < 0) { q -= 1; r += beta; }
-  if (r >= beta) { q += 1; r -= beta; }
-  return q + (r > 0 ? 1 : 0);
-}
-
 // Eq. 9 in whole nanoseconds for a swap moving expert ei off rank ra and expert ej off rank rb
 // (-1: an empty slot, which transfers nothing).
 template <class SH>
@@ -184,47 +174,6 @@ __device__ __forceinline__ void pair_of(int k, int& x, int& y) {
   while ((b + 1) * b / 2 <= k) ++b;
   y = b;
   x = k - b * (b - 1) / 2;
-}
-
-// (gain, cost, tie) ordering of the time-budgeted planner; gain 0 means "no candidate".
-__device__ __forceinline__ bool ratio_better(uint64_t g1, uint64_t c1, uint64_t t1, uint64_t g2,
-                                             uint64_t c2, uint64_t t2) {
-  if (g1 == 0) return false;
-  if (g2 == 0) return true;
-  // the products in double precision decide unless they are within 2^-30 of each other (their
-  // relative rounding error is below 2^-51); only then the exact 128-bit products are formed
-  const double ld = (double)g1 * (double)c2, rd = (double)g2 * (double)c1;
-  const double tol = 0x1p-30 * (ld > rd ? ld : rd);
-  if (ld - rd > tol) return true;
-  if (rd - ld > tol) return false;
-  const unsigned __int128 l = (unsigned __int128)g1 * c2, r = (unsigned __int128)g2 * c1;
-  if (l != r) return l > r;
-  return t1 < t2;
-}
-
-// One step of the time-budgeted reduction (the better (gain, cost, tie) by ratio_better) with the
-// lane that DPP control CTRL names.
-template <int CTRL>
-__device__ __forceinline__ void ratio_step(uint64_t& g, uint64_t& c, uint64_t& t) {
-  const uint64_t g2 = dpp_u64<CTRL>(g), c2 = dpp_u64<CTRL>(c), t2 = dpp_u64<CTRL>(t);
-  if (ratio_better(g2, c2, t2, g, c, t)) { g = g2; c = c2; t = t2; }
-}
-
-// Best (gain, cost, tie) of the wave by ratio_better (every lane takes part; uniform result): each
-// row of 16 lanes by DPP (lane ^ 1, lane ^ 2, the mirror within 8 lanes, the mirror within 16),
-// then the four rows.
-__device__ __forceinline__ void wave_best_ratio(uint64_t& g, uint64_t& c, uint64_t& t) {
-  ratio_step<0xB1>(g, c, t);
-  ratio_step<0x4E>(g, c, t);
-  ratio_step<0x141>(g, c, t);
-  ratio_step<0x140>(g, c, t);
-  uint64_t bg = readlane_u64(g, 0), bc = readlane_u64(c, 0), bt = readlane_u64(t, 0);
-#pragma unroll
-  for (int r = 1; r < 4; ++r) {
-    const uint64_t og = readlane_u64(g, 16 * r), oc = readlane_u64(c, 16 * r), ot = readlane_u64(t, 16 * r);
-    if (ratio_better(og, oc, ot, bg, bc, bt)) { bg = og; bc = oc; bt = ot; }
-  }
-  g = bg; c = bc; t = bt;
 }
 
 // NT threads (256: frontier mode, 1024: full mode); SMALL: tables of at most kSmallRS slots and
@@ -1013,8 +962,9 @@ __global__ __launch_bounds__(64, 1) void plan_frontier_wave(PlanDeviceLaunch a) 
 int launch_plan_device(const PlanDeviceLaunch& a) {
   (void)hipGetLastError();
   hipStream_t st = static_cast<hipStream_t>(a.stream);
-  if (!a.timed && a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 128) {
-    // the routing below keeps R * S within the chosen kernel's slot capacity
+  if (a.budget.mode == FB_FRONTIER && (int64_t)a.S * a.S <= 128 && (!a.timed || a.R <= 64)) {
+    // the routing below keeps R * S within the chosen kernel's slot capacity (time budgets: one
+    // rank per lane)
     const int rpl = a.R <= 64 ? 1 : a.R <= 128 ? 2 : a.R <= 256 ? 4 : 16;
     if ((int64_t)a.R * a.S > wave_cap(rpl, (int64_t)a.S * a.S <= 64 ? 1 : 2)) return FB_EUNSUPPORTED;
     if ((int64_t)a.S * a.S <= 64) {

@@ -181,6 +181,59 @@ __device__ __forceinline__ int32_t replica_share(int x, const int32_t* counts, c
   if (k == 1) return n;
   return n / k + (j < n % k ? 1 : 0);
 }
+// ---- time budget: costs and the benefit / cost order (both planners) -------------------------
+// ceil(num / beta) for 0 <= num < 2^52 and 1 <= beta <= 2^40, exactly: a double-precision
+// quotient is within one of the truncated one (its relative error is below 2^-51), and one
+// integer correction step settles it.
+__device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t beta, double inv_beta) {
+  int64_t q = (int64_t)((double)num * inv_beta);
+  int64_t r = num - q * beta;
+  if (r < 0) { q -= 1; r += beta; }
+  if (r >= beta) { q += 1; r -= beta; }
+  return q + (r > 0 ? 1 : 0);
+}
+
+// (gain, cost, tie) ordering of the time-budgeted planner; gain 0 means "no candidate".
+__device__ __forceinline__ bool ratio_better(uint64_t g1, uint64_t c1, uint64_t t1, uint64_t g2,
+                                             uint64_t c2, uint64_t t2) {
+  if (g1 == 0) return false;
+  if (g2 == 0) return true;
+  // the products in double precision decide unless they are within 2^-30 of each other (their
+  // relative rounding error is below 2^-51); only then the exact 128-bit products are formed
+  const double ld = (double)g1 * (double)c2, rd = (double)g2 * (double)c1;
+  const double tol = 0x1p-30 * (ld > rd ? ld : rd);
+  if (ld - rd > tol) return true;
+  if (rd - ld > tol) return false;
+  const unsigned __int128 l = (unsigned __int128)g1 * c2, r = (unsigned __int128)g2 * c1;
+  if (l != r) return l > r;
+  return t1 < t2;
+}
+
+// One step of the time-budgeted reduction (the better (gain, cost, tie) by ratio_better) with the
+// lane that DPP control CTRL names.
+template <int CTRL>
+__device__ __forceinline__ void ratio_step(uint64_t& g, uint64_t& c, uint64_t& t) {
+  const uint64_t g2 = dpp_u64<CTRL>(g), c2 = dpp_u64<CTRL>(c), t2 = dpp_u64<CTRL>(t);
+  if (ratio_better(g2, c2, t2, g, c, t)) { g = g2; c = c2; t = t2; }
+}
+
+// Best (gain, cost, tie) of the wave by ratio_better (every lane takes part; uniform result): each
+// row of 16 lanes by DPP (lane ^ 1, lane ^ 2, the mirror within 8 lanes, the mirror within 16),
+// then the four rows.
+__device__ __forceinline__ void wave_best_ratio(uint64_t& g, uint64_t& c, uint64_t& t) {
+  ratio_step<0xB1>(g, c, t);
+  ratio_step<0x4E>(g, c, t);
+  ratio_step<0x141>(g, c, t);
+  ratio_step<0x140>(g, c, t);
+  uint64_t bg = readlane_u64(g, 0), bc = readlane_u64(c, 0), bt = readlane_u64(t, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    const uint64_t og = readlane_u64(g, 16 * r), oc = readlane_u64(c, 16 * r), ot = readlane_u64(t, 16 * r);
+    if (ratio_better(og, oc, ot, bg, bc, bt)) { bg = og; bc = oc; bt = ot; }
+  }
+  g = bg; c = bc; t = bt;
+}
+
 // ---- one-wave frontier planner ------------------------------------------------------------------
 constexpr uint32_t kMovedBit = 0x80000000u;
 
@@ -321,29 +374,46 @@ constexpr int wave_cap(int RPL, int CPL) {
 
 // LDS of the one-wave planner, provided by the caller: vals, cnt, ej, reps, base and flag hold at
 // least wave_cap(RPL, CPL) entries, slot as many (8-byte aligned), part 64 * RPL; bad and jmax one
-// word each.
+// word each.  With one rank per lane (RPL 1) the planner also takes time budgets: ebytes holds the
+// expert sizes (as many entries as slots), acc_pair and acc_cost the link and cost of every
+// accepted swap (kMaxTimedSwaps); NULL otherwise.
 struct PlanWaveLds {
   int32_t *vals, *cnt, *ej, *reps, *base, *flag;
   uint2* slot;
   int32_t* part;
   int32_t *bad, *jmax;
+  int64_t* ebytes;
+  int64_t* acc_cost;
+  int32_t* acc_pair;
 };
 
 // Bytes of PlanWaveLds for CAP slots and RPL ranks per lane, laid out as plan_wave_lds carves them.
 constexpr size_t plan_wave_lds_bytes(int CAP, int RPL) {
-  return (size_t)CAP * 8 + (size_t)CAP * 4 * 6 + (size_t)64 * RPL * 4 + 8;
+  return (size_t)CAP * 8 + (RPL == 1 ? (size_t)CAP * 8 + (size_t)kMaxTimedSwaps * 12 : 0) +
+         (size_t)CAP * 4 * 6 + (size_t)64 * RPL * 4 + 8;
 }
 // Carves PlanWaveLds out of `mem` (8-byte aligned, plan_wave_lds_bytes(CAP, RPL) bytes).
 __device__ __forceinline__ PlanWaveLds plan_wave_lds(char* mem, int CAP, int RPL) {
   PlanWaveLds l;
   l.slot = reinterpret_cast<uint2*>(mem);
-  int32_t* w = reinterpret_cast<int32_t*>(mem + (size_t)CAP * 8);
+  char* m = mem + (size_t)CAP * 8;
+  l.ebytes = nullptr;
+  l.acc_cost = nullptr;
+  l.acc_pair = nullptr;
+  if (RPL == 1) {
+    l.ebytes = reinterpret_cast<int64_t*>(m);
+    m += (size_t)CAP * 8;
+    l.acc_cost = reinterpret_cast<int64_t*>(m);
+    m += (size_t)kMaxTimedSwaps * 8;
+  }
+  int32_t* w = reinterpret_cast<int32_t*>(m);
   l.vals = w; w += CAP;
   l.cnt = w; w += CAP;
   l.ej = w; w += CAP;
   l.reps = w; w += CAP;
   l.base = w; w += CAP;
   l.flag = w; w += CAP;
+  if (RPL == 1) { l.acc_pair = w; w += kMaxTimedSwaps; }
   l.part = w; w += 64 * RPL;
   l.bad = w; l.jmax = w + 1;
   return l;
@@ -352,6 +422,9 @@ __device__ __forceinline__ PlanWaveLds plan_wave_lds(char* mem, int CAP, int RPL
 // RPL: ranks per lane (R <= 64 * RPL); rank r lives in lane r % 64, register r / 64.
 // CPL: candidates per lane, 1 for S * S <= 64, 2 for S * S <= 128.
 // Runs in the first wave of its workgroup (threadIdx.x < 64); the caller's other waves take no part.
+// Time budgets (a.timed) need RPL 1: every candidate between the two frontier ranks is costed by
+// Eq. 9 on their link, admitted if it fits what is left of both ranks' and of the link's budgets,
+// and the round's best is the largest benefit / cost, then the tie key.
 template <int RPL, int CPL>
 __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds) {
   int32_t* const vals = lds.vals;      // the input tables
@@ -367,11 +440,21 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
   const int lane = threadIdx.x;
   const int E = a.E, R = a.R, S = a.S, RS = R * S;
   const fb_budget bg = a.budget;
+  const bool timed = RPL == 1 && a.timed;
+  int64_t* const ebytes = lds.ebytes;
+  const float inv_e = 1.0f / (float)E;
 
-  // both input tables are fetched before the first wait
-  for (int e = lane; e < E; e += 64) { cnt[e] = a.counts[e]; reps[e] = 0; }
+  // every input table is fetched before the first wait
+  for (int e = lane; e < E; e += 64) {
+    cnt[e] = a.counts[e];
+    reps[e] = 0;
+    if (timed) ebytes[e] = a.expert_bytes[e];
+  }
   for (int c = lane; c < RS; c += 64) vals[c] = a.slot_expert[c];
   for (int r = lane; r < R; r += 64) part[r] = 0;
+  // time budget: rank `lane`'s node and what is left of its budget
+  const int32_t node_r = timed && lane < R ? a.rank_node[lane] : 0;
+  int64_t left_r = a.cost.rank_budget_ns;
   plan_sync<64>();
   // short check of a plain placement (every expert exactly once); a replica (a value >= E) sends the
   // table to the full check
@@ -392,6 +475,8 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
   } else {
     for (int e = lane; e < E; e += 64) bad |= (reps[e] != 1) | (cnt[e] < 0);
   }
+  if (timed)
+    for (int e = lane; e < E; e += 64) bad |= (ebytes[e] < 0) | (ebytes[e] > kCostLimit);
   const int V = E * J;               // slot values are below V; empty-slot ids from V
   const bool any_bad = __ballot(bad) != 0;
   if (any_bad || (int64_t)V + RS > ((int64_t)1 << kItemBits)) {
@@ -439,7 +524,7 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
   const bool active = N > 0 && bg.max_swaps > 0 && R > 1;
   bool small_done = false;
   if constexpr (RPL == 1) {
-    if (active && N < (int64_t)0x7fffffff && J == 1) {
+    if (active && N < (int64_t)0x7fffffff && J == 1 && !timed) {
       uint32_t Lu = (uint32_t)Lr[0];
       ns = rounds_small<CPL>(a, slot, part, Lu, g_num, g_den);
       Lr[0] = Lu;
@@ -471,7 +556,31 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
     ko = wave_max_u64(ko);
     const int64_t other = ko ? (int64_t)ko - 1 : INT64_MIN;
 
-    uint64_t gk = 0, tk = 0;
+    // time budget: the pair's link and the most a candidate may cost there
+    int64_t alpha = 0, beta = 1, cap_ns = 0;
+    double inv_beta = 1.0;
+    const bool link_scan = timed && a.cost.link_budget_ns < a.cost.rank_budget_ns;
+    const int key = amax < amin ? amax * kMaxR + amin : amin * kMaxR + amax;
+    if (timed) {
+      const int tl = __builtin_amdgcn_readlane(node_r, amax) == __builtin_amdgcn_readlane(node_r, amin) ? 0 : 1;
+      alpha = a.cost.alpha_ns[tl];
+      beta = a.cost.beta_bytes_per_us[tl];
+      inv_beta = 1.0 / (double)beta;
+      const int64_t left_a = (int64_t)readlane_u64((uint64_t)left_r, amax);
+      const int64_t left_b = (int64_t)readlane_u64((uint64_t)left_r, amin);
+      cap_ns = left_a < left_b ? left_a : left_b;
+      if (link_scan) {
+        // a link budget below the rank budget: what the pair's accepted swaps left of it
+        uint64_t used = 0;
+        for (int s0 = 0; s0 < ns; s0 += 64) {
+          const int s = s0 + lane;
+          used += s < ns && lds.acc_pair[s] == key ? (uint64_t)lds.acc_cost[s] : 0ull;
+        }
+        const int64_t left_l = a.cost.link_budget_ns - (int64_t)wave_sum_u64(used);
+        cap_ns = left_l < cap_ns ? left_l : cap_ns;
+      }
+    }
+    uint64_t gk = 0, tk = 0, ck = 1;
     int64_t dl = 0;
     uint2 ea = {0u, 0u}, eb = {0u, 0u};
     const bool cap_hit = capped && (part[amax] >= bg.per_rank_cap || part[amin] >= bg.per_rank_cap);
@@ -482,7 +591,6 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
     // its set bits are rare and are walked with uniform values
     uint32_t eq_rows = 0, eq_cols = 0;
     if (J > 1) {
-      const float inv_e = 1.0f / (float)E;
 #pragma unroll
       for (int h = 0; h < CPL; ++h) {
         bool eqh = false;
@@ -517,17 +625,35 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
       const int64_t gain = g_den * (M - m2) + spread;
       // tie order inside the fixed pair (amax, amin): item ids; the slots ride along below them
       const uint64_t th = ((((uint64_t)i << kItemBits) | j) << 8) | ((uint64_t)pl << 4) | (uint64_t)ql;
-      if (ok && gain > 0 && (gk == 0 || (uint64_t)gain > gk || ((uint64_t)gain == gk && th < tk))) {
-        gk = (uint64_t)gain;
-        tk = th;
-        dl = d;
-        ea = xa;
-        eb = xb;
+      if (!ok || gain <= 0) continue;
+      if (timed) {
+        const int ei = i >= (uint32_t)V ? -1 : J == 1 ? (int)i : expert_of((int)i, E, inv_e);
+        const int ej2 = j >= (uint32_t)V ? -1 : J == 1 ? (int)j : expert_of((int)j, E, inv_e);
+        const int64_t bytes = (ei >= 0 ? ebytes[ei] : 0) + (ej2 >= 0 ? ebytes[ej2] : 0);
+        const int64_t c = alpha + ceil_div(bytes * 1000, beta, inv_beta);
+        if (c > cap_ns || !ratio_better((uint64_t)gain, (uint64_t)c, th, gk, ck, tk)) continue;
+        ck = (uint64_t)c;
+      } else if (!(gk == 0 || (uint64_t)gain > gk || ((uint64_t)gain == gk && th < tk))) {
+        continue;
       }
+      gk = (uint64_t)gain;
+      tk = th;
+      dl = d;
+      ea = xa;
+      eb = xb;
     }
-    const uint64_t g = wave_max_u64(gk);
-    if (g == 0) break;                          // no admissible candidate with positive benefit
-    const uint64_t t = ~wave_max_u64(gk == g ? ~tk : 0ull);
+    uint64_t g, t, cst = 1;
+    if (timed) {
+      g = gk;
+      cst = ck;
+      t = tk;
+      wave_best_ratio(g, cst, t);
+      if (g == 0) break;                        // no admissible candidate with positive benefit
+    } else {
+      g = wave_max_u64(gk);
+      if (g == 0) break;
+      t = ~wave_max_u64(gk == g ? ~tk : 0ull);
+    }
     const int wp = (int)(t >> 4) & 15, wq = (int)t & 15;
     const int wi = (int)(t >> (8 + kItemBits)) & ((1 << kItemBits) - 1);
     const int wj = (int)(t >> 8) & ((1 << kItemBits) - 1);
@@ -545,7 +671,12 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
       sw.expert_dst = wj < V ? wj : -1;
       sw.gain = (int64_t)g;
       a.swaps[ns] = sw;
+      if (timed) {
+        if (link_scan) { lds.acc_pair[ns] = key; lds.acc_cost[ns] = (int64_t)cst; }
+        if (a.swap_cost_ns) a.swap_cost_ns[ns] = (int64_t)cst;
+      }
     }
+    if (timed && (lane == amax || lane == amin)) left_r -= (int64_t)cst;
 #pragma unroll
     for (int m = 0; m < RPL; ++m) {
       const int r = lane + 64 * m;

@@ -37,7 +37,7 @@ def test_header_declares_the_boundary():
                             "fb_fold_rank_loads", "fb_plan_swaps_timed",
                             "fb_plan_swaps_timed_device", "fb_predict_split_workspace_bytes",
                             "fb_fold_slot_loads", "fb_predict_load_packed_noalloc",
-                            "fb_predict_plan_packed"])
+                            "fb_predict_plan_packed", "fb_predict_plan_timed_packed"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -56,7 +56,7 @@ def test_struct_layouts_match_header():
 
 def test_version_and_status_strings():
     lib = fb.lib()
-    assert lib.fb_abi_version() == 5
+    assert lib.fb_abi_version() == 6
     for code in (0, -1, -2, -3, -4):
         assert L.status_string(code).startswith("FB_")
     assert "unknown" in L.status_string(7)
@@ -424,6 +424,54 @@ def _predict_plan_call(**over):
 def test_predict_plan_validation_without_gpu(over, code):
     """Both calls' arguments are checked on the host before anything runs."""
     assert _predict_plan_call(**over) == code
+
+
+def _cost(**over):
+    a = dict(nodes=[0, 0, 1, 1], sizes=[1000] * 16, alpha=(10, 20), beta=(100, 50), rank=10_000,
+             link=None)
+    a.update(over)
+    return fb.CostModel(a["nodes"], a["sizes"], a["alpha"], a["beta"], a["rank"], a["link"]).to_c()
+
+
+def _predict_plan_timed_call(**over):
+    """fb_predict_plan_timed_packed with fake (never dereferenced) pointers."""
+    a = dict(hidden=0x1000, T=4, H=64, ld=64, dtype=L.FB_BF16, wp=0x2000, wpb=8192, E=16, lb=None,
+             sb=None, sc=fb.Scoring("softmax", 2).to_c(), e2r=0x3000, R=4, counts=0x4000,
+             rl=0x5000, mm=0x6000, ws=0x7000, wsb=2048, slots=0x8000, S=4,
+             bg=fb.Budget(4).to_c(), cm=_cost(), nodes=0xf000, nbytes=0xf800, swaps=0x9000,
+             costs=None, ns=0xa000, nslots=0xb000, ne2r=0xc000, nrl=0xd000, status=0xe000,
+             stream=None)
+    a.update(over)
+    sc, bg, cm = a["sc"], a["bg"], a["cm"]
+    return fb.lib().fb_predict_plan_timed_packed(
+        a["hidden"], a["T"], a["H"], a["ld"], a["dtype"], a["wp"], a["wpb"], a["E"], a["lb"],
+        a["sb"], ctypes.byref(sc) if sc is not None else None, a["e2r"], a["R"], a["counts"],
+        a["rl"], a["mm"], a["ws"], a["wsb"], a["slots"], a["S"],
+        ctypes.byref(bg) if bg is not None else None, ctypes.byref(cm) if cm is not None else None,
+        a["nodes"], a["nbytes"], a["swaps"], a["costs"], a["ns"], a["nslots"], a["ne2r"], a["nrl"],
+        a["status"], a["stream"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(wp=None), L.FB_EINVAL),
+    (dict(wpb=8191), L.FB_ENOSPC),
+    (dict(counts=None), L.FB_EINVAL),
+    (dict(H=48), L.FB_EUNSUPPORTED),
+    (dict(slots=None), L.FB_EINVAL),
+    (dict(S=3), L.FB_EINVAL),                     # E = 16 > R * S = 12
+    (dict(swaps=None), L.FB_EINVAL),
+    (dict(cm=None), L.FB_EINVAL),
+    (dict(nodes=None), L.FB_EINVAL),
+    (dict(nbytes=None), L.FB_EINVAL),
+    (dict(cm=_cost(alpha=(0, 20))), L.FB_EINVAL),
+    (dict(cm=_cost(beta=(100, 0))), L.FB_EINVAL),
+    (dict(cm=_cost(rank=-1)), L.FB_EINVAL),
+    (dict(cm=_cost(link=-2)), L.FB_EINVAL),
+    (dict(bg=fb.Budget(1025).to_c()), L.FB_EUNSUPPORTED),   # the device cap of timed swaps
+])
+def test_predict_plan_timed_validation_without_gpu(over, code):
+    """The prediction's, the plan's and the cost model's arguments are checked on the host."""
+    assert _predict_plan_timed_call(**over) == code
 
 
 def test_unpacked_predict_needs_room_for_the_packed_weight():

@@ -173,3 +173,98 @@ def test_fused_plan_repeats_and_reuses_its_outputs():
     torch.cuda.synchronize()
     assert np.array_equal(out.counts.cpu().numpy(), first[0])
     _same_plan(plan.to_host(), first[1])
+
+
+# ---- under a time budget (Eq. 9-10): fb_predict_plan_timed_packed -----------------------------------
+
+def _timed_both(wl, slots, e2r, budget, cost, split=True):
+    """The fused call with a cost model, and the prediction followed by the time-budgeted device
+    planner; both results on the host."""
+    li = make_layer(wl, 0)
+    x = to_device(li.x, wl.dtype)
+    wp = fb.pack_router_weight(to_device(li.w, wl.dtype))
+    sb = None if li.select_bias is None else torch.from_numpy(li.select_bias).cuda()
+    slots_t, e2r_t = _t(slots), _t(e2r)
+    sc = scoring_of(wl)
+    p1 = fb.Predictor(split=split)
+    out1, plan1 = p1.predict_plan(x, wp, sc, e2r_t, slots_t, budget, select_bias=sb,
+                                  cost=fb.CostModel(*cost))
+    p2 = fb.Predictor(split=split)
+    out2 = p2.predict_load(x, wp, sc, e2r_t, slots.shape[0], select_bias=sb)
+    plan2 = fb.plan_swaps_timed_device(out2.counts, slots_t, budget, fb.CostModel(*cost))
+    torch.cuda.synchronize()
+    assert not p1.workspace[:2048].cpu().numpy().any()
+    c1, c2 = out1.counts.cpu().numpy(), out2.counts.cpu().numpy()
+    assert np.array_equal(c1, c2)
+    assert np.array_equal(out1.rank_loads.cpu().numpy(), out2.rank_loads.cpu().numpy())
+    h1, h2 = plan1.to_host(), plan2.to_host()
+    _same_plan(h1, h2)
+    assert h1.costs == h2.costs
+    return c1, h1
+
+
+def _nodes_sizes(R, E, per_node, rng, mixed):
+    nodes = [r // per_node for r in range(R)]
+    mb = 7168 * 2048 * 2
+    sizes = [int(v) * mb for v in rng.integers(1, 4, E)] if mixed else [3 * mb] * E
+    return nodes, sizes
+
+
+@pytest.mark.parametrize("name,T,R,S,per_node,mixed,link_ms,B", [
+    ("dsv3", 3000, 32, 8, 8, False, None, 64),     # 88 MB experts, 4 nodes of 8 ranks
+    ("dsv3", 2048, 32, 8, 8, True, 3, 64),         # mixed sizes, a binding 3 ms link budget
+    ("dsv3", 2048, 64, 4, 16, False, None, 16),    # 64 ranks: the most the fused planner takes
+    ("qwen3", 1500, 8, 11, 4, True, None, 8),      # 11 slots per rank: two candidates per lane
+    ("mixtral", 1000, 8, 2, 4, False, None, 4),    # split mode; one expert per rank and a spare
+])
+def test_timed_fused_plan_matches_the_two_calls_and_the_oracle(name, T, R, S, per_node, mixed,
+                                                               link_ms, B):
+    from oracle.cost import CostModel as OCost
+    wl = CONFIGS[name]
+    E = wl.E if S != 11 else 64
+    wl = dataclasses.replace(wl, T=T, H=512 if name != "mixtral" else 4096, E=E, R=R, S=S,
+                             n_clusters=min(wl.n_clusters, E), k=min(wl.k, E))
+    slots, e2r = contiguous_placement(E, R, S)
+    nodes, sizes = _nodes_sizes(R, E, per_node, np.random.default_rng(7), mixed)
+    cost = OCost(nodes, sizes, (20_000, 50_000), (100_000, 25_000), 8_000_000,
+                 None if link_ms is None else link_ms * 1_000_000)
+    bg = fb.Budget(B)
+    counts, h = _timed_both(wl, slots, e2r, bg, cost, split=True)
+    ref = OP.plan_swaps(counts.astype(np.int64), slots, B, cost=cost)
+    _same_plan(h, ref)
+    assert h.costs == ref.costs
+    _say(f"[predict_plan timed] {name} R={R} S={S}: {len(h.swaps)} swaps, costs {h.costs[:3]}")
+
+
+@pytest.mark.parametrize("R,S,mode", [(32, 8, "full"), (128, 2, "frontier")])
+def test_timed_plans_the_fused_planner_does_not_take(R, S, mode):
+    """Full mode, and more than 64 ranks under a time budget: the plan runs as its own kernel."""
+    from oracle.cost import CostModel as OCost
+    wl = dataclasses.replace(CONFIGS["dsv3"], T=2048, H=512, R=R, S=S)
+    slots, e2r = contiguous_placement(wl.E, R, S)
+    nodes, sizes = _nodes_sizes(R, wl.E, 8, np.random.default_rng(3), False)
+    # 16 ms per rank: a swap across nodes (about 7 ms for two 88 MB experts) fits twice
+    cost = OCost(nodes, sizes, (20_000, 50_000), (100_000, 25_000), 16_000_000)
+    counts, h = _timed_both(wl, slots, e2r, fb.Budget(16, mode=mode), cost)
+    assert len(h.swaps) >= 1
+    _say(f"[predict_plan timed] R={R} {mode}: {len(h.swaps)} swaps")
+
+
+def test_timed_fused_plan_reports_a_bad_expert_size_and_keeps_the_prediction():
+    from oracle.cost import CostModel as OCost
+    wl = dataclasses.replace(CONFIGS["dsv3"], T=1024, H=512)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    sizes = [1000] * wl.E
+    sizes[5] = (1 << 40) + 1                      # beyond 2^40 bytes
+    cost = OCost([r // 8 for r in range(wl.R)], sizes, (20_000, 50_000), (100_000, 25_000), 10 ** 9)
+    li = make_layer(wl, 0)
+    x = to_device(li.x, wl.dtype)
+    wp = fb.pack_router_weight(to_device(li.w, wl.dtype))
+    sb = torch.from_numpy(li.select_bias).cuda()
+    out, plan = fb.Predictor().predict_plan(x, wp, scoring_of(wl), _t(e2r), _t(slots), fb.Budget(8),
+                                            select_bias=sb, cost=fb.CostModel(*cost))
+    ref = fb.Predictor().predict_load(x, wp, scoring_of(wl), _t(e2r), wl.R, select_bias=sb)
+    torch.cuda.synchronize()
+    assert int(plan.status.item()) == fb._lib.FB_EINVAL
+    assert int(plan.n_swaps.item()) == 0
+    assert np.array_equal(out.counts.cpu().numpy(), ref.counts.cpu().numpy())
