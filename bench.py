@@ -28,12 +28,18 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "predict_dsv3_counters.txt")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_14205_amd", "csrc", "fb_predict.hip")
+# the predictor kernel's sources: its own file and the headers compiled into it (the one-wave
+# planner of its last workgroup among them)
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_14205_amd", "csrc", f)
+                  for f in ("fb_predict.hip", "fb_plan_wave.h", "fb_internal.h")]
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def algorithmic_bytes(wl) -> int:
