@@ -179,27 +179,33 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
                                   stream=side)
     torch.cuda.synchronize()
     lat = []                          # the early pass's own latency in the last run_once
+    timed_pass = {}                   # the time-budgeted early pass: its outputs and cost model
 
-    def early_pass():
+    def early_pass(timed=False):
         p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         p0.record(side)
-        pred.predict_plan(x, wp, scoring, e2r_t, slots_t, budget, select_bias=sb, out=out,
-                          plan=plan, stream=side)
+        if timed:
+            tp = timed_pass
+            pred.predict_plan(x, wp, scoring, e2r_t, slots_t, tp["budget"], select_bias=sb,
+                              out=tp["out"], plan=tp["plan"], cost=tp["cost"], stream=side)
+        else:
+            pred.predict_plan(x, wp, scoring, e2r_t, slots_t, budget, select_bias=sb, out=out,
+                              plan=plan, stream=side)
         p1.record(side)
         lat[:] = [(p0, p1)]
 
-    def run_once(attn, use_attn, use_pp, pp_first=False):
+    def run_once(attn, use_attn, use_pp, pp_first=False, timed=False):
         st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e_side = torch.cuda.Event()
         torch.cuda.synchronize()
         st.record(main)
         side.wait_event(st)
         if use_pp and pp_first:
-            early_pass()
+            early_pass(timed)
         if use_attn:
             attn(main)
         if use_pp and not pp_first:
-            early_pass()
+            early_pass(timed)
         e_side.record(side)
         main.wait_event(e_side)
         en.record(main)
@@ -248,6 +254,23 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
         d_first.append(t["first"] - t["alone"])
     med = lambda v: sorted(v)[len(v) // 2]
     quart = lambda v: [sorted(v)[len(v) // 4], sorted(v)[(3 * len(v)) // 4]]
+    # the early pass under the time budget of that layer's own window (Eq. 10) in one call
+    # (fb_predict_plan_timed_packed), enqueued before the attention: its latency beside it, and its
+    # plan against the time-budgeted device planner's on the same counts
+    B1 = max(0, int((med(ta) - t_pp) * 1e6))
+    tb = fb.Budget(64)
+    cm1 = fb.CostModel(nodes_t, sizes_t, (20_000, 50_000), (100_000, 25_000), B1)
+    o1, p1_ = pred.predict_plan(x, wp, scoring, e2r_t, slots_t, tb, select_bias=sb, cost=cm1,
+                                stream=side)
+    timed_pass.update(budget=tb, cost=cm1, out=o1, plan=p1_)
+    l_timed = []
+    for _ in range(7):
+        run_once(attn, True, True, pp_first=True, timed=True)
+        l_timed.append(lat[0][0].elapsed_time(lat[0][1]))
+    got = p1_.to_host()
+    ref = fb.plan_swaps_timed_device(o1.counts, slots_t, tb, cm1).to_host()
+    assert [tuple(v) for v in got.swaps] == [tuple(v) for v in ref.swaps] and got.costs == ref.costs, \
+        "the one-call timed early pass disagrees with the time-budgeted device planner"
     full = per_type["full"]
     return {"attention_standin": "4 sequences x 8192 tokens x 128 heads x 128 dims: S = QK^T and "
                                  "O = SV as bf16 batched GEMMs (hipBLASLt via torch.bmm), main stream; "
@@ -264,6 +287,13 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
                 "hidden_fraction_pass_first": 1.0 - med(d_first) / t_pp,
                 "early_pass_latency_ms_pass_after": med(l_after),
                 "early_pass_latency_ms_pass_first": med(l_first),
+                "timed_early_pass": {"B_l_ns": B1, "swaps": len(got.swaps),
+                                     "cost_ns": sum(got.costs or []),
+                                     "latency_ms_pass_first": med(l_timed),
+                                     "what": "fb_predict_plan_timed_packed with B_l = this "
+                                             "attention's time minus t_predict_plan, 7 runs "
+                                             "enqueued before it; plan = the time-budgeted "
+                                             "device planner's"},
                 "what": f"{reps} repetitions, each timing the attention alone and with the early pass "
                         "(fb_predict_plan_packed) enqueued after and before it (rotating order); "
                         "added = that repetition's difference to the attention alone, median and "
