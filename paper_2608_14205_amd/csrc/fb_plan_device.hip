@@ -76,6 +76,7 @@ struct SharedT {
   uint8_t fr_n[NPAIR];
   uint8_t fr_pt[NPAIR][kFrontCap];
   int32_t last[2];               // ranks of the swap accepted in the previous round
+  int64_t link_used[NPAIR];      // time budget: cost charged to each rank pair's link so far
   int32_t item[CRS];             // slot -> item id (slot value, or V + slot for an empty slot)
   int32_t sload[CRS];            // slot -> load (token share) of its item
   uint8_t mslot[CRS];            // slot -> its item has moved
@@ -208,6 +209,8 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
     eb[u] = a.timed && e < E ? a.expert_bytes[e] : 0;
   }
   for (int r = tid; r < R; r += NT) sh.part[r] = 0;
+  if constexpr (kFront)
+    for (int k = tid; k < R * (R - 1) / 2; k += NT) sh.link_used[k] = 0;
   if (a.timed)
     for (int r = tid; r < R; r += NT) { sh.node[r] = a.rank_node[r]; sh.rank_left[r] = a.cost.rank_budget_ns; }
   __syncthreads();
@@ -453,7 +456,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         // plain count-budget round is straight-line code.
         // The pair {x, y}: its orientation (ra the more loaded rank), D = L_ra - L_rb, and what its
         // candidates may cost; false when none of them can be admissible.
-        auto pair_setup = [&](auto TIMED, int x, int y, int& ra, int& rb, int64_t& D,
+        auto pair_setup = [&](auto TIMED, int k, int x, int y, int& ra, int& rb, int64_t& D,
                               PairCost& pc) -> bool {
           const int64_t Lx = sh.L[x], Ly = sh.L[y];
           if (Lx == Ly) return false;
@@ -468,9 +471,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
             // a link budget at least the rank budget never binds (every swap on the link also
             // charges both ranks); else what the pair's accepted swaps left of it
             if (a.cost.link_budget_ns < a.cost.rank_budget_ns) {
-              const int key = ra < rb ? ra * kMaxR + rb : rb * kMaxR + ra;
-              int64_t left = a.cost.link_budget_ns;
-              for (int s2 = 0; s2 < sh.ns; ++s2) left -= sh.acc_pair[s2] == key ? sh.acc_cost[s2] : 0;
+              const int64_t left = a.cost.link_budget_ns - sh.link_used[k];
               pc.cap_ns = left < pc.cap_ns ? left : pc.cap_ns;
             }
             if (sh.cmin[t] > pc.cap_ns) return false;      // no swap on this link fits any more
@@ -541,7 +542,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
             int ra = 0, rb = 0;
             int64_t D = 0;
             PairCost pc;
-            const bool live = pv && pair_setup(TIMED, x, y, ra, rb, D, pc);
+            const bool live = pv && pair_setup(TIMED, k, x, y, ra, rb, D, pc);
             // slot p of ra, and the S slots of rb (indices clamped into the rank)
             const int sa = ra * S + (p < S ? p : S - 1), sb0 = rb * S;
             const int ia = sh.item[sa];
@@ -646,7 +647,7 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
             int64_t D;
             pair_of(k, x, y);
             PairCost pc;
-            if (!pair_setup(TIMED, x, y, ra, rb, D, pc)) continue;
+            if (!pair_setup(TIMED, k, x, y, ra, rb, D, pc)) continue;
             int64_t other = INT64_MIN;
             for (int t3 = 0; t3 < 3; ++t3) {
               const int tr = sh.top[t3];
@@ -919,7 +920,14 @@ __global__ __launch_bounds__(NT, 1) void plan_general(PlanDeviceLaunch a) {
         sh.L[cb] -= d;
         sh.mslot[sa] = 1; sh.mslot[sb] = 1;
         ++sh.part[ca]; ++sh.part[cb];
-        if constexpr (kFront) { sh.last[0] = ca; sh.last[1] = cb; }
+        if constexpr (kFront) {
+          sh.last[0] = ca;
+          sh.last[1] = cb;
+          if (a.timed) {
+            const int lo = ca < cb ? ca : cb, hi = ca < cb ? cb : ca;
+            sh.link_used[hi * (hi - 1) / 2 + lo] += (int64_t)cst;
+          }
+        }
         fb_swap sw;
         sw.src_rank = ca; sw.dst_rank = cb; sw.src_slot = sa - ca * S; sw.dst_slot = sb - cb * S;
         sw.expert_src = ci < V ? ci : -1;
