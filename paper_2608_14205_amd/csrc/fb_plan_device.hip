@@ -45,7 +45,7 @@ namespace {
 constexpr int kMaxSurvivors = 8192;           // full mode: work units listed per round (more are
                                               // evaluated where their bound test ran)
 // Tables of at most kSmallRS slots and kSmallR ranks run in a workgroup that holds a fraction of the
-// LDS (about 29 KB in frontier mode, 76 KB in full mode, against 153 KB for the largest tables), so
+// LDS (about 29 KB in frontier mode, 92 KB in full mode, against 153 KB for the largest tables), so
 // that it can start on a CU beside another kernel's workgroups, for instance attention's while the
 // plan is made on a side stream, instead of waiting for a whole CU to drain.
 constexpr int kSmallRS = 512;
