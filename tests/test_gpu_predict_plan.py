@@ -268,3 +268,43 @@ def test_timed_fused_plan_reports_a_bad_expert_size_and_keeps_the_prediction():
     assert int(plan.status.item()) == fb._lib.FB_EINVAL
     assert int(plan.n_swaps.item()) == 0
     assert np.array_equal(out.counts.cpu().numpy(), ref.counts.cpu().numpy())
+
+
+def test_timed_fused_plan_on_an_empty_batch_and_on_replicated_placements():
+    from oracle.cost import CostModel as OCost
+    # an empty batch: zero counts, no swap, the placement unchanged
+    wl = dataclasses.replace(CONFIGS["dsv3"], T=0, H=512)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    cost = OCost([r // 8 for r in range(wl.R)], [1000] * wl.E, (20, 50), (100, 25), 10 ** 6)
+    x = torch.empty((0, 512), dtype=torch.bfloat16, device="cuda")
+    w = to_device(make_layer(dataclasses.replace(wl, T=1), 0).w, wl.dtype)
+    out, plan = fb.Predictor().predict_plan(x, fb.pack_router_weight(w), scoring_of(wl), _t(e2r),
+                                            _t(slots), fb.Budget(8), cost=fb.CostModel(*cost))
+    torch.cuda.synchronize()
+    assert not out.counts.cpu().numpy().any()
+    h = plan.to_host()
+    assert h.swaps == [] and np.array_equal(h.slots, slots) and h.costs == []
+    # replicated placements on 8 ranks: the fused timed plan = the two calls (and the oracle)
+    g = np.random.default_rng(23)
+    done = 0
+    while done < 4:
+        drawn = random_replicated_placement(g, 8, 6)
+        if drawn is None:
+            continue
+        slots, E = drawn
+        if E < 2:
+            continue
+        wl = dataclasses.replace(CONFIGS["tiny"], T=700, H=256, E=E, k=min(2, E), n_clusters=E,
+                                 R=8, S=6)
+        e2r = np.zeros(E, np.int32)
+        for c, v in enumerate(slots.reshape(-1)):
+            if 0 <= v < E:
+                e2r[v] = c // 6                  # rank of replica 0
+        cost = OCost(list(g.integers(0, 2, 8)), list(g.integers(0, 400, E)), (5, 30), (300, 60),
+                     int(g.integers(2000, 9000)))
+        counts, h = _timed_both(wl, slots, e2r, fb.Budget(4), cost)
+        ref = OP.plan_swaps(counts.astype(np.int64), slots, 4, cost=cost)
+        _same_plan(h, ref)
+        assert h.costs == ref.costs
+        done += 1
+    _say("[predict_plan timed] empty batch and replicated placements ok")
