@@ -108,6 +108,50 @@ def test_graph_replay_of_the_one_call_early_pass():
     assert not pred.workspace[:2048].any().item()
 
 
+def test_graph_replay_of_the_time_budgeted_one_call_early_pass():
+    """fb_predict_plan_timed_packed captured as one graph node (node ids and expert sizes already on
+    the device, so the call copies nothing); every replay against the eager result, costs too."""
+    _say("[graph] capture predict_plan under a time budget")
+    wl, slots, e2r, x, w, sb = _setup(T=6000, layer=2)
+    e2r_t = torch.from_numpy(e2r).cuda()
+    slots_t = torch.from_numpy(slots).cuda()
+    wp = fb.pack_router_weight(w)
+    sc, bg = scoring_of(wl), fb.Budget(16)
+    nodes = torch.tensor([r // 8 for r in range(wl.R)], dtype=torch.int32, device="cuda")
+    sizes = torch.full((wl.E,), 3 * 7168 * 2048 * 2, dtype=torch.int64, device="cuda")
+    cm = fb.CostModel(nodes, sizes, (20_000, 50_000), (100_000, 25_000), 8_000_000)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        pred = fb.Predictor(stream=side)
+        out, plan = pred.predict_plan(x, wp, sc, e2r_t, slots_t, bg, select_bias=sb, cost=cm)
+    side.synchronize()
+    eager = (out.counts.clone(), _plan_tuple(plan), plan.costs.clone())
+    assert len(eager[1][0]) > 0                  # the budget admits swaps
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        pred.predict_plan(x, wp, sc, e2r_t, slots_t, bg, select_bias=sb, out=out, plan=plan, cost=cm)
+    torch.cuda.synchronize()
+
+    x2 = to_device(make_layer(wl, 3).x, wl.dtype)   # eager work on other data between replays
+    for rep in range(4):
+        out.counts.fill_(-7)
+        plan.n_swaps.fill_(-7)
+        plan.slots.fill_(-7)
+        plan.costs.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.counts, eager[0]), f"replay {rep}: counts"
+        pt = _plan_tuple(plan)
+        assert pt[0] == eager[1][0] and np.array_equal(pt[1], eager[1][1]) and np.array_equal(pt[2], eager[1][2])
+        n = int(plan.n_swaps.item())
+        assert torch.equal(plan.costs[:n], eager[2][:n])
+        other = fb.predict_load(x2, w, sc, e2r_t, wl.R, select_bias=sb)
+        torch.cuda.synchronize()
+        assert int(other.counts.sum().item()) == x2.shape[0] * wl.k
+    assert not pred.workspace[:2048].any().item()
+
+
 def test_side_stream_next_to_other_work():
     """The predictor on its own stream while a dense bf16 GEMM runs on another (the early pass shares
     the GPU with other layer work): both results stay correct.  The timings are printed."""
