@@ -300,6 +300,53 @@ def measure_overlap(fb, torch, wl, x, wp, scoring, budget, e2r_t, slots_t, sb, c
                         "quartiles; hidden fraction = 1 - added / t_predict_plan; early-pass "
                         "latency = its own start-to-end on the side stream beside the attention"}}
 
+def measure_sequence(fb, torch, wl, x0, w, scoring, budget, e2r_t, slots_t, sb, layers, nbytes):
+    """The early passes of `layers` distinct layers back to back on one stream, as a forward pass
+    issues them (each layer: `fb_predict_plan_packed` on its own hidden states with its own packed
+    router).  Layer l's hidden states are the batch's rows rotated by l * 997 and its router the
+    weight's rows permuted by a seeded permutation: the same statistics, distinct bytes, so every
+    layer reads its hidden states from HBM.  Reported against `layers` x the algorithmic bytes at
+    the HBM peak."""
+    dev = x0.device
+    g = torch.Generator(device="cpu")
+    g.manual_seed(7)
+    xs = [torch.roll(x0, shifts=(l * 997) % max(wl.T, 1), dims=0).contiguous() for l in range(layers)]
+    wps = [fb.pack_router_weight(w[torch.randperm(wl.E, generator=g).to(dev)].contiguous())
+           for _ in range(layers)]
+    pred = fb.Predictor(dev)
+    outs, plans = [], []
+    for l in range(layers):
+        o, p = pred.predict_plan(xs[l], wps[l], scoring, e2r_t, slots_t, budget, select_bias=sb)
+        outs.append(o)
+        plans.append(p)
+    torch.cuda.synchronize()
+    for o in outs:
+        assert int(o.counts.sum().item()) == wl.T * wl.k, "a layer failed the count invariant"
+
+    def once():
+        for l in range(layers):
+            pred.predict_plan(xs[l], wps[l], scoring, e2r_t, slots_t, budget, select_bias=sb,
+                              out=outs[l], plan=plans[l])
+
+    for _ in range(3):
+        once()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(7):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        once()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    ms = sorted(times)[len(times) // 2]
+    roof_ms = layers * nbytes / (PEAK_HBM_GBS * 1e9) * 1e3
+    return {"layers": layers, "ms": ms, "us_per_layer": ms / layers * 1e3,
+            "roofline_ms": roof_ms, "frac": roof_ms / ms,
+            "what": "median of 7 passes over the layers, each layer's fb_predict_plan_packed call "
+                    "back to back on one stream; roofline = layers x algorithmic bytes at 8 TB/s"}
+
+
 def _time_ms(torch, stream, fn, K):
     """Average duration of K back-to-back calls of fn, bracketed by events on the stream."""
     a = torch.cuda.Event(enable_timing=True)
@@ -478,6 +525,9 @@ def main():
     ap.add_argument("--workload", default="deepseek-v3",
                     choices=["deepseek-v3", "mixtral", "qwen3", "sweep-4096", "sweep-16384",
                              "sweep-65536"])
+    # the multi-layer workloads (48 Qwen3-shaped layers, 58 sweep layers): also time that many
+    # distinct layers back to back, as a forward pass issues their early passes
+    ap.add_argument("--layers", type=int, default=0)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the predictor shards over tokens with one 1 KB count "
@@ -726,6 +776,9 @@ def main():
                  "max_mean_after": float(host_plan.rank_loads.max() * wl.R / host_plan.rank_loads.sum())},
         "cpu_baseline": cpu,
     }
+    if args.layers > 0:
+        result["sequence"] = measure_sequence(fb, torch, wl, x0, w, scoring, budget, e2r_t, slots_t,
+                                              sb, args.layers, nbytes)
     print(json.dumps(result), flush=True)
 
 
