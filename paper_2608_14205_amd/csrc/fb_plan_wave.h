@@ -422,10 +422,12 @@ __device__ __forceinline__ PlanWaveLds plan_wave_lds(char* mem, int CAP, int RPL
 // RPL: ranks per lane (R <= 64 * RPL); rank r lives in lane r % 64, register r / 64.
 // CPL: candidates per lane, 1 for S * S <= 64, 2 for S * S <= 128.
 // Runs in the first wave of its workgroup (threadIdx.x < 64); the caller's other waves take no part.
+// TABLES_IN_LDS: the caller has already put the counts in lds.cnt, the slot table in lds.vals and,
+// under a time budget, the expert sizes in lds.ebytes (all published by a barrier).
 // Time budgets (a.timed) need RPL 1: every candidate between the two frontier ranks is costed by
 // Eq. 9 on their link, admitted if it fits what is left of both ranks' and of the link's budgets,
 // and the round's best is the largest benefit / cost, then the tie key.
-template <int RPL, int CPL>
+template <int RPL, int CPL, bool TABLES_IN_LDS = false>
 __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds) {
   int32_t* const vals = lds.vals;      // the input tables
   int32_t* const cnt = lds.cnt;
@@ -446,11 +448,14 @@ __device__ void plan_wave_body(const PlanDeviceLaunch& a, const PlanWaveLds& lds
 
   // every input table is fetched before the first wait
   for (int e = lane; e < E; e += 64) {
-    cnt[e] = a.counts[e];
+    if (!TABLES_IN_LDS) {
+      cnt[e] = a.counts[e];
+      if (timed) ebytes[e] = a.expert_bytes[e];
+    }
     reps[e] = 0;
-    if (timed) ebytes[e] = a.expert_bytes[e];
   }
-  for (int c = lane; c < RS; c += 64) vals[c] = a.slot_expert[c];
+  if (!TABLES_IN_LDS)
+    for (int c = lane; c < RS; c += 64) vals[c] = a.slot_expert[c];
   for (int r = lane; r < R; r += 64) part[r] = 0;
   // time budget: rank `lane`'s node and what is left of its budget
   const int32_t node_r = timed && lane < R ? a.rank_node[lane] : 0;

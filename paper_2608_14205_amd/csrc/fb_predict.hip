@@ -1036,13 +1036,34 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   for (int r = tid; r < p.R; r += kThreads) rl[r] = 0;
   if (tid == 0) s_flag = 0;
   __syncthreads();
+  // the swap plan's tables are fetched while the counters are read, and go straight to the
+  // planner's LDS (its arrays lie past the rank loads at the start of smem); R * S <= 704 and E <= 256
+  static_assert(SMEM >= plan_wave_lds_bytes(wave_cap(1, 2), 1), "the planner's LDS fits");
+  const PlanWaveLds pl = plan_wave_lds(smem, wave_cap(1, 2), 1);
+  constexpr int kPre = (wave_cap(1, 2) + kThreads - 1) / kThreads;
+  const int rs_plan = p.plan_cpl != 0 ? p.plan.R * p.plan.S : 0;
+  int32_t pre[kPre];
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int c = tid + i * kThreads;
+    pre[i] = c < rs_plan ? p.plan.slot_expert[c] : 0;
+  }
+  const bool pre_bytes = p.plan_cpl != 0 && p.plan.timed && tid < E;
+  const int64_t preb = pre_bytes ? p.plan.expert_bytes[tid] : 0;
   for (int e = tid; e < E; e += kThreads) {
     const int v = atomicExch(&p.ws_acc[e], 0);
     p.counts[e] = v;
+    if (p.plan_cpl != 0) pl.cnt[e] = v;
     const int r = p.e2r[e];
     if (r >= 0 && r < p.R) atomicAdd(&rl[r], v);
     else s_flag = 1;
   }
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int c = tid + i * kThreads;
+    if (c < rs_plan) pl.vals[c] = pre[i];
+  }
+  if (pre_bytes) pl.ebytes[tid] = preb;
   __syncthreads();
   int64_t mx = 0, sum = 0;
   for (int r = tid; r < p.R; r += kThreads) {
@@ -1069,14 +1090,12 @@ __global__ __launch_bounds__(kThreads, 1) void predict_kernel(Params p) {
   }
   if (p.plan_cpl != 0) {
     // The swap plan of the counts just written (Alg. 1, frontier mode): the one-wave planner in
-    // this workgroup's first wave, in LDS the selection no longer needs.  The barrier publishes
-    // every wave's counts; the other waves are done.
-    static_assert(SMEM >= plan_wave_lds_bytes(wave_cap(1, 2), 1), "the planner's LDS fits");
+    // this workgroup's first wave, in LDS the selection no longer needs, with its tables already
+    // there.  The barrier publishes every wave's entries; the other waves are done.
     __syncthreads();
     if (wave != 0) return;
-    const PlanWaveLds l = plan_wave_lds(smem, wave_cap(1, 2), 1);
-    if (p.plan_cpl == 1) plan_wave_body<1, 1>(p.plan, l);
-    else plan_wave_body<1, 2>(p.plan, l);
+    if (p.plan_cpl == 1) plan_wave_body<1, 1, true>(p.plan, pl);
+    else plan_wave_body<1, 2, true>(p.plan, pl);
   }
 }
 
