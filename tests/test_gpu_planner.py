@@ -256,6 +256,58 @@ def test_device_planner_seeded_fuzz():
     assert n > 900
 
 
+def test_timed_device_planner_seeded_fuzz():
+    """device = host (plans and Eq. 9 costs) on 400 seeded random instances under time budgets:
+    plain and replicated placements, R up to 129, S up to 11 (the one-wave kernel for frontier plans
+    on at most 64 ranks, the general kernel otherwise, stored per-pair frontiers in full mode on at
+    most 64 ranks and 8 slots), nodes of 1-16 ranks, expert sizes 0-2^30 bytes, rank budgets that
+    admit anywhere from no swap to all of them, and link budgets below or above them."""
+    from workloads import random_replicated_placement
+    print("[plan] timed seeded fuzz", flush=True)
+    g = np.random.default_rng(20262)
+    n = full = swaps = 0
+    for it in range(400):
+        R = int(g.integers(2, [9, 33, 65, 130][it % 4]))
+        S = int(g.integers(1, 12))
+        if R * S > 2048:
+            continue
+        if g.random() < 0.4:
+            got = random_replicated_placement(g, R, S)
+            if got is None:
+                continue
+            slots, E = got
+        else:
+            E = int(g.integers(1, R * S + 1))
+            t = np.full(R * S, -1, np.int32)
+            t[g.permutation(R * S)[:E]] = np.arange(E)
+            slots = t.reshape(R, S)
+        hi = [5, 60, 3000, 2 ** 20][int(g.integers(0, 4))]
+        counts = (g.integers(0, hi, size=E) * (g.random(E) < 0.9)).astype(np.int32)
+        mode = "full" if g.random() < 0.35 and R * R * S * S <= 300000 else "frontier"
+        per_node = int(g.integers(1, 17))
+        sizes = (g.integers(0, 2 ** 30, size=E) if g.random() < 0.5
+                 else np.full(E, int(g.integers(0, 2 ** 30)))).tolist()
+        alpha = (int(g.integers(0, 50_000)), int(g.integers(0, 100_000)))
+        beta = (int(g.integers(1_000, 200_000)), int(g.integers(1_000, 50_000)))
+        # one swap of two average experts across nodes, to scale the budgets
+        one = max(alpha[i] + 2 * int(np.mean(sizes)) * 1000 // beta[i] for i in (0, 1))
+        rank_ns = int(one * g.choice([0, 0.5, 1, 2, 4, 16, 64]))
+        link_ns = None if g.random() < 0.5 else int(rank_ns * g.choice([0, 0.3, 1, 3]))
+        cm = fb.CostModel([r // per_node for r in range(R)], sizes, alpha, beta, rank_ns, link_ns)
+        gamma = [None, (0, 1), (1, 7), (3, 2)][int(g.integers(0, 4))]
+        bg = fb.Budget(int(g.integers(0, 12)), mode=mode, per_rank_cap=int(g.integers(0, 3)),
+                       tau=int(g.integers(0, 3)), gamma=gamma, layer_id=int(g.integers(0, 5)))
+        host = fb.plan_swaps_timed(counts, slots, bg, cm)
+        dev = _dev_timed(counts, slots, bg, cm)
+        _same(dev, host)
+        assert dev.costs == host.costs, it
+        n += 1
+        full += mode == "full"
+        swaps += len(host.swaps) > 0
+    print(f"[plan]   {n} instances, {full} in full mode, {swaps} with swaps", flush=True)
+    assert n > 350 and full > 80 and swaps > 150
+
+
 @pytest.mark.parametrize("max_swaps", [1, 6])
 def test_full_mode_pair_with_a_long_staircase(max_swaps):
     """Full mode under a time budget on two ranks of 8 slots whose candidates form a staircase of 9

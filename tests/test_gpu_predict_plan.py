@@ -236,6 +236,53 @@ def test_timed_fused_plan_matches_the_two_calls_and_the_oracle(name, T, R, S, pe
     _say(f"[predict_plan timed] {name} R={R} S={S}: {len(h.swaps)} swaps, costs {h.costs[:3]}")
 
 
+def test_timed_fused_plan_seeded_fuzz():
+    """The one-call early pass under time budgets on 24 seeded random instances the fused planner
+    takes (2-64 ranks, 1-11 slots per rank, random plain slot tables with empty slots, both input
+    dtypes, fused and split prediction, nodes of 1-16 ranks, random expert sizes, rank and link
+    budgets): the fused plan = the two calls, and the host planner and the oracle on its counts."""
+    from oracle.cost import CostModel as OCost
+    g = np.random.default_rng(4242)
+    swaps = 0
+    for it in range(24):
+        R = int(g.integers(2, 65))
+        S = int(g.integers(1, 12))
+        E = int(g.integers(2, min(256, R * S) + 1))
+        t = np.full(R * S, -1, np.int32)
+        t[g.permutation(R * S)[:E]] = np.arange(E)
+        slots = t.reshape(R, S)
+        e2r = np.zeros(E, np.int32)
+        for c, v in enumerate(t):
+            if v >= 0:
+                e2r[v] = c // S
+        wl = dataclasses.replace(CONFIGS["tiny"], T=int(g.integers(200, 1500)), H=256, E=E,
+                                 k=min(4, E), n_clusters=E, R=R, S=S,
+                                 dtype=["f32", "bf16"][it % 2])
+        per_node = int(g.integers(1, 17))
+        sizes = [int(v) for v in g.integers(0, 2 ** 28, size=E)]
+        alpha = (int(g.integers(0, 50_000)), int(g.integers(0, 100_000)))
+        beta = (int(g.integers(1_000, 200_000)), int(g.integers(1_000, 50_000)))
+        one = max(alpha[i] + 2 * int(np.mean(sizes)) * 1000 // beta[i] for i in (0, 1))
+        rank_ns = int(one * g.choice([0.5, 1, 2, 4, 16]))
+        link_ns = None if g.random() < 0.5 else int(rank_ns * g.choice([0.3, 1, 3]))
+        cost = OCost([r // per_node for r in range(R)], sizes, alpha, beta, rank_ns, link_ns)
+        bg = fb.Budget(int(g.integers(1, 17)), per_rank_cap=int(g.integers(0, 3)),
+                       tau=int(g.integers(0, 3)), layer_id=int(g.integers(0, 5)))
+        _say(f"[predict_plan timed fuzz] {it}: R={R} S={S} E={E} T={wl.T} {wl.dtype}")
+        counts, h = _timed_both(wl, slots, e2r, bg, cost, split=bool(it % 3))
+        host = fb.plan_swaps_timed(counts, slots, bg, fb.CostModel(*cost))
+        _same_plan(h, host)
+        assert h.costs == host.costs
+        if R * S <= 256:
+            ref = OP.plan_swaps(counts.astype(np.int64), slots, bg.max_swaps, tau=bg.tau,
+                                per_rank_cap=bg.per_rank_cap, layer_id=bg.layer_id, cost=cost)
+            _same_plan(h, ref)
+            assert h.costs == ref.costs
+        swaps += len(h.swaps) > 0
+    _say(f"[predict_plan timed fuzz] {swaps} of 24 with swaps")
+    assert swaps >= 12
+
+
 @pytest.mark.parametrize("R,S,mode", [(32, 8, "full"), (128, 2, "frontier")])
 def test_timed_plans_the_fused_planner_does_not_take(R, S, mode):
     """Full mode, and more than 64 ranks under a time budget: the plan runs as its own kernel."""
