@@ -287,7 +287,7 @@ def test_timed_device_planner_seeded_fuzz():
         per_node = int(g.integers(1, 17))
         sizes = (g.integers(0, 2 ** 30, size=E) if g.random() < 0.5
                  else np.full(E, int(g.integers(0, 2 ** 30)))).tolist()
-        alpha = (int(g.integers(0, 50_000)), int(g.integers(0, 100_000)))
+        alpha = (int(g.integers(1, 50_000)), int(g.integers(1, 100_000)))
         beta = (int(g.integers(1_000, 200_000)), int(g.integers(1_000, 50_000)))
         # one swap of two average experts across nodes, to scale the budgets
         one = max(alpha[i] + 2 * int(np.mean(sizes)) * 1000 // beta[i] for i in (0, 1))

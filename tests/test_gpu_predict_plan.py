@@ -260,7 +260,7 @@ def test_timed_fused_plan_seeded_fuzz():
                                  dtype=["f32", "bf16"][it % 2])
         per_node = int(g.integers(1, 17))
         sizes = [int(v) for v in g.integers(0, 2 ** 28, size=E)]
-        alpha = (int(g.integers(0, 50_000)), int(g.integers(0, 100_000)))
+        alpha = (int(g.integers(1, 50_000)), int(g.integers(1, 100_000)))
         beta = (int(g.integers(1_000, 200_000)), int(g.integers(1_000, 50_000)))
         one = max(alpha[i] + 2 * int(np.mean(sizes)) * 1000 // beta[i] for i in (0, 1))
         rank_ns = int(one * g.choice([0.5, 1, 2, 4, 16]))
