@@ -198,6 +198,115 @@ def test_prediction_equals_actual_when_inputs_coincide():
     assert np.array_equal(a["topk"], b["topk"]) and np.array_equal(a["counts"], b["counts"])
 
 
+def _zero_hidden(wl, layer=0, select_bias=None):
+    """The layer's router weight with hidden states that are exactly zero, so every logit is zero."""
+    li = make_layer(wl, layer)
+    x = np.zeros_like(li.x)
+    return dataclasses.replace(li, x=x, select_bias=select_bias)
+
+
+@pytest.mark.parametrize("E,k,dtype,packed", [(128, 8, "bf16", False), (128, 8, "bf16", True),
+                                              (16, 2, "f32", False), (16, 16, "bf16", True),
+                                              (256, 1, "bf16", True), (8, 8, "bf16", True),
+                                              (256, 32, "f32", False)])
+def test_all_tied_logits_take_the_lowest_indices(E, k, dtype, packed):
+    """Zero hidden states make every logit exactly zero: every expert ties with every other, so each
+    token takes experts 0 .. k-1 (ties go to the lower index, Sec. "Residual Workload Prediction",
+    the model's top-k rule) and the counts are T for those experts and zero elsewhere.  Checked
+    exactly on every token of a batch that spans several tiles and a ragged tail, in fused and
+    split launches; no near-tie exemption applies."""
+    T = 300
+    wl = dataclasses.replace(CONFIGS["tiny"].with_T(T), H=256, E=E, k=k, dtype=dtype, R=8,
+                             S=max(1, E // 8), n_clusters=E)
+    e2r = (np.arange(E) * 8 // E).astype(np.int32)
+    li = _zero_hidden(wl)
+    gpu = run_gpu(li, wl, e2r, packed=packed)
+    _say(f"[ties] E={E} k={k} {dtype} packed={packed}")
+    assert not gpu["logits"].any()
+    assert np.array_equal(np.sort(gpu["topk"], axis=1), np.tile(np.arange(k), (T, 1)))
+    want = np.where(np.arange(E) < k, T, 0)
+    assert np.array_equal(gpu["counts"], want)
+    assert np.array_equal(gpu["rank_loads"], np.bincount(e2r, weights=want, minlength=8).astype(np.int64))
+    check_counts_consistent(gpu, wl, e2r)
+
+
+def _tied_group_bias():
+    """A selection bias of multiples of 1/1024 (the sigmoid scores 0.5 + b are exact in float32 and
+    float64) for 8 groups of 32 experts, built so that the group rule meets exact ties: the best two
+    scores of groups 3, 4 and 6 sum to the same value at the fourth place (group 3, the lowest index,
+    is kept), and the eighth and ninth experts of the kept groups tie (the lower index is taken).
+    Returns the bias and the eight experts the rule selects."""
+    g = np.random.default_rng(77)
+    j = np.zeros(256, np.int64)
+    tops = {0: (60, 40, 30), 1: (50, 40), 2: (45, 35), 3: (40, 30), 4: (35, 35), 5: (31, 29),
+            6: (60, 10), 7: (25, 25)}
+    chosen = []
+    for grp, vals in tops.items():
+        pos = g.permutation(32)
+        rest = g.integers(-100, 10, size=32)       # below every group's second best: no effect
+        j[32 * grp: 32 * grp + 32] = rest
+        for v, p in zip(vals, pos):
+            j[32 * grp + p] = v
+        if grp <= 3:
+            chosen += [(v, 32 * grp + p) for v, p in zip(vals, pos)]
+    # kept groups 0-3 (sums 100, 90, 80, 70; groups 4 and 6 also sum to 70); the eight best by
+    # (score desc, index asc): 60, 50, 45, the three 40s, 35, then group 0's 30 before group 3's
+    chosen.sort(key=lambda t: (-t[0], t[1]))
+    want = sorted(int(e) for _, e in chosen[:8])
+    return (j / 1024.0).astype(np.float32), want
+
+
+@pytest.mark.parametrize("packed", [False, True])
+def test_tied_groups_and_experts_follow_the_lower_index(packed):
+    """Zero hidden states under the DeepSeek-V3 rule (sigmoid plus selection bias, 8 groups, the 4
+    with the largest sum of their best two scores kept, top-8) with the bias above: exact ties
+    between group scores and at the k-th expert.  Every token must select exactly the experts the
+    rule gives (worked out by hand and by the oracle)."""
+    T = 333
+    wl = dataclasses.replace(CONFIGS["dsv3"].with_T(T), H=256)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    sb, want = _tied_group_bias()
+    oracle_topk = OP.select(np.zeros((1, wl.E), np.float32), wl.k, wl.kind, sb, wl.n_group,
+                            wl.topk_group, wl.group_topn)[0]
+    assert sorted(oracle_topk[0].tolist()) == want
+    li = _zero_hidden(wl, select_bias=sb)
+    gpu = run_gpu(li, wl, e2r, packed=packed)
+    _say(f"[ties] DS-V3 rule, tied groups, packed={packed}: {want}")
+    assert np.array_equal(np.sort(gpu["topk"], axis=1), np.tile(want, (T, 1)))
+    counts = np.zeros(wl.E, np.int64)
+    counts[want] = T
+    assert np.array_equal(gpu["counts"], counts)
+    check_counts_consistent(gpu, wl, e2r)
+
+
+@pytest.mark.parametrize("E,n_group,topk_group,kind,topn", [(64, 8, 2, "sigmoid", 2),
+                                                           (128, 4, 1, "softmax", 1),
+                                                           (32, 4, 4, "sigmoid", 1)])
+def test_k_fills_the_kept_groups(E, n_group, topk_group, kind, topn):
+    """k = topk_group x group size: each token selects every expert of its kept groups, so its
+    selection is a union of whole groups (with every group kept, all E experts and counts of T)."""
+    gsz = E // n_group
+    k = topk_group * gsz
+    T = 400
+    wl = dataclasses.replace(CONFIGS["dsv3"].with_T(T), H=320, E=E, k=k, kind=kind,
+                             n_group=n_group, topk_group=topk_group, group_topn=topn,
+                             select_bias=(kind == "sigmoid"), R=8, S=E // 8, n_clusters=E)
+    e2r = (np.arange(E) % 8).astype(np.int32)
+    li = make_layer(wl, 1)
+    gpu = run_gpu(li, wl, e2r)
+    _say(f"[ties] k={k} fills {topk_group} of {n_group} groups, E={E} {kind}")
+    check_prediction(gpu, li, wl, e2r, label=f"k fills groups E={E}")
+    check_counts_consistent(gpu, wl, e2r)
+    sel = np.sort(gpu["topk"], axis=1)
+    groups = sel // gsz
+    for t in range(T):
+        kept = np.unique(groups[t])
+        assert kept.size == topk_group
+        assert np.array_equal(sel[t], np.concatenate([np.arange(gg * gsz, gg * gsz + gsz) for gg in kept]))
+    if topk_group == n_group:
+        assert np.array_equal(gpu["counts"], np.full(E, T))
+
+
 def test_bad_rank_table_is_reported():
     _say("[e2r] out-of-range rank id")
     wl, e2r = _case("qwen3", 100, H=128)
