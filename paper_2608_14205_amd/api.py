@@ -116,6 +116,39 @@ class DevicePlan:
                     self.expert_to_rank.cpu().numpy(), self.rank_loads.cpu().numpy(), costs)
 
 
+def _fits(checks, what: str) -> None:
+    for t, dtype, n, dev in checks:
+        if t.dtype != dtype or t.device != dev or not t.is_contiguous() or t.numel() < n:
+            raise ValueError(what)
+
+
+def _check_prediction_out(out: "Prediction", E: int, R: int, T: int, k: int, dev,
+                          topk: bool, logits: bool) -> None:
+    """A caller's Prediction must have room for what the kernels write: E counts, R rank loads,
+    one ratio and, when asked for, T x k selections and T x E logits."""
+    checks = [(out.counts, torch.int32, E, dev), (out.rank_loads, torch.int32, R, dev),
+              (out.max_mean, torch.float64, 1, dev)]
+    if topk:
+        checks.append((out.topk, torch.int32, T * k, dev))
+    if logits:
+        checks.append((out.logits, torch.float32, T * E, dev))
+    _fits(checks, "out does not fit this call: contiguous int32[E] counts, int32[R] rank_loads, "
+                  "float64[1] max_mean, int32[T * k] topk and float32[T * E] logits on the device")
+
+
+def _check_plan_out(plan: "DevicePlan", R: int, S: int, E: int, cap: int, dev) -> None:
+    """A caller's DevicePlan must have room for what the planner writes: up to max_swaps swap
+    records (and costs), the R x S table, E expert ranks, R loads and the two status words."""
+    checks = [(plan.swaps, torch.uint8, cap * SWAP_BYTES, dev), (plan.n_swaps, torch.int32, 1, dev),
+              (plan.slots, torch.int32, R * S, dev), (plan.expert_to_rank, torch.int32, E, dev),
+              (plan.rank_loads, torch.int64, R, dev), (plan.status, torch.int32, 1, dev)]
+    if plan.costs is not None:
+        checks.append((plan.costs, torch.int64, cap, dev))
+    _fits(checks, "plan does not fit this call: contiguous buffers on the device with room for "
+                  "max_swaps swaps (and costs), int32[R, S] slots, int32[E] expert ranks and "
+                  "int64[R] loads")
+
+
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
@@ -259,6 +292,7 @@ class Predictor:
             out.topk = torch.empty((T, scoring.k), dtype=torch.int32, device=self.device)
         if return_logits and out.logits is None:
             out.logits = torch.empty((T, E), dtype=torch.float32, device=self.device)
+        _check_prediction_out(out, E, R, T, scoring.k, self.device, return_topk, return_logits)
         sc = scoring.to_c()
         ld = hidden.stride(0) if T > 0 else H
         topk = _ptr(out.topk) if return_topk else None
@@ -332,6 +366,8 @@ class Predictor:
                               torch.empty(R, dtype=torch.int64, device=dev),
                               torch.empty(1, dtype=torch.int32, device=dev),
                               None if cost is None else torch.zeros(cap, dtype=torch.int64, device=dev))
+        _check_prediction_out(out, E, R, T, scoring.k, dev, False, False)
+        _check_plan_out(plan, R, S, E, cap, dev)
         sc = scoring.to_c()
         bg = budget.to_c()
         ld = hidden.stride(0) if T > 0 else H
@@ -380,13 +416,7 @@ def predict_load_packed_noalloc(hidden: torch.Tensor, router: PackedRouter, scor
     E = router.E
     if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
         raise ValueError("expert_to_rank must be int32[E]")
-    if (out.counts.dtype != torch.int32 or out.counts.numel() < E or out.rank_loads.dtype != torch.int32
-            or out.rank_loads.numel() < R or out.max_mean.dtype != torch.float64):
-        raise ValueError("out must hold int32[E] counts, int32[R] rank_loads and a float64 max_mean")
-    if out.topk is not None and (out.topk.dtype != torch.int32 or out.topk.numel() < T * scoring.k):
-        raise ValueError("out.topk must be int32[T * k]")
-    if out.logits is not None and (out.logits.dtype != torch.float32 or out.logits.numel() < T * E):
-        raise ValueError("out.logits must be float32[T * E]")
+    _check_prediction_out(out, E, R, T, scoring.k, dev, out.topk is not None, out.logits is not None)
     for b in (logit_bias, select_bias):
         if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
             raise ValueError("biases must be contiguous float32[E]")
@@ -489,6 +519,7 @@ def plan_swaps_device(counts: torch.Tensor, slots: torch.Tensor, budget: Budget,
                          torch.empty(E, dtype=torch.int32, device=dev),
                          torch.empty(R, dtype=torch.int64, device=dev),
                          torch.empty(1, dtype=torch.int32, device=dev))
+    _check_plan_out(out, R, S, E, max(budget.max_swaps, 1), dev)
     bg = budget.to_c()
     with torch.cuda.device(dev):
         st = L.lib().fb_plan_swaps_device(
@@ -525,6 +556,7 @@ def plan_swaps_timed_device(counts: torch.Tensor, slots: torch.Tensor, budget: B
                          torch.empty(R, dtype=torch.int64, device=dev),
                          torch.empty(1, dtype=torch.int32, device=dev),
                          torch.zeros(cap, dtype=torch.int64, device=dev))
+    _check_plan_out(out, R, S, E, cap, dev)
     bg = budget.to_c()
     cm = cost.to_c()
     with torch.cuda.device(dev):

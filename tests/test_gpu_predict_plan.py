@@ -355,3 +355,39 @@ def test_timed_fused_plan_on_an_empty_batch_and_on_replicated_placements():
         assert h.costs == ref.costs
         done += 1
     _say("[predict_plan timed] empty batch and replicated placements ok")
+
+
+def test_reused_outputs_that_do_not_fit_are_refused():
+    """Outputs passed back in (out=, plan=) must have room for the call's sizes: a plan made for 2
+    swaps cannot take a budget of 8, nor a prediction for 16 experts a call with 256; the binding
+    refuses them before anything is launched."""
+    wl = dataclasses.replace(CONFIGS["dsv3"], T=256, H=256)
+    slots, e2r = contiguous_placement(wl.E, wl.R, wl.S)
+    li = make_layer(wl, 0)
+    x = to_device(li.x, wl.dtype)
+    wp = fb.pack_router_weight(to_device(li.w, wl.dtype))
+    sb = torch.from_numpy(li.select_bias).cuda()
+    pred = fb.Predictor()
+    out = pred.predict_load(x, wp, scoring_of(wl), _t(e2r), wl.R, select_bias=sb)
+    small = fb.plan_swaps_device(out.counts, _t(slots), fb.Budget(2))
+    with pytest.raises(ValueError):
+        fb.plan_swaps_device(out.counts, _t(slots), fb.Budget(8), out=small)
+    with pytest.raises(ValueError):
+        pred.predict_plan(x, wp, scoring_of(wl), _t(e2r), _t(slots), fb.Budget(8),
+                          select_bias=sb, plan=small)
+    tiny = fb.Prediction(torch.zeros(16, dtype=torch.int32, device="cuda"),
+                         torch.zeros(wl.R, dtype=torch.int32, device="cuda"),
+                         torch.zeros(1, dtype=torch.float64, device="cuda"))
+    with pytest.raises(ValueError):
+        pred.predict_load(x, wp, scoring_of(wl), _t(e2r), wl.R, select_bias=sb, out=tiny)
+    short_topk = fb.Prediction(out.counts, out.rank_loads, out.max_mean,
+                               topk=torch.zeros(10, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError):
+        pred.predict_load(x, wp, scoring_of(wl), _t(e2r), wl.R, select_bias=sb, out=short_topk,
+                          return_topk=True)
+    # the same buffers still serve calls they fit, with results equal to fresh ones
+    again = fb.plan_swaps_device(out.counts, _t(slots), fb.Budget(2), out=small)
+    fresh = fb.plan_swaps_device(out.counts, _t(slots), fb.Budget(2))
+    torch.cuda.synchronize()
+    _same_plan(again.to_host(), fresh.to_host())
+    _say("[predict_plan] reused outputs checked")
