@@ -149,6 +149,16 @@ def _check_plan_out(plan: "DevicePlan", R: int, S: int, E: int, cap: int, dev) -
                   "int64[R] loads")
 
 
+def _one_gpu(dev, *tensors) -> None:
+    """Every tensor handed to a kernel must be a GPU tensor on the call's device: a host or other
+    device's pointer would be dereferenced by the kernel."""
+    if torch.device(dev).type != "cuda":
+        raise ValueError("tensors must live on a GPU")
+    for t in tensors:
+        if t is not None and t.device != dev:
+            raise ValueError("all tensors of a call must live on one GPU")
+
+
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
@@ -184,6 +194,7 @@ def pack_router_weight(router_w: torch.Tensor,
         raise ValueError("router_w must be a contiguous E x H tensor")
     E, H = router_w.shape
     code = _dtype_code(router_w)
+    _one_gpu(router_w.device, router_w)
     lib = L.lib()
     nbytes = int(lib.fb_router_packed_bytes(E, H, code))
     if nbytes == 0:
@@ -222,6 +233,8 @@ class Predictor:
     def __init__(self, device=None, stream: Optional[torch.cuda.Stream] = None,
                  split: bool = True):
         dev = torch.device(device) if device is not None else torch.device("cuda")
+        if dev.type != "cuda":
+            raise ValueError("the predictor runs on a GPU device")
         if dev.index is None:
             dev = torch.device("cuda", torch.cuda.current_device())
         self.device = dev
@@ -267,8 +280,9 @@ class Predictor:
                 raise ValueError("all tensors must live on the predictor's device")
         if wdev != self.device:
             raise ValueError("all tensors must live on the predictor's device")
-        if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
-            raise ValueError("expert_to_rank must be int32[E]")
+        if (expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E
+                or not expert_to_rank.is_contiguous()):
+            raise ValueError("expert_to_rank must be a contiguous int32[E]")
         for b in (logit_bias, select_bias):
             if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
                 raise ValueError("biases must be contiguous float32[E]")
@@ -338,8 +352,9 @@ class Predictor:
         for t in (hidden, expert_to_rank, slots, logit_bias, select_bias, router.data):
             if t is not None and t.device != self.device:
                 raise ValueError("all tensors must live on the predictor's device")
-        if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
-            raise ValueError("expert_to_rank must be int32[E]")
+        if (expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E
+                or not expert_to_rank.is_contiguous()):
+            raise ValueError("expert_to_rank must be a contiguous int32[E]")
         for b in (logit_bias, select_bias):
             if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
                 raise ValueError("biases must be contiguous float32[E]")
@@ -409,13 +424,12 @@ def predict_load_packed_noalloc(hidden: torch.Tensor, router: PackedRouter, scor
     if router.H != H or router.dtype != hidden.dtype:
         raise ValueError("packed router was built for another H or dtype")
     dev = hidden.device
-    for t in (router.data, expert_to_rank, logit_bias, select_bias, out.counts, out.rank_loads,
-              out.max_mean, out.topk, out.logits):
-        if t is not None and t.device != dev:
-            raise ValueError("all tensors must live on the hidden states' device")
+    _one_gpu(dev, hidden, router.data, expert_to_rank, logit_bias, select_bias, out.counts,
+             out.rank_loads, out.max_mean, out.topk, out.logits)
     E = router.E
-    if expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E:
-        raise ValueError("expert_to_rank must be int32[E]")
+    if (expert_to_rank.dtype != torch.int32 or expert_to_rank.numel() != E
+            or not expert_to_rank.is_contiguous()):
+        raise ValueError("expert_to_rank must be a contiguous int32[E]")
     _check_prediction_out(out, E, R, T, scoring.k, dev, out.topk is not None, out.logits is not None)
     for b in (logit_bias, select_bias):
         if b is not None and (b.dtype != torch.float32 or b.numel() != E or not b.is_contiguous()):
@@ -510,6 +524,7 @@ def plan_swaps_device(counts: torch.Tensor, slots: torch.Tensor, budget: Budget,
     if not (counts.is_contiguous() and slots.is_contiguous()):
         raise ValueError("counts and slots must be contiguous")
     dev = counts.device
+    _one_gpu(dev, counts, slots)
     R, S = slots.shape
     E = counts.numel()
     if out is None:
@@ -541,6 +556,7 @@ def plan_swaps_timed_device(counts: torch.Tensor, slots: torch.Tensor, budget: B
     if not (counts.is_contiguous() and slots.is_contiguous()):
         raise ValueError("counts and slots must be contiguous")
     dev = counts.device
+    _one_gpu(dev, counts, slots)
     R, S = slots.shape
     E = counts.numel()
     nodes = torch.as_tensor(cost.rank_node, dtype=torch.int32, device=dev).contiguous()
@@ -607,6 +623,7 @@ def row_cosine_mean(a: torch.Tensor, b: torch.Tensor,
         raise ValueError("a and b must be matching 2-D tensors on one device")
     if a.stride(1) != 1 or b.stride(1) != 1:
         raise ValueError("rows must be contiguous")
+    _one_gpu(a.device, a, b)
     out = torch.empty(1, dtype=torch.float64, device=a.device)
     ws = _cosine_workspace(a.device)
     with torch.cuda.device(a.device):
@@ -626,6 +643,7 @@ def topk_hits(topk_pred: torch.Tensor, topk_actual: torch.Tensor,
     for t in (topk_pred, topk_actual):
         if t.dtype != torch.int32 or not t.is_contiguous():
             raise ValueError("top-k tables must be contiguous int32")
+    _one_gpu(topk_pred.device, topk_pred, topk_actual)
     out = torch.empty(1, dtype=torch.int64, device=topk_pred.device)
     rate = torch.empty(1, dtype=torch.float64, device=topk_pred.device) if with_rate else None
     with torch.cuda.device(topk_pred.device):
@@ -642,7 +660,10 @@ def fold_rank_loads(counts: torch.Tensor, expert_to_rank: torch.Tensor, R: int,
         raise ValueError("counts and expert_to_rank must be int32")
     if counts.numel() != expert_to_rank.numel():
         raise ValueError("counts and expert_to_rank must have E entries each")
+    if not (counts.is_contiguous() and expert_to_rank.is_contiguous()):
+        raise ValueError("counts and expert_to_rank must be contiguous")
     dev = counts.device
+    _one_gpu(dev, counts, expert_to_rank)
     loads = torch.empty(R, dtype=torch.int32, device=dev)
     mm = torch.empty(1, dtype=torch.float64, device=dev)
     with torch.cuda.device(dev):
@@ -662,6 +683,7 @@ def fold_slot_loads(counts: torch.Tensor, slots: torch.Tensor,
     if not (counts.is_contiguous() and slots.is_contiguous()) or counts.device != slots.device:
         raise ValueError("counts and slots must be contiguous and on one device")
     dev = counts.device
+    _one_gpu(dev, counts, slots)
     R, S = slots.shape
     loads = torch.empty(R, dtype=torch.int32, device=dev)
     mm = torch.empty(1, dtype=torch.float64, device=dev)

@@ -644,3 +644,33 @@ def test_split_workspace_sizes_without_gpu():
     assert lib.fb_predict_split_workspace_bytes(32768, 256, 7168, 0) == 2048
     # a batch of 77 tokens with E = 16 (128-token tiles, H = 1024 fp32: 16 stages) splits 4 ways
     assert lib.fb_predict_split_workspace_bytes(77, 16, 1024, 1) == 2048 + 1 * 4 * 128 * 32 * 4
+
+
+def test_bindings_refuse_host_tensors():
+    """Every binding that launches a kernel refuses tensors that do not live on a GPU before
+    anything reaches the library: a host pointer would be dereferenced by the kernel."""
+    import torch
+    i32 = lambda *shape: torch.zeros(*shape, dtype=torch.int32)
+    counts, slots = i32(16), i32(8, 2)
+    with pytest.raises(ValueError):
+        fb.plan_swaps_device(counts, slots, fb.Budget(2))
+    with pytest.raises(ValueError):
+        fb.plan_swaps_timed_device(counts, slots, fb.Budget(2),
+                                   fb.CostModel([0] * 8, [1] * 16, (1, 1), (1, 1), 10))
+    with pytest.raises(ValueError):
+        fb.fold_rank_loads(counts, i32(16), 8)
+    with pytest.raises(ValueError):
+        fb.fold_slot_loads(counts, slots)
+    with pytest.raises(ValueError):
+        fb.topk_hits(i32(4, 2), i32(4, 2))
+    with pytest.raises(ValueError):
+        fb.row_cosine_mean(torch.zeros(4, 8), torch.zeros(4, 8))
+    with pytest.raises(ValueError):
+        fb.pack_router_weight(torch.zeros(16, 64))
+    with pytest.raises(ValueError):
+        fb.Predictor("cpu")
+    packed = fb.PackedRouter(torch.zeros(64, dtype=torch.uint8), 16, 64, torch.float32)
+    out = fb.Prediction(i32(16), i32(8), torch.zeros(1, dtype=torch.float64))
+    with pytest.raises(ValueError):
+        fb.predict_load_packed_noalloc(torch.zeros(4, 64), packed, fb.Scoring("softmax", 2),
+                                       i32(16), 8, out)
